@@ -1,0 +1,177 @@
+"""CPU oracle for the TokenTiming verification hot path -- TEST INFRASTRUCTURE.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may import
+this package.  The GPU library never calls it and shares no code with it.
+
+`tt_oracle.c` holds the arithmetic (plain C, fp32 where the inputs are fp32,
+exact integers elsewhere); this module builds it with gcc and wraps it with
+ctypes over numpy arrays.  See the header of `tt_oracle.c` for the paper
+passages each function follows and the readings taken where the paper is silent.
+
+Parity status: every function here is pinned by tests under `tests/`
+(test_oracle_*.py) against the paper's worked examples, closed forms,
+brute force on tiny inputs and distributional properties.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tt_oracle.c")
+_LIB = os.path.join(_HERE, "libtt_oracle.so")
+CFLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", "-std=c11",
+          "-Wall", "-Wextra", "-pthread"]
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc into oracle/libtt_oracle.so."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", *CFLAGS, _SRC, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i32, i64, f32, u64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_uint64
+        L.orc_levenshtein.argtypes = [P, ctypes.c_int, P, ctypes.c_int]
+        L.orc_levenshtein.restype = ctypes.c_int
+        L.orc_align.argtypes = [P, P, i32, i32, P, P, i32, i32, i32, P, P, P, P, i32, i32, i32,
+                                P, P, P, P, ctypes.c_int]
+        L.orc_align.restype = None
+        L.orc_transfer.argtypes = [i32, i32, P, P, P, P, P, i64, P]
+        L.orc_transfer.restype = None
+        L.orc_verify.argtypes = [i32, i32, P, P, P, P, i64, P, P, i32, P, P, P, P, P, i32,
+                                 ctypes.c_int]
+        L.orc_verify.restype = None
+        L.orc_verify_dense.argtypes = [i32, P, P, i32, f32, f32, P]
+        L.orc_verify_dense.restype = i32
+        L.orc_threshold.argtypes = [f32, u64]
+        L.orc_threshold.restype = u64
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def threads_default() -> int:
+    return max(1, len(os.sched_getaffinity(0)))
+
+
+# ------------------------------------------------------------------------------------
+def levenshtein(s: bytes, t: bytes) -> int:
+    """App. H edit distance over bytes."""
+    a = np.frombuffer(s, dtype=np.uint8) if s else np.zeros(1, np.uint8)
+    b = np.frombuffer(t, dtype=np.uint8) if t else np.zeros(1, np.uint8)
+    return int(lib().orc_levenshtein(_p(a), len(s), _p(b), len(t)))
+
+
+def align(vd_bytes, vd_off, vd_maxlen, vt_bytes, vt_off, vt_maxlen, draft_ids, draft_off,
+          target_ids, target_off, w, max_k=None, max_m=None, n_threads=None):
+    """Alg. 1 over every pair.  Returns (cost, path_len, path, map) as numpy arrays.
+
+    path is int32 [2*(sum K + sum M)]; pair b's (i, j) pairs start at
+    2*(draft_off[b] + target_off[b]).
+    """
+    vd_bytes, vt_bytes = _c(vd_bytes, np.uint8), _c(vt_bytes, np.uint8)
+    vd_off, vt_off = _c(vd_off, np.int32), _c(vt_off, np.int32)
+    draft_ids, draft_off = _c(draft_ids, np.int32), _c(draft_off, np.int32)
+    target_ids, target_off = _c(target_ids, np.int32), _c(target_off, np.int32)
+    n = len(draft_off) - 1
+    if max_k is None:
+        max_k = int(np.diff(draft_off).max()) if n else 0
+    if max_m is None:
+        max_m = int(np.diff(target_off).max()) if n else 0
+    cost = np.zeros(n, np.int32)
+    plen = np.zeros(n, np.int32)
+    path = np.full(2 * (int(draft_off[-1]) + int(target_off[-1])) + 2, -7, np.int32)
+    mp = np.full(max(1, int(target_off[-1])), -7, np.int32)
+    lib().orc_align(_p(vd_bytes), _p(vd_off), len(vd_off) - 1, vd_maxlen,
+                    _p(vt_bytes), _p(vt_off), len(vt_off) - 1, vt_maxlen,
+                    n, _p(draft_ids), _p(draft_off), _p(target_ids), _p(target_off),
+                    max_k, max_m, w, _p(cost), _p(plen), _p(path), _p(mp),
+                    n_threads or threads_default())
+    return cost, plen, path[:-2], mp[:int(target_off[-1])]
+
+
+def transfer(v_d, draft_ids, draft_off, target_off, mp, draft_probs):
+    draft_ids, draft_off = _c(draft_ids, np.int32), _c(draft_off, np.int32)
+    target_off, mp = _c(target_off, np.int32), _c(mp, np.int32)
+    assert draft_probs.dtype == np.float32 and draft_probs.flags.c_contiguous
+    q = np.zeros(max(1, int(target_off[-1])), np.float32)
+    lib().orc_transfer(len(draft_off) - 1, v_d, _p(draft_ids), _p(draft_off), _p(target_off),
+                       _p(mp), _p(draft_probs), draft_probs.shape[1], _p(q))
+    return q[:int(target_off[-1])]
+
+
+def verify(v_t, target_ids, target_off, q, target_probs, u_accept, u_sample, max_m=None,
+           residual=False, select=None, n_threads=None):
+    """Returns (n_accepted, out_token, residual or None, Z per stream as uint64)."""
+    target_ids, target_off = _c(target_ids, np.int32), _c(target_off, np.int32)
+    q, u_accept, u_sample = _c(q, np.float32), _c(u_accept, np.float32), _c(u_sample, np.float32)
+    assert target_probs.dtype == np.float32 and target_probs.flags.c_contiguous
+    n = len(target_off) - 1
+    if max_m is None:
+        max_m = int(np.diff(target_off).max()) if n else 0
+    nacc = np.full(n, -7, np.int32)
+    tok = np.full(n, -7, np.int32)
+    z = np.zeros(n, np.uint64)
+    res = np.zeros((n, target_probs.shape[1]), np.float32) if residual else None
+    sel = None if select is None else _c(select, np.int32)
+    # keep non-empty buffers alive for ctypes when arrays are empty
+    q_ = q if q.size else np.zeros(1, np.float32)
+    ua = u_accept if u_accept.size else np.zeros(1, np.float32)
+    ti = target_ids if target_ids.size else np.zeros(1, np.int32)
+    lib().orc_verify(n, v_t, _p(ti), _p(target_off), _p(q_), _p(target_probs),
+                     target_probs.shape[1], _p(ua), _p(u_sample), max_m, _p(nacc), _p(tok),
+                     _p(res), _p(z), _p(sel), 0 if sel is None else len(sel),
+                     n_threads or threads_default())
+    return nacc, tok, res, z
+
+
+def verify_dense(p, qd, x, u_accept, u_sample):
+    """Test-only: App. D Alg. 4 for one drafted position with a dense proposal."""
+    p, qd = _c(p, np.float32), _c(qd, np.float32)
+    acc = ctypes.c_int32(0)
+    tok = lib().orc_verify_dense(len(p), _p(p), _p(qd), int(x), float(u_accept), float(u_sample),
+                                 ctypes.byref(acc))
+    return int(tok), int(acc.value)
+
+
+def threshold(u: float, Z: int) -> int:
+    return int(lib().orc_threshold(float(np.float32(u)), int(Z)))
+
+
+# ------------------------------------------------------------------------------------
+def run_workload(wl, n_threads=None, residual=False, select=None):
+    """align -> transfer -> verify on a synth.Workload (probability stage included)."""
+    vd, vt = wl.vocab_d, wl.vocab_t
+    cost, plen, path, mp = align(vd.data, vd.offsets, vd.max_len, vt.data, vt.offsets, vt.max_len,
+                                 wl.draft_ids, wl.draft_off, wl.target_ids, wl.target_off, wl.w,
+                                 n_threads=n_threads)
+    out = {"cost": cost, "path_len": plen, "path": path, "map": mp}
+    if wl.draft_probs is not None:
+        q = transfer(wl.v_d, wl.draft_ids, wl.draft_off, wl.target_off, mp, wl.draft_probs)
+        nacc, tok, res, z = verify(wl.v_t, wl.verify_ids, wl.target_off, q, wl.target_probs,
+                                   wl.u_accept, wl.u_sample, residual=residual, select=select,
+                                   n_threads=n_threads)
+        out.update(q=q, n_accepted=nacc, out_token=tok, residual=res, z=z)
+    return out
