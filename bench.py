@@ -1,0 +1,290 @@
+"""Benchmark of the TokenTiming verification hot path on one MI355X.
+
+One step = tt_align + tt_transfer + tt_verify over one batch of synthetic input
+(default: 256 streams, K=8 draft tokens, V_d=128,256, V_t=151,936, w=8).  Inputs
+are resident in HBM before timing starts.  The probability rows are replicated
+(--replicas) and consecutive steps read different replicas, so the 256 MB
+Infinity Cache cannot serve a row from the previous step.
+
+Prints one JSON line: verified draft tokens/s for the step, per-kernel times, DTW
+cells/s, verify HBM GB/s against the 8 TB/s peak, and the CPU oracle timed on the
+host cores on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+# int32 VALU lane-ops: 256 CUs x 4 SIMDs x 16 lanes per cycle x 2.4 GHz
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+
+
+def band_cells(K, M, w):
+    """In-band cells per pair: |i - j| <= max(w, |K-M|) (w < 0: all K*M)."""
+    K = np.asarray(K, np.int64)
+    M = np.asarray(M, np.int64)
+    L = np.where(w < 0, np.maximum(K, M), np.maximum(w, np.abs(K - M)))
+    total = 0
+    for k, m, l in zip(K, M, L):
+        i = np.arange(1, k + 1)
+        total += int(np.maximum(0, np.minimum(m, i + l) - np.maximum(1, i - l) + 1).sum())
+    return total
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=3, help="synthetic workload 1-5")
+    ap.add_argument("--streams", type=int, default=None, help="override the stream count")
+    ap.add_argument("--w", type=int, default=8)
+    ap.add_argument("--replicas", type=int, default=4)
+    ap.add_argument("--eager", action="store_true", help="launch every call from Python (no HIP graph)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--copy-calib-mb", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--only", choices=["verify", "align", "transfer"], default=None,
+                    help="after the timed steps, loop only this call (for profiler passes)")
+    ap.add_argument("--traffic", type=str, default=None,
+                    help="JSON file with measured HBM bytes per verify launch (from counter runs)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the verification path runs per stream on a single device; "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2510_15545_amd as tt
+    from paper_2510_15545_amd import synth
+
+    tt.lib()  # fail loudly if the HIP library is not built
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    t_gen = time.time()
+    wl0 = synth.make(args.workload, n_streams=args.streams, w=args.w)
+    stage = wl0.prob if args.workload == 4 else wl0
+    t_gen = time.time() - t_gen
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    # alignment inputs (the long pairs for workload 4, the stream batch otherwise)
+    A = wl0
+    vd = tt.Vocab.from_host(A.vocab_d.data, A.vocab_d.offsets, A.vocab_d.max_len, dev)
+    vt = tt.Vocab.from_host(A.vocab_t.data, A.vocab_t.offsets, A.vocab_t.max_len, dev)
+    a_di, a_do, a_ti, a_to = t(A.draft_ids), t(A.draft_off), t(A.target_ids), t(A.target_off)
+    a_maxk, a_maxm = max(1, A.max_k), max(1, A.max_m)
+    npath = tt.path_capacity(A.draft_off[-1], A.target_off[-1])
+    a_out = tt.align(vd, vt, a_di, a_do, a_ti, a_to, args.w, a_maxk, a_maxm, n_path=npath)
+
+    S = stage
+    s_di, s_do, s_to = t(S.draft_ids), t(S.draft_off), t(S.target_off)
+    s_vi = t(S.verify_ids)
+    if args.workload == 4:  # the probability stage aligns its own short streams
+        s_out = tt.align(vd, vt, s_di, s_do, t(S.target_ids), s_to, args.w, S.max_k, S.max_m)
+    else:
+        s_out = a_out
+    R = max(1, args.replicas)
+    draft_probs = t(S.draft_probs)
+    target_probs = [t(S.target_probs)]
+    for _ in range(R - 1):
+        target_probs.append(target_probs[0].clone())
+    ua, us = t(S.u_accept), t(S.u_sample)
+    q = torch.empty(max(1, int(S.target_off[-1])), dtype=torch.float32, device=dev)
+    n = S.n
+    nacc = torch.empty(n, dtype=torch.int32, device=dev)
+    tok = torch.empty(n, dtype=torch.int32, device=dev)
+    ws = tt.verify_workspace(n, S.v_t, dev)
+    torch.cuda.synchronize()
+    host_rows_bytes = S.target_probs.nbytes
+    del wl0  # keep host memory for the CPU leg only where needed
+
+    def do_align():
+        tt.align(vd, vt, a_di, a_do, a_ti, a_to, args.w, a_maxk, a_maxm, out=a_out)
+
+    def do_transfer():
+        tt.transfer(S.v_d, s_di, s_do, s_to, s_out[3], draft_probs, out=q)
+
+    def do_verify(r):
+        tt.verify(S.v_t, s_vi, s_to, q, target_probs[r], ua, us, max(0, S.max_m), workspace=ws,
+                  out=(nacc, tok, None))
+
+    def step(r):
+        do_align()
+        if args.workload == 4:
+            tt.align(vd, vt, s_di, s_do, t_short_ids, s_to, args.w, S.max_k, S.max_m, out=s_out)
+        do_transfer()
+        do_verify(r)
+
+    t_short_ids = t(S.target_ids) if args.workload == 4 else None
+
+    for i in range(args.warmup):
+        step(i % R)
+    torch.cuda.synchronize()
+
+    graphs = None
+    if not args.eager:
+        graphs = []
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            for r in range(R):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=cap):
+                    step(r)
+                graphs.append(g)
+        torch.cuda.current_stream().wait_stream(cap)
+        for r in range(R):
+            graphs[r].replay()
+        torch.cuda.synchronize()
+
+    def run_steps(k):
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s0.record()
+        for i in range(k):
+            if graphs is not None:
+                graphs[i % R].replay()
+            else:
+                step(i % R)
+        s1.record()
+        torch.cuda.synchronize()
+        return s0.elapsed_time(s1) / k
+
+    ms_step = run_steps(args.steps)
+    ms_eager = None
+    if graphs is not None:
+        graphs_saved, graphs = graphs, None
+        ms_eager = run_steps(max(20, args.steps // 4))
+        graphs = graphs_saved
+
+    # per-kernel averages: each call alone, back to back, rotating replicas
+    def kernel_ms(fn, k):
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s0.record()
+        for i in range(k):
+            fn(i)
+        s1.record()
+        torch.cuda.synchronize()
+        return s0.elapsed_time(s1) / k
+
+    kreps = max(50, args.steps)
+    ms_verify = kernel_ms(lambda i: do_verify(i % R), kreps)
+    ms_align = kernel_ms(lambda i: do_align(), kreps)
+    ms_transfer = kernel_ms(lambda i: do_transfer(), kreps)
+    if args.only == "verify":
+        kernel_ms(lambda i: do_verify(i % R), 200)
+    elif args.only == "align":
+        kernel_ms(lambda i: do_align(), 200)
+    elif args.only == "transfer":
+        kernel_ms(lambda i: do_transfer(), 200)
+
+    if args.copy_calib_mb:
+        src = torch.empty(args.copy_calib_mb * (1 << 20) // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+
+    # ---- derived metrics
+    Ka = np.diff(A.draft_off)
+    Ma = np.diff(A.target_off)
+    cells = band_cells(Ka, Ma, args.w)
+    m_s = np.diff(S.target_off)
+    verify_bytes = int(n * 4 * S.v_t + 16 * int(m_s.sum()) + 12 * n)
+    draft_tokens = int(S.draft_off[-1])
+    gbs_verify = verify_bytes / (ms_verify * 1e-3) / 1e9
+    cells_per_s = cells / (ms_align * 1e-3)
+    acc = nacc.cpu().numpy()
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            traffic = json.load(f).get("verify_bytes_per_launch")
+
+    times = {"align": ms_align, "transfer": ms_transfer, "verify": ms_verify}
+    dominant = max(times, key=times.get)
+    if dominant == "verify":
+        roof = {"kernel": "verify_stream", "bound": "hbm", "achieved": round(gbs_verify, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs_verify / HBM_PEAK_GBS, 4),
+                "traffic": traffic, "algorithmic_bytes_per_launch": verify_bytes}
+    else:
+        roof = {"kernel": "dtw_band_wave" if dominant == "align" else "transfer_gather",
+                "bound": "alu" if dominant == "align" else "hbm",
+                "achieved": round(cells_per_s / 1e9, 3), "unit": "Gcells/s", "peak": None, "frac": None,
+                "traffic": None, "note": "see DESIGN.md for the ALU roofline of the alignment kernel"}
+
+    result = {
+        "metric": "verified draft tokens/s + DTW cells/s at V_t=151,936; verify HBM GB/s vs peak",
+        "value": round(draft_tokens / (ms_step * 1e-3), 1),
+        "unit": "draft tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "fp32+int", "data": "synthetic",
+        "config": {"workload": synth.SPECS[args.workload].name, "streams": n,
+                   "draft_tokens_per_step": draft_tokens, "target_positions": int(m_s.sum()),
+                   "v_t": S.v_t, "v_d": S.v_d, "w": args.w, "replicas": R,
+                   "launch": "eager" if graphs is None else "hip-graph"},
+        "kernels_ms": {k: round(v, 5) for k, v in times.items()},
+        "eager_ms_per_step": None if ms_eager is None else round(ms_eager, 5),
+        "dtw": {"band_cells": cells, "cells_per_s": round(cells_per_s, 1),
+                "full_cells": int((Ka * Ma).sum())},
+        "verify": {"GBps": round(gbs_verify, 1), "frac_of_peak": round(gbs_verify / HBM_PEAK_GBS, 4),
+                   "algorithmic_bytes": verify_bytes, "accept_rate": round(float(acc[acc >= 0].sum()) /
+                                                                           max(1, int(m_s.sum())), 4)},
+        "roofline": roof,
+        "gen_seconds": round(t_gen, 1),
+    }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(args, S, A, nacc, tok, s_out, a_out)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(args, S, A, nacc, tok, s_out, a_out):
+    """The oracle, unmodified, on the host cores: whole steps over the same batch,
+    repeated until about --cpu-seconds of work; also checks the GPU outputs."""
+    import oracle
+
+    threads = len(os.sched_getaffinity(0))
+    reps, t0 = 0, time.time()
+    out = None
+    while reps == 0 or (time.time() - t0 < args.cpu_seconds and reps < 50):
+        if S is not A:
+            oracle.align(A.vocab_d.data, A.vocab_d.offsets, A.vocab_d.max_len, A.vocab_t.data,
+                         A.vocab_t.offsets, A.vocab_t.max_len, A.draft_ids, A.draft_off, A.target_ids,
+                         A.target_off, args.w, n_threads=threads)
+        out = oracle.run_workload(S, n_threads=threads)
+        reps += 1
+    dt = (time.time() - t0) / reps
+    draft_tokens = int(S.draft_off[-1])
+    match = bool(np.array_equal(out["n_accepted"], nacc.cpu().numpy()) and
+                 np.array_equal(out["out_token"], tok.cpu().numpy()) and
+                 np.array_equal(out["cost"], s_out[0].cpu().numpy()))
+    return {"value": round(draft_tokens / dt, 1), "unit": "draft tokens/s", "cores": threads,
+            "kind": "oracle", "sample": f"{reps} whole steps of the benchmark batch "
+                                        f"({S.n} streams), {dt * 1e3:.1f} ms each",
+            "matches_gpu": match}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,181 @@
+/*
+ * tt.h -- TokenTiming verification hot path on AMD Instinct MI355X (gfx950).
+ *
+ * TokenTiming lets a draft model with vocabulary V_d propose tokens to a target
+ * model with a different vocabulary V_t.  Per decode step and per stream:
+ *   - the K draft tokens D are re-encoded into M proxy target tokens T with the
+ *     same bytes (Sec. 4.2.1, App. A.1; done by the caller's tokenizer);
+ *   - tt_align     Dynamic Token Warping aligns D with T (Sec. 4.1, Alg. 1) and
+ *                  maps every target position to a draft position (App. A.2);
+ *   - tt_transfer  gathers the draft probability of the aligned draft token for
+ *                  every target position (Alg. 2 "MapProbabilities", App. A.2);
+ *   - tt_verify    runs the speculative acceptance test on the target
+ *                  probabilities and samples the next token from the residual
+ *                  or bonus distribution (Sec. 3, Sec. 4.2.2-4.2.3, App. D Alg. 4).
+ *
+ * Conventions shared by every call
+ *   - Every array pointer is a DEVICE pointer owned by the caller (e.g. a torch
+ *     tensor's data_ptr()).  The library never allocates, frees or keeps them.
+ *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL is
+ *     the default stream).  Nothing synchronises the host.
+ *   - Calls return a status (TT_OK or a negative TT_E* code) and never throw.
+ *     Host-visible argument errors are reported before anything is launched.
+ *   - Errors only the device can see (a stream whose length is outside the
+ *     caller's stated bound, an id outside its vocabulary) do not fail the call:
+ *     that stream gets sentinel outputs (cost = -1, n_accepted = -1,
+ *     out_token = -1, map = -1, q = NaN) and the other streams are unaffected.
+ *   - Batches are CSR: stream b owns ids[off[b] .. off[b+1]).  Offsets are
+ *     non-decreasing int32 with off[0] = 0.
+ *   - The library holds no global state; calls on distinct workspaces are
+ *     reentrant.
+ */
+#ifndef TT_H
+#define TT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    TT_OK = 0,
+    TT_EINVAL = -1,        /* null pointer, negative size, inconsistent scalar */
+    TT_EUNSUPPORTED = -2,  /* valid request outside what the kernels implement */
+    TT_ELAUNCH = -3,       /* the HIP runtime reported an error */
+    TT_EWORKSPACE = -4     /* workspace missing or smaller than required */
+};
+
+/* Human-readable text for a status code (static storage, never NULL). */
+const char *tt_status_string(int status);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int tt_version(void);
+
+/*
+ * Token byte table (Sec. 4.1 token distance over UTF-8 bytes, App. H).
+ * Token t is bytes[offsets[t] .. offsets[t+1]).  `bytes` and `offsets` are
+ * device pointers; `offsets` has n_tokens + 1 entries.  max_token_bytes is an
+ * upper bound on every token's length (1..64); a token found longer than it on
+ * the device makes its pair a sentinel pair.
+ */
+typedef struct {
+    const uint8_t *bytes;
+    const int32_t *offsets;
+    int32_t n_tokens;
+    int32_t max_token_bytes;
+} tt_vocab;
+
+/*
+ * Workspace bytes tt_align needs for these bounds (currently always 0: the
+ * alignment keeps its whole working set in LDS).  Returns TT_EUNSUPPORTED when
+ * the bounds need more LDS than one MI355X workgroup can hold.
+ */
+int tt_align_workspace_size(int32_t n_pairs, int32_t max_k, int32_t max_m, int32_t w,
+                            int32_t max_token_bytes, size_t *bytes);
+
+/*
+ * tt_align -- Dynamic Token Warping (Sec. 4.1, Alg. 1) with the byte-level
+ * Levenshtein token distance (App. H) and the Sakoe-Chiba band |i - j| <= w,
+ * followed by the backtrack to the optimal path and the mapping of App. A.2.
+ *
+ *   vd, vt         draft / target token tables (host structs, device arrays)
+ *   n_pairs        number of (draft, proxy target) sequence pairs, >= 0
+ *   draft_ids      [sum K_b] draft token ids, CSR by draft_off[n_pairs + 1]
+ *   target_ids     [sum M_b] proxy target ids, CSR by target_off[n_pairs + 1]
+ *   max_k, max_m   bounds on K_b and M_b (1..4096); a pair with K_b or M_b
+ *                  outside [1, bound] gets sentinel outputs
+ *   w              band half-width; w < 0 means no band.  When |K_b - M_b| > w
+ *                  the band is widened to |K_b - M_b| so the corner (K_b, M_b)
+ *                  stays reachable.
+ * Outputs (device):
+ *   cost[b]        C* = C(K_b, M_b), sum of token distances along the path
+ *   path_len[b]    number of cells on the optimal path (max(K,M)..K+M-1)
+ *   path           int32 (i, j) pairs, 0-based, in forward order; pair b's
+ *                  cells start at int32 index 2*(draft_off[b] + target_off[b])
+ *                  (room for K_b + M_b cells per pair: size 2*(sum K + sum M))
+ *   map            [sum M_b]: for target position j the largest draft index i
+ *                  with (i, j) on the path (the terminal draft token of a
+ *                  many-to-one block, the shared token of a one-to-many block)
+ * Ties between equally cheap predecessors go to the diagonal step, then to
+ * (i-1, j), then to (i, j-1).
+ * workspace / workspace_bytes may be NULL / 0 (see tt_align_workspace_size).
+ */
+int tt_align(const tt_vocab *vd, const tt_vocab *vt, int32_t n_pairs,
+             const int32_t *draft_ids, const int32_t *draft_off,
+             const int32_t *target_ids, const int32_t *target_off,
+             int32_t max_k, int32_t max_m, int32_t w,
+             int32_t *cost, int32_t *path_len, int32_t *path, int32_t *map,
+             void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * tt_transfer -- draft probabilities onto target positions (Alg. 2
+ * "MapProbabilities", App. A.2 cases 1-2, Limitations: one-hot form).
+ *
+ *   q[target_off[b] + j] = draft_probs[(draft_off[b] + i) * draft_ld + d_i]
+ *   with i = map[target_off[b] + j] and d_i = draft_ids[draft_off[b] + i],
+ * i.e. the probability the draft model gave to the token it emitted at the
+ * aligned draft position.  draft_probs is fp32 with one row of width >= v_d per
+ * draft position (row stride draft_ld >= v_d elements).  i outside [0, K_b) or
+ * d_i outside [0, v_d) gives q = NaN (a NaN proposal is always rejected).
+ */
+int tt_transfer(int32_t n_pairs, int32_t v_d,
+                const int32_t *draft_ids, const int32_t *draft_off,
+                const int32_t *target_off, const int32_t *map,
+                const float *draft_probs, int64_t draft_ld,
+                float *q, void *stream);
+
+/* Workspace bytes tt_verify needs for n_streams rows of width v_t. */
+int tt_verify_workspace_size(int32_t n_streams, int32_t v_t, size_t *bytes);
+
+/*
+ * tt_verify -- lossless speculative sampling over the full target vocabulary
+ * (Sec. 3 "Standard Speculative Sampling", Sec. 4.2.2 acceptance rule,
+ * Sec. 4.2.3 / Alg. 2 next-token sample, App. D Alg. 4 residual distribution).
+ *
+ * Inputs (device):
+ *   target_ids   [sum M_b] proxy target tokens (CSR by target_off), ids index
+ *                the target rows and must lie in [0, v_t)
+ *   q            [sum M_b] transferred draft probabilities (tt_transfer)
+ *   target_probs fp32 rows of width v_t, stride target_ld >= v_t elements;
+ *                stream b owns M_b + 1 consecutive rows starting at row
+ *                target_off[b] + b: row j is the target distribution after
+ *                accepting t_1..t_j (row M_b is the bonus row)
+ *   u_accept     [sum M_b] uniforms in [0,1) for the acceptance tests
+ *   u_sample     [n_streams] uniforms in [0,1) for the final sample
+ *   max_m        bound on M_b (0..65536); a stream outside [0, max_m] or with an
+ *                id outside [0, v_t) gets sentinel outputs
+ * Outputs (device):
+ *   n_accepted[b]  gamma: t_j is accepted while u_j < P_t(t_j) / q_j (fp32,
+ *                  round-to-nearest; q_j <= 0 always accepts), stopping at the
+ *                  first rejection
+ *   out_token[b]   next token: with r = gamma, sampled from
+ *                  R(x) = max(0, P_t[r](x) - q_r [x == t_r]) if r < M_b
+ *                  (rejection), or from P_t[M_b] (all accepted).  R is clamped
+ *                  to [0,1] (NaN counts as 0), quantised to Q62 fixed point by
+ *                  truncation, Z = sum, T = floor(u_sample * Z) exactly, and the
+ *                  token is the first index whose inclusive prefix sum exceeds T.
+ *                  If Z = 0 the token is the first maximum of the row.
+ *   residual       optional (may be NULL): [n_streams x target_ld] fp32, row b
+ *                  receives R(x) / Z_f (Z_f = Z * 2^-62 rounded to fp32) for
+ *                  x < v_t, or a one-hot row at out_token when Z = 0.
+ * Rows are expected to be probability distributions (entries in [0,1], sum
+ * about 1); a row whose Q62 mass exceeds 2^64 gives an in-range but
+ * unspecified token.
+ * workspace: device memory of tt_verify_workspace_size bytes, zero-filled once
+ * before its first use; every call leaves it zero-filled again when it
+ * completes on `stream`.  Calls that overlap in time must not share it.
+ */
+int tt_verify(int32_t n_streams, int32_t v_t,
+              const int32_t *target_ids, const int32_t *target_off, const float *q,
+              const float *target_probs, int64_t target_ld,
+              const float *u_accept, const float *u_sample, int32_t max_m,
+              int32_t *n_accepted, int32_t *out_token, float *residual,
+              void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TT_H */

@@ -1,0 +1,210 @@
+"""TokenTiming verification hot path on AMD Instinct MI355X (gfx950).
+
+Thin ctypes binding over the C-ABI in include/tt.h (libtt.so, built from csrc/).
+Each function marshals torch device tensors into pointers and calls the library on
+the current HIP stream; all arithmetic happens in the HIP kernels.  Nothing here
+falls back to the CPU: if libtt.so is missing or a call fails, an exception is
+raised.
+
+    align     tt_align     Dynamic Token Warping + backtrack + mapping (Sec. 4.1, Alg. 1, App. A.2)
+    transfer  tt_transfer  draft probability of the aligned draft token (Alg. 2, App. A.2)
+    verify    tt_verify    acceptance, residual / bonus sampling (Sec. 3, 4.2.2-4.2.3, App. D Alg. 4)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = ["Vocab", "align", "transfer", "verify", "verify_workspace", "lib", "LIB_PATH",
+           "TTError", "path_capacity"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtt.so")
+
+TT_OK, TT_EINVAL, TT_EUNSUPPORTED, TT_ELAUNCH, TT_EWORKSPACE = 0, -1, -2, -3, -4
+
+
+class TTError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {lib().tt_status_string(status).decode()} (status {status})")
+
+
+class c_tt_vocab(ctypes.Structure):
+    _fields_ = [("bytes", ctypes.c_void_p), ("offsets", ctypes.c_void_p),
+                ("n_tokens", ctypes.c_int32), ("max_token_bytes", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libtt.so with argument types declared (raises if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run paper_2510_15545_amd/build.py "
+                               "(or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        VP = ctypes.POINTER(c_tt_vocab)
+        L.tt_status_string.argtypes = [ctypes.c_int]
+        L.tt_status_string.restype = ctypes.c_char_p
+        L.tt_version.argtypes = []
+        L.tt_version.restype = ctypes.c_int
+        L.tt_align_workspace_size.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(sz)]
+        L.tt_align_workspace_size.restype = ctypes.c_int
+        L.tt_align.argtypes = [VP, VP, i32, P, P, P, P, i32, i32, i32, P, P, P, P, P, sz, P]
+        L.tt_align.restype = ctypes.c_int
+        L.tt_transfer.argtypes = [i32, i32, P, P, P, P, P, i64, P, P]
+        L.tt_transfer.restype = ctypes.c_int
+        L.tt_verify_workspace_size.argtypes = [i32, i32, ctypes.POINTER(sz)]
+        L.tt_verify_workspace_size.restype = ctypes.c_int
+        L.tt_verify.argtypes = [i32, i32, P, P, P, P, i64, P, P, i32, P, P, P, P, sz, P]
+        L.tt_verify.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _torch():
+    import torch
+
+    return torch
+
+
+def _stream_handle(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t, dtype, name, allow_none=False):
+    if t is None:
+        if allow_none:
+            return None
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _check(status: int, where: str):
+    if status != TT_OK:
+        raise TTError(status, where)
+
+
+class Vocab:
+    """Token byte table on the device: token t is data[offsets[t]:offsets[t+1]]."""
+
+    def __init__(self, data, offsets, max_token_bytes: int):
+        torch = _torch()
+        self.data = data if data.numel() else torch.zeros(1, dtype=torch.uint8, device=offsets.device)
+        self.offsets = offsets
+        self.n_tokens = int(offsets.numel()) - 1
+        self.max_token_bytes = int(max_token_bytes)
+        self._c = c_tt_vocab(_ptr(self.data, torch.uint8, "vocab bytes").value,
+                             _ptr(self.offsets, torch.int32, "vocab offsets").value,
+                             self.n_tokens, self.max_token_bytes)
+
+    @classmethod
+    def from_host(cls, data, offsets, max_token_bytes: int, device="cuda"):
+        torch = _torch()
+        return cls(torch.as_tensor(data, dtype=torch.uint8).to(device),
+                   torch.as_tensor(offsets, dtype=torch.int32).to(device), max_token_bytes)
+
+
+def path_capacity(draft_off_last: int, target_off_last: int) -> int:
+    """int32 entries the path output needs: 2 * (sum K + sum M)."""
+    return 2 * (int(draft_off_last) + int(target_off_last))
+
+
+def align(vd: Vocab, vt: Vocab, draft_ids, draft_off, target_ids, target_off, w: int,
+          max_k: int, max_m: int, n_path: int | None = None, out=None, stream=None):
+    """tt_align.  Returns (cost, path_len, path, map) device tensors (int32).
+
+    n_path: length of the path buffer (2 * (sum K + sum M)); read from the CSR
+    offsets on the host if not given (one small device->host copy).
+    """
+    torch = _torch()
+    i32 = torch.int32
+    n = int(draft_off.numel()) - 1
+    dev = draft_off.device
+    if out is None:
+        if n_path is None:
+            n_path = path_capacity(draft_off[-1].item(), target_off[-1].item())
+        m_total = int(target_ids.numel())
+        out = (torch.empty(n, dtype=i32, device=dev), torch.empty(n, dtype=i32, device=dev),
+               torch.empty(max(1, n_path), dtype=i32, device=dev),
+               torch.empty(max(1, m_total), dtype=i32, device=dev))
+    cost, plen, path, mp = out
+    di = draft_ids if draft_ids.numel() else torch.zeros(1, dtype=i32, device=dev)
+    ti = target_ids if target_ids.numel() else torch.zeros(1, dtype=i32, device=dev)
+    st = lib().tt_align(ctypes.byref(vd._c), ctypes.byref(vt._c), n,
+                        _ptr(di, i32, "draft_ids"), _ptr(draft_off, i32, "draft_off"),
+                        _ptr(ti, i32, "target_ids"), _ptr(target_off, i32, "target_off"),
+                        int(max_k), int(max_m), int(w),
+                        _ptr(cost, i32, "cost"), _ptr(plen, i32, "path_len"),
+                        _ptr(path, i32, "path"), _ptr(mp, i32, "map"), None, 0, _stream_handle(stream))
+    _check(st, "tt_align")
+    return out
+
+
+def transfer(v_d: int, draft_ids, draft_off, target_off, mp, draft_probs, out=None, stream=None):
+    """tt_transfer.  Returns q (float32, one per target position)."""
+    torch = _torch()
+    i32 = torch.int32
+    n = int(draft_off.numel()) - 1
+    if draft_probs.dim() != 2 or draft_probs.stride(1) != 1:
+        raise ValueError("draft_probs must be a 2-D row-major tensor")
+    if draft_probs.dtype != torch.float32 or not draft_probs.is_cuda:
+        raise ValueError("draft_probs must be a float32 device tensor")
+    if out is None:
+        out = torch.empty(max(1, int(mp.numel())), dtype=torch.float32, device=mp.device)
+    st = lib().tt_transfer(n, int(v_d), _ptr(draft_ids, i32, "draft_ids"), _ptr(draft_off, i32, "draft_off"),
+                           _ptr(target_off, i32, "target_off"), _ptr(mp, i32, "map"),
+                           ctypes.c_void_p(draft_probs.data_ptr()),
+                           int(draft_probs.stride(0)), _ptr(out, torch.float32, "q"), _stream_handle(stream))
+    _check(st, "tt_transfer")
+    return out
+
+
+def verify_workspace(n_streams: int, v_t: int, device="cuda"):
+    """A zero-filled workspace for tt_verify (reusable across calls on one stream)."""
+    torch = _torch()
+    n = ctypes.c_size_t(0)
+    _check(lib().tt_verify_workspace_size(int(n_streams), int(v_t), ctypes.byref(n)),
+           "tt_verify_workspace_size")
+    return torch.zeros(max(1, n.value), dtype=torch.uint8, device=device)
+
+
+def verify(v_t: int, target_ids, target_off, q, target_probs, u_accept, u_sample, max_m: int,
+           workspace=None, residual: bool = False, out=None, stream=None):
+    """tt_verify.  Returns (n_accepted, out_token, residual or None)."""
+    torch = _torch()
+    i32, f32 = torch.int32, torch.float32
+    n = int(target_off.numel()) - 1
+    dev = target_off.device
+    if target_probs.dim() != 2 or target_probs.stride(1) != 1:
+        raise ValueError("target_probs must be a 2-D row-major tensor")
+    if workspace is None:
+        workspace = verify_workspace(n, v_t, dev)
+    if out is None:
+        out = (torch.empty(n, dtype=i32, device=dev), torch.empty(n, dtype=i32, device=dev),
+               torch.zeros((n, target_probs.stride(0)), dtype=f32, device=dev) if residual else None)
+    nacc, tok, res = out
+    ti = target_ids if target_ids.numel() else torch.zeros(1, dtype=i32, device=dev)
+    qq = q if q.numel() else torch.zeros(1, dtype=f32, device=dev)
+    ua = u_accept if u_accept.numel() else torch.zeros(1, dtype=f32, device=dev)
+    if target_probs.dtype != f32 or not target_probs.is_cuda:
+        raise ValueError("target_probs must be a float32 device tensor")
+    st = lib().tt_verify(n, int(v_t), _ptr(ti, i32, "target_ids"), _ptr(target_off, i32, "target_off"),
+                         _ptr(qq, f32, "q"), ctypes.c_void_p(target_probs.data_ptr()),
+                         int(target_probs.stride(0)), _ptr(ua, f32, "u_accept"),
+                         _ptr(u_sample, f32, "u_sample"), int(max_m), _ptr(nacc, i32, "n_accepted"),
+                         _ptr(tok, i32, "out_token"), _ptr(res, f32, "residual", allow_none=True),
+                         ctypes.c_void_p(workspace.data_ptr()), int(workspace.numel()), _stream_handle(stream))
+    _check(st, "tt_verify")
+    return out

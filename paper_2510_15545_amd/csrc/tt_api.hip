@@ -1,0 +1,129 @@
+// C-ABI of the library: argument validation, workspace sizing and launches.
+// Every entry point returns a status and never throws; nothing is launched when a
+// host-visible argument is invalid.
+#include "tt_internal.h"
+
+namespace {
+
+constexpr int32_t kMaxAlignLen = 4096;   // bound on K_b / M_b accepted by tt_align
+constexpr int32_t kMaxVerifyLen = 65536; // bound on M_b accepted by tt_verify
+
+bool vocab_ok(const tt_vocab *v) {
+    return v != nullptr && v->bytes != nullptr && v->offsets != nullptr && v->n_tokens >= 1 &&
+           v->max_token_bytes >= 1;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *tt_status_string(int status) {
+    switch (status) {
+        case TT_OK: return "ok";
+        case TT_EINVAL: return "invalid argument";
+        case TT_EUNSUPPORTED: return "unsupported configuration";
+        case TT_ELAUNCH: return "HIP launch or runtime error";
+        case TT_EWORKSPACE: return "workspace missing or too small";
+        default: return "unknown status";
+    }
+}
+
+int tt_version(void) { return 100; }
+
+int tt_align_workspace_size(int32_t n_pairs, int32_t max_k, int32_t max_m, int32_t w,
+                            int32_t max_token_bytes, size_t *bytes) {
+    if (bytes == nullptr || n_pairs < 0 || max_k < 1 || max_m < 1 || max_k > kMaxAlignLen ||
+        max_m > kMaxAlignLen || max_token_bytes < 1)
+        return TT_EINVAL;
+    const int tb = tt::align_token_slot(max_token_bytes);
+    if (tb == 0 || tt::align_lds_bytes(max_k, max_m, w, tb) == 0) return TT_EUNSUPPORTED;
+    *bytes = 0;
+    return TT_OK;
+}
+
+int tt_align(const tt_vocab *vd, const tt_vocab *vt, int32_t n_pairs, const int32_t *draft_ids,
+             const int32_t *draft_off, const int32_t *target_ids, const int32_t *target_off,
+             int32_t max_k, int32_t max_m, int32_t w, int32_t *cost, int32_t *path_len, int32_t *path,
+             int32_t *map, void *workspace, size_t workspace_bytes, void *stream) {
+    (void)workspace;
+    (void)workspace_bytes;
+    if (!vocab_ok(vd) || !vocab_ok(vt) || n_pairs < 0) return TT_EINVAL;
+    if (max_k < 1 || max_m < 1 || max_k > kMaxAlignLen || max_m > kMaxAlignLen) return TT_EINVAL;
+    if (n_pairs == 0) return TT_OK;
+    if (!draft_ids || !draft_off || !target_ids || !target_off || !cost || !path_len || !path || !map)
+        return TT_EINVAL;
+    const int32_t mt = vd->max_token_bytes > vt->max_token_bytes ? vd->max_token_bytes : vt->max_token_bytes;
+    const int tb = tt::align_token_slot(mt);
+    if (tb == 0 || tt::align_lds_bytes(max_k, max_m, w, tb) == 0) return TT_EUNSUPPORTED;
+    tt::AlignArgs a;
+    a.vd = *vd;
+    a.vt = *vt;
+    a.n_pairs = n_pairs;
+    a.draft_ids = draft_ids;
+    a.draft_off = draft_off;
+    a.target_ids = target_ids;
+    a.target_off = target_off;
+    a.max_k = max_k;
+    a.max_m = max_m;
+    a.w = w;
+    a.cost = cost;
+    a.path_len = path_len;
+    a.path = path;
+    a.map = map;
+    return tt::launch_align(a, static_cast<hipStream_t>(stream));
+}
+
+int tt_transfer(int32_t n_pairs, int32_t v_d, const int32_t *draft_ids, const int32_t *draft_off,
+                const int32_t *target_off, const int32_t *map, const float *draft_probs, int64_t draft_ld,
+                float *q, void *stream) {
+    if (n_pairs < 0 || v_d < 1 || draft_ld < v_d) return TT_EINVAL;
+    if (n_pairs == 0) return TT_OK;
+    if (!draft_ids || !draft_off || !target_off || !map || !draft_probs || !q) return TT_EINVAL;
+    tt::TransferArgs a;
+    a.n_pairs = n_pairs;
+    a.v_d = v_d;
+    a.draft_ids = draft_ids;
+    a.draft_off = draft_off;
+    a.target_off = target_off;
+    a.map = map;
+    a.draft_probs = draft_probs;
+    a.draft_ld = draft_ld;
+    a.q = q;
+    return tt::launch_transfer(a, static_cast<hipStream_t>(stream));
+}
+
+int tt_verify_workspace_size(int32_t n_streams, int32_t v_t, size_t *bytes) {
+    if (bytes == nullptr || n_streams < 0 || v_t < 1) return TT_EINVAL;
+    *bytes = tt::verify_layout(n_streams, v_t).total;
+    return TT_OK;
+}
+
+int tt_verify(int32_t n_streams, int32_t v_t, const int32_t *target_ids, const int32_t *target_off,
+              const float *q, const float *target_probs, int64_t target_ld, const float *u_accept,
+              const float *u_sample, int32_t max_m, int32_t *n_accepted, int32_t *out_token,
+              float *residual, void *workspace, size_t workspace_bytes, void *stream) {
+    if (n_streams < 0 || v_t < 1 || target_ld < v_t || max_m < 0 || max_m > kMaxVerifyLen) return TT_EINVAL;
+    if (n_streams == 0) return TT_OK;
+    if (!target_ids || !target_off || !q || !target_probs || !u_accept || !u_sample || !n_accepted ||
+        !out_token)
+        return TT_EINVAL;
+    tt::VerifyArgs a;
+    a.n_streams = n_streams;
+    a.v_t = v_t;
+    a.target_ids = target_ids;
+    a.target_off = target_off;
+    a.q = q;
+    a.target_probs = target_probs;
+    a.target_ld = target_ld;
+    a.u_accept = u_accept;
+    a.u_sample = u_sample;
+    a.max_m = max_m;
+    a.n_accepted = n_accepted;
+    a.out_token = out_token;
+    a.residual = residual;
+    a.workspace = workspace;
+    a.workspace_bytes = workspace_bytes;
+    return tt::launch_verify(a, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,60 @@
+// Internal declarations shared by the library's translation units (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "tt.h"
+
+namespace tt {
+
+// ---------------------------------------------------------------- alignment (dtw.hip)
+struct AlignArgs {
+    tt_vocab vd, vt;
+    int32_t n_pairs;
+    const int32_t *draft_ids, *draft_off, *target_ids, *target_off;
+    int32_t max_k, max_m, w;
+    int32_t *cost, *path_len, *path, *map;
+};
+
+// LDS bytes one alignment workgroup needs for these bounds; 0 if they exceed the
+// per-workgroup LDS of gfx950.  `tb` is the token slot width chosen for the vocabularies.
+size_t align_lds_bytes(int32_t max_k, int32_t max_m, int32_t w, int tb);
+int align_token_slot(int32_t max_token_bytes);  // 8, 16, 32 or 64; 0 if unsupported
+int launch_align(const AlignArgs &a, hipStream_t stream);
+
+// ---------------------------------------------------------------- transfer (transfer.hip)
+struct TransferArgs {
+    int32_t n_pairs, v_d;
+    const int32_t *draft_ids, *draft_off, *target_off, *map;
+    const float *draft_probs;
+    int64_t draft_ld;
+    float *q;
+};
+int launch_transfer(const TransferArgs &a, hipStream_t stream);
+
+// ---------------------------------------------------------------- verify (verify.hip)
+struct VerifyArgs {
+    int32_t n_streams, v_t;
+    const int32_t *target_ids, *target_off;
+    const float *q, *target_probs;
+    int64_t target_ld;
+    const float *u_accept, *u_sample;
+    int32_t max_m;
+    int32_t *n_accepted, *out_token;
+    float *residual;
+    void *workspace;
+    size_t workspace_bytes;
+};
+
+// Workspace layout for tt_verify.
+struct VerifyLayout {
+    size_t counters, zsum, rsel, partials, total;
+    int32_t n_chunks;
+};
+VerifyLayout verify_layout(int32_t n_streams, int32_t v_t);
+int launch_verify(const VerifyArgs &a, hipStream_t stream);
+
+}  // namespace tt

@@ -1,0 +1,78 @@
+"""The C-ABI library: loads on a host without a GPU, exports every declared symbol,
+and rejects host-visible argument errors before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2510_15545_amd as tt
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "tt.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tt_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert {"tt_align", "tt_transfer", "tt_verify", "tt_status_string"} <= set(names)
+    lib = ctypes.CDLL(tt.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version():
+    L = tt.lib()
+    for code in (0, -1, -2, -3, -4, 7):
+        assert L.tt_status_string(code)
+    assert L.tt_version() >= 100
+
+
+def test_workspace_sizes_are_host_computed():
+    L = tt.lib()
+    n = ctypes.c_size_t(0)
+    assert L.tt_verify_workspace_size(256, 151936, ctypes.byref(n)) == 0
+    # counters + Q62 sums + gamma, and one Q62 sum per 1024-float chunk per stream
+    assert n.value >= 256 * (4 + 8 + 4) + 256 * 149 * 8
+    assert L.tt_verify_workspace_size(-1, 10, ctypes.byref(n)) == tt.TT_EINVAL
+    assert L.tt_align_workspace_size(1024, 512, 512, 8, 8, ctypes.byref(n)) == 0 and n.value == 0
+    assert L.tt_align_workspace_size(8, 4096, 4096, -1, 8, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
+    assert L.tt_align_workspace_size(8, 16, 16, 8, 65, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
+
+
+def test_invalid_arguments_return_before_launch():
+    L = tt.lib()
+    P = ctypes.c_void_p
+    dummy = P(0x1000)  # never dereferenced: every call below fails validation first
+    v = tt.c_tt_vocab(0x1000, 0x1000, 10, 8)
+    assert L.tt_align(None, ctypes.byref(v), 1, dummy, dummy, dummy, dummy, 4, 4, 8,
+                      dummy, dummy, dummy, dummy, None, 0, None) == tt.TT_EINVAL
+    assert L.tt_align(ctypes.byref(v), ctypes.byref(v), -1, dummy, dummy, dummy, dummy, 4, 4, 8,
+                      dummy, dummy, dummy, dummy, None, 0, None) == tt.TT_EINVAL
+    big = tt.c_tt_vocab(0x1000, 0x1000, 10, 65)
+    assert L.tt_align(ctypes.byref(big), ctypes.byref(v), 1, dummy, dummy, dummy, dummy, 4, 4, 8,
+                      dummy, dummy, dummy, dummy, None, 0, None) == tt.TT_EUNSUPPORTED
+    assert L.tt_align(ctypes.byref(v), ctypes.byref(v), 1, None, dummy, dummy, dummy, 4, 4, 8,
+                      dummy, dummy, dummy, dummy, None, 0, None) == tt.TT_EINVAL
+    assert L.tt_align(ctypes.byref(v), ctypes.byref(v), 0, None, None, None, None, 4, 4, 8,
+                      None, None, None, None, None, 0, None) == tt.TT_OK  # empty batch
+    assert L.tt_transfer(1, 10, dummy, dummy, dummy, dummy, dummy, 5, dummy, None) == tt.TT_EINVAL
+    assert L.tt_transfer(1, 10, dummy, None, dummy, dummy, dummy, 10, dummy, None) == tt.TT_EINVAL
+    assert L.tt_verify(1, 10, dummy, dummy, dummy, dummy, 9, dummy, dummy, 4, dummy, dummy, None,
+                       dummy, 1 << 20, None) == tt.TT_EINVAL  # ld < v_t
+    assert L.tt_verify(1, 10, dummy, dummy, dummy, dummy, 10, dummy, dummy, -1, dummy, dummy, None,
+                       dummy, 1 << 20, None) == tt.TT_EINVAL
+    assert L.tt_verify(1, 10, dummy, dummy, dummy, dummy, 10, dummy, dummy, 4, dummy, dummy, None,
+                       dummy, 0, None) == tt.TT_EWORKSPACE
+    assert L.tt_verify(1, 10, None, dummy, dummy, dummy, 10, dummy, dummy, 4, dummy, dummy, None,
+                       dummy, 1 << 20, None) == tt.TT_EINVAL
+
+
+def test_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    with pytest.raises(ValueError):
+        tt._ptr(torch.zeros(3, dtype=torch.int32), torch.int32, "x")

@@ -1,0 +1,176 @@
+"""GPU edge cases, each compared with the oracle (or with the documented sentinel)."""
+import numpy as np
+import pytest
+
+from gpu_util import compare_align, compare_verify, gpu_run, oracle_run, to_dev
+from paper_2510_15545_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def vocab_of(tokens):
+    tokens = list(tokens)
+    off = np.zeros(len(tokens) + 1, np.int32)
+    off[1:] = np.cumsum([len(t) for t in tokens])
+    data = np.frombuffer(b"".join(tokens), np.uint8).copy()
+    return synth.Vocab(tokens, {t: i for i, t in enumerate(tokens)}, data, off,
+                       max([len(t) for t in tokens]))
+
+
+def workload(vd, vt, pairs, v_d, v_t, w=8, seed=0, probs=True):
+    def csr(lists):
+        off = np.zeros(len(lists) + 1, np.int32)
+        off[1:] = np.cumsum([len(l) for l in lists])
+        return np.array([x for l in lists for x in l], np.int32), off
+
+    di, do = csr([p[0] for p in pairs])
+    ti, to = csr([p[1] for p in pairs])
+    spec = synth.Spec(0, "edge", len(pairs), 0, v_d, v_t, b"", 64, None, w)
+    wl = synth.Workload(spec, vd, vt, di, do, ti, to, w, v_d=v_d, v_t=v_t, verify_ids=ti)
+    if probs:
+        rng = np.random.default_rng(seed)
+        n = len(pairs)
+
+        def rows(k, width):
+            x = rng.standard_normal((k, width)).astype(np.float32) * np.float32(2)
+            e = np.exp(x - x.max(axis=1, keepdims=True)).astype(np.float32)
+            return (e / e.sum(axis=1, keepdims=True, dtype=np.float32)).astype(np.float32)
+
+        wl.draft_probs = rows(int(do[-1]), v_d)
+        wl.target_probs = rows(int(to[-1]) + n, v_t)
+        wl.u_accept = (rng.integers(0, 1 << 24, int(to[-1])) * 2.0**-24).astype(np.float32)
+        wl.u_sample = (rng.integers(0, 1 << 24, n) * 2.0**-24).astype(np.float32)
+    return wl
+
+
+def random_tokens(rng, n, lo, hi, alphabet=b"abcdefgh"):
+    out = set()
+    alpha = np.frombuffer(alphabet, np.uint8)
+    while len(out) < n:
+        ln = int(rng.integers(lo, hi + 1))
+        out.add(alpha[rng.integers(0, len(alpha), ln)].tobytes())
+    return sorted(out)
+
+
+@pytest.mark.parametrize("maxlen", [8, 16, 32, 64])
+def test_token_slot_widths(maxlen):
+    """Every token-width instantiation (8/16/32/64-byte slots) against the oracle."""
+    print(f"[case] token slots maxlen={maxlen}", flush=True)
+    rng = np.random.default_rng(maxlen)
+    toks_d = random_tokens(rng, 300, 1, maxlen, bytes(range(0x20, 0x7F)) + b"\x00\xc3\xa9")
+    toks_t = random_tokens(rng, 400, 1, maxlen, bytes(range(0x20, 0x7F)) + b"\x00\xc3\xa9")
+    vd, vt = vocab_of(toks_d), vocab_of(toks_t)
+    pairs = [(list(rng.integers(0, len(toks_d), rng.integers(1, 40))),
+              list(rng.integers(0, len(toks_t), rng.integers(1, 40)))) for _ in range(40)]
+    wl = workload(vd, vt, pairs, len(toks_d), len(toks_t))
+    for w in (8, -1, 3):
+        g, o = gpu_run(wl, w=w), oracle_run(wl, w=w)
+        compare_align(wl, g, o)
+        compare_verify(g, o)
+
+
+def test_strips_longer_than_a_wave():
+    """K and M well above 64 rows, every w in the paper's sweep (strip boundaries, band widening)."""
+    rng = np.random.default_rng(5)
+    toks = random_tokens(rng, 200, 1, 4)
+    v = vocab_of(toks)
+    pairs = []
+    for k, m in ((65, 64), (64, 65), (130, 129), (200, 60), (60, 200), (128, 128), (1, 300), (300, 1)):
+        pairs.append((list(rng.integers(0, len(toks), k)), list(rng.integers(0, len(toks), m))))
+    wl = workload(v, v, pairs, len(toks), len(toks), probs=False)
+    for w in (4, 8, 16, -1, 0, 70):
+        print(f"[case] strips w={w}", flush=True)
+        compare_align(wl, gpu_run(wl, w=w), oracle_run(wl, w=w))
+
+
+def test_sentinel_pairs_and_streams():
+    rng = np.random.default_rng(6)
+    toks = random_tokens(rng, 50, 1, 5)
+    v = vocab_of(toks)
+    pairs = [([1, 2, 3], [4, 5]), ([1, 999], [3]), ([2, 3], [4, -1]), ([5], [6, 7, 8])]
+    wl = workload(v, v, pairs, len(toks), len(toks))
+    wl.verify_ids = wl.target_ids.copy()
+    wl.verify_ids[wl.target_off[2] + 1] = 10**6  # out of range for verify as well
+    g, o = gpu_run(wl), oracle_run(wl)
+    compare_align(wl, g, o)
+    assert list(g["cost"][1:3]) == [-1, -1] and list(g["map"][wl.target_off[1]:wl.target_off[3]]) == [-1] * 3
+    compare_verify(g, o)
+    assert int(g["n_accepted"][2]) == -1 and int(g["out_token"][2]) == -1
+
+
+def test_bounds_smaller_than_pairs_give_sentinels():
+    import paper_2510_15545_amd as tt
+
+    rng = np.random.default_rng(7)
+    toks = random_tokens(rng, 50, 1, 5)
+    v = vocab_of(toks)
+    pairs = [([1, 2, 3], [4, 5]), ([1, 2, 3, 4, 5, 6], [3]), ([2], [4, 5, 6, 7, 8, 9])]
+    wl = workload(v, v, pairs, len(toks), len(toks), probs=False)
+    from gpu_util import upload
+
+    d = upload(wl)
+    cost, plen, path, mp = tt.align(d["vd"], d["vt"], d["draft_ids"], d["draft_off"], d["target_ids"],
+                                    d["target_off"], 8, 4, 4)
+    cost = cost.cpu().numpy()
+    assert cost[0] >= 0 and cost[1] == -1 and cost[2] == -1
+    assert list(mp.cpu().numpy()[wl.target_off[2]:]) == [-1] * 6
+
+
+def test_verify_edge_values():
+    """M = 0 streams, q = 0 / NaN, u at the ends of [0,1), a zero-mass residual, rows not 16-B aligned."""
+    import torch
+    import oracle
+    import paper_2510_15545_amd as tt
+
+    V, ld = 3001, 3003  # ragged tail, ld % 4 != 0 -> scalar loads
+    rng = np.random.default_rng(8)
+    n = 7
+    Ms = [0, 1, 2, 3, 1, 2, 1]
+    off = np.zeros(n + 1, np.int32)
+    off[1:] = np.cumsum(Ms)
+    ids = rng.integers(0, V, int(off[-1])).astype(np.int32)
+    rows = rng.random((int(off[-1]) + n, ld)).astype(np.float32)
+    rows /= rows[:, :V].sum(axis=1, keepdims=True, dtype=np.float32)
+    q = rng.random(int(off[-1])).astype(np.float32)
+    ua = (rng.integers(0, 1 << 24, int(off[-1])) * 2.0**-24).astype(np.float32)
+    us = (rng.integers(0, 1 << 24, n) * 2.0**-24).astype(np.float32)
+    q[off[1]] = 0.0             # stream 1: q = 0 -> accepted
+    q[off[2]] = np.nan          # stream 2: NaN proposal -> rejected
+    us[3] = 0.0
+    us[4] = np.float32(1 - 2**-24)
+    # stream 5: the residual is empty (all mass on the rejected proposal, q > 1)
+    r5 = off[5] + 5
+    rows[r5, :] = 0.0
+    rows[r5, ids[off[5]]] = 1.0
+    q[off[5]] = 2.0
+    ua[off[5]] = 0.9
+    # stream 6: NaN and negative entries in the bonus row, q tiny -> accepted
+    q[off[6]] = 1e-30
+    rows[off[6] + 6 + 1, 5] = np.nan
+    rows[off[6] + 6 + 1, 6] = -0.5
+    rows_c = np.ascontiguousarray(rows)
+    o_nacc, o_tok, o_res, _ = oracle.verify(V, ids, off, q, rows_c, ua, us, residual=True)
+    dev = {k: to_dev(v) for k, v in dict(ids=ids, off=off, q=q, ua=ua, us=us).items()}
+    P = to_dev(rows_c)
+    nacc, tok, res = tt.verify(V, dev["ids"], dev["off"], dev["q"], P, dev["ua"], dev["us"], 3, residual=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(nacc.cpu().numpy(), o_nacc)
+    assert np.array_equal(tok.cpu().numpy(), o_tok)
+    r = res.cpu().numpy()[:, :V]
+    ro = o_res[:, :V]
+    assert np.all(np.abs(r.astype(np.float64) - ro) <= 1e-6 * np.abs(ro))
+    assert int(o_tok[5]) == int(ids[off[5]])  # zero-mass fallback = first argmax
+
+
+def test_empty_batch_and_argument_errors():
+    import torch
+    import paper_2510_15545_amd as tt
+
+    e = torch.zeros(1, dtype=torch.int32, device="cuda")
+    off = torch.zeros(1, dtype=torch.int32, device="cuda")
+    P = torch.zeros((1, 8), dtype=torch.float32, device="cuda")
+    f = torch.zeros(1, dtype=torch.float32, device="cuda")
+    nacc, tok, _ = tt.verify(8, e, off, f, P, f, f, 0)
+    assert nacc.numel() == 0 and tok.numel() == 0
+    with pytest.raises(tt.TTError):
+        tt.verify(8, e, torch.zeros(2, dtype=torch.int32, device="cuda"), f, P, f, f, -1)
