@@ -163,9 +163,11 @@ int tt_verify_workspace_size(int32_t n_streams, int32_t v_t, size_t *bytes);
  * Rows are expected to be probability distributions (entries in [0,1], sum
  * about 1); a row whose Q62 mass exceeds 2^64 gives an in-range but
  * unspecified token.
- * workspace: device memory of tt_verify_workspace_size bytes, zero-filled once
- * before its first use; every call leaves it zero-filled again when it
- * completes on `stream`.  Calls that overlap in time must not share it.
+ * workspace: device memory of tt_verify_workspace_size bytes (per-chunk Q62
+ * sums and per-stream scratch); it needs no initialisation.  Calls that overlap
+ * in time must not share it.
+ * Launches: one streaming kernel over B x S workgroups, one sampling kernel over
+ * B workgroups, and (if residual != NULL) one kernel writing the residual rows.
  */
 int tt_verify(int32_t n_streams, int32_t v_t,
               const int32_t *target_ids, const int32_t *target_off, const float *q,

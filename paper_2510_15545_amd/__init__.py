@@ -172,7 +172,7 @@ def transfer(v_d: int, draft_ids, draft_off, target_off, mp, draft_probs, out=No
 
 
 def verify_workspace(n_streams: int, v_t: int, device="cuda"):
-    """A zero-filled workspace for tt_verify (reusable across calls on one stream)."""
+    """A workspace for tt_verify (reusable by calls that do not overlap in time)."""
     torch = _torch()
     n = ctypes.c_size_t(0)
     _check(lib().tt_verify_workspace_size(int(n_streams), int(v_t), ctypes.byref(n)),

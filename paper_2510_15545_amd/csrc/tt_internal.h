@@ -51,7 +51,7 @@ struct VerifyArgs {
 
 // Workspace layout for tt_verify.
 struct VerifyLayout {
-    size_t counters, zsum, rsel, partials, total;
+    size_t zsum, rsel, partials, total;
     int32_t n_chunks;
 };
 VerifyLayout verify_layout(int32_t n_streams, int32_t v_t);

@@ -7,18 +7,24 @@
 //
 // The row of stream b is read once from HBM.  It is cut into chunks of 1024 floats
 // (one wave, 16 floats per lane, 16-byte loads).  Each chunk's residual mass is
-// accumulated in exact Q62 fixed point (R quantised by truncation), so the chunk sums
-// and their prefix are independent of summation order and the sampled token is
-// bit-identical to a sequential scan.  A stream's chunks are split over `splits`
-// workgroups; each publishes its chunk sums, then bumps the stream's arrival
-// counter.  The last workgroup to arrive forms Z and T = floor(u * Z) exactly,
-// finds the chunk whose prefix crosses T, re-reads that one chunk (4 KiB, normally
-// in the XCD's L2: all workgroups of a stream are placed on one XCD)
-// and scans it to the crossing index.
+// accumulated in exact Q62 fixed point (R quantised by truncation), so chunk sums and
+// their prefix are independent of summation order and the sampled token is
+// bit-identical to a sequential scan.
+//
+// Two kernels, ordered by the stream:
+//   verify_stream  grid B x S: every workgroup of stream b recomputes gamma_b (M_b
+//                  scalar gathers), then streams its share of row gamma_b and stores one
+//                  Q62 sum per chunk.  Split 0 records gamma_b.
+//   verify_sample  grid B: forms Z and T = floor(u * Z) exactly, scans the chunk sums to
+//                  the crossing chunk, re-reads that one chunk (4 KiB) and scans it to the
+//                  crossing index.
+// The kernel boundary publishes the chunk sums; an in-kernel hand-off between
+// workgroups would need agent-scope fences, which on gfx950 write back and invalidate
+// the whole L2 of an XCD.
 //
 // Workgroup id -> (stream, split) is XCD-aware: the hardware deals workgroup ids
 // round-robin over the 8 XCDs, so XCD x receives the contiguous work range
-// [x * G/8, (x+1) * G/8) and a stream's splits share that XCD's L2.
+// [x * G/8, (x+1) * G/8) and a stream's splits share one XCD.
 #include <climits>
 #include <cmath>
 
@@ -36,7 +42,6 @@ constexpr int kTargetWorkgroups = 2048;
 
 struct VParams {
     VerifyArgs a;
-    uint32_t *counters;
     uint64_t *zsum;
     int32_t *rsel;
     uint64_t *partials;
@@ -146,11 +151,7 @@ __global__ void __launch_bounds__(kThreads) verify_stream(VParams p) {
     const int b = work / p.splits, s = work % p.splits;
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
 
-    __shared__ int sh_gamma, sh_ok, sh_last, sh_chunk, sh_tok;
-    __shared__ uint64_t sh_base;
-    __shared__ uint64_t sh_scan[kWaves];
-    __shared__ float sh_av[kThreads];
-    __shared__ int sh_ai[kThreads];
+    __shared__ int sh_gamma, sh_ok;
 
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
@@ -192,10 +193,12 @@ __global__ void __launch_bounds__(kThreads) verify_stream(VParams p) {
         if (s == 0 && tid == 0) {
             a.n_accepted[b] = -1;
             a.out_token[b] = -1;
+            p.rsel[b] = -1;
         }
         return;
     }
     const int r = sh_gamma;
+    if (s == 0 && tid == 0) p.rsel[b] = r;
     const int vt = a.v_t;
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
     const int rtok = r < M ? a.target_ids[t0 + r] : -1;
@@ -235,17 +238,27 @@ __global__ void __launch_bounds__(kThreads) verify_stream(VParams p) {
         }
     }
 
-    // ---- phase C: arrival; the last workgroup of the stream samples
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-        const uint32_t prev = atomicAdd(&p.counters[b], 1u);
-        sh_last = (prev == (uint32_t)(p.splits - 1)) ? 1 : 0;
-        __threadfence();
-    }
-    __syncthreads();
-    if (!sh_last) return;
-    __threadfence();
+}
+
+// One workgroup per stream: exact threshold, crossing chunk, crossing index.
+__global__ void __launch_bounds__(kThreads) verify_sample(VParams p) {
+    const VerifyArgs &a = p.a;
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int r = p.rsel[b];
+    if (r < 0) return;  // sentinel stream, outputs already written
+    __shared__ int sh_chunk, sh_tok;
+    __shared__ uint64_t sh_base;
+    __shared__ uint64_t sh_scan[kWaves];
+    __shared__ float sh_av[kThreads];
+    __shared__ int sh_ai[kThreads];
+
+    const int t0 = a.target_off[b];
+    const int M = a.target_off[b + 1] - t0;
+    const int vt = a.v_t;
+    const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
+    const int rtok = r < M ? a.target_ids[t0 + r] : -1;
+    const float rq = r < M ? a.q[t0 + r] : 0.0f;
 
     const int nc = p.nc;
     const uint64_t *part = p.partials + (int64_t)b * nc;
@@ -307,8 +320,6 @@ __global__ void __launch_bounds__(kThreads) verify_stream(VParams p) {
         a.n_accepted[b] = r;
         a.out_token[b] = token;
         p.zsum[b] = Z;
-        p.rsel[b] = r;
-        p.counters[b] = 0u;
     }
 }
 
@@ -348,8 +359,6 @@ VerifyLayout verify_layout(int32_t n_streams, int32_t v_t) {
     const size_t n = n_streams > 0 ? (size_t)n_streams : 0;
     L.n_chunks = v_t > 0 ? (int32_t)((v_t + kChunk - 1) / kChunk) : 0;
     size_t off = 0;
-    L.counters = off;
-    off = align256(off + 4 * n);
     L.zsum = off;
     off = align256(off + 8 * n);
     L.rsel = off;
@@ -366,7 +375,6 @@ int launch_verify(const VerifyArgs &a, hipStream_t stream) {
     uint8_t *ws = static_cast<uint8_t *>(a.workspace);
     VParams p;
     p.a = a;
-    p.counters = reinterpret_cast<uint32_t *>(ws + L.counters);
     p.zsum = reinterpret_cast<uint64_t *>(ws + L.zsum);
     p.rsel = reinterpret_cast<int32_t *>(ws + L.rsel);
     p.partials = reinterpret_cast<uint64_t *>(ws + L.partials);
@@ -382,6 +390,8 @@ int launch_verify(const VerifyArgs &a, hipStream_t stream) {
     p.vec4 = ((reinterpret_cast<uintptr_t>(a.target_probs) & 15u) == 0 && (a.target_ld % 4) == 0) ? 1 : 0;
     const int grid = ((p.work_items + kXcds - 1) / kXcds) * kXcds;
     hipLaunchKernelGGL(verify_stream, dim3(grid), dim3(kThreads), 0, stream, p);
+    if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    hipLaunchKernelGGL(verify_sample, dim3(a.n_streams), dim3(kThreads), 0, stream, p);
     if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
     if (a.residual != nullptr) {
         int rsplit = (a.v_t + 8191) / 8192;

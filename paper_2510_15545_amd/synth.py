@@ -387,9 +387,10 @@ def _make_probs(wl: Workload, seed_shift: int) -> None:
     else:  # pragma: no cover
         raise ValueError(c)
 
-    rng_u = np.random.default_rng([SEED_UNIF + c + seed_shift])
-    wl.u_accept = _uniform24(rng_u, int(wl.target_off[-1]))
-    wl.u_sample = _uniform24(rng_u, n)
+    # accept uniforms in CSR order from one stream, sample uniforms from another, so a
+    # reduced workload's uniforms are a prefix of the full workload's
+    wl.u_accept = _uniform24(np.random.default_rng([SEED_UNIF + c + seed_shift, 0]), int(wl.target_off[-1]))
+    wl.u_sample = _uniform24(np.random.default_rng([SEED_UNIF + c + seed_shift, 1]), n)
 
 
 def _long_pair_prob_stage(spec, vd, vt, pairs, seed_shift, probs, w) -> Workload:

@@ -36,8 +36,8 @@ def test_workspace_sizes_are_host_computed():
     L = tt.lib()
     n = ctypes.c_size_t(0)
     assert L.tt_verify_workspace_size(256, 151936, ctypes.byref(n)) == 0
-    # counters + Q62 sums + gamma, and one Q62 sum per 1024-float chunk per stream
-    assert n.value >= 256 * (4 + 8 + 4) + 256 * 149 * 8
+    # Q62 mass + gamma per stream, and one Q62 sum per 1024-float chunk per stream
+    assert n.value >= 256 * (8 + 4) + 256 * 149 * 8
     assert L.tt_verify_workspace_size(-1, 10, ctypes.byref(n)) == tt.TT_EINVAL
     assert L.tt_align_workspace_size(1024, 512, 512, 8, 8, ctypes.byref(n)) == 0 and n.value == 0
     assert L.tt_align_workspace_size(8, 4096, 4096, -1, 8, ctypes.byref(n)) == tt.TT_EUNSUPPORTED

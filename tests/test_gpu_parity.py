@@ -85,6 +85,6 @@ def test_workspace_reuse_gives_identical_results():
                                  d["u_accept"], d["u_sample"], wl.max_m, workspace=ws)
         torch.cuda.synchronize()
         outs.append((nacc.cpu().numpy(), tok.cpu().numpy()))
-        assert int(ws.cpu().numpy()[:4 * wl.n].view(np.uint32).max()) == 0  # counters restored
+        ws.fill_(0xA5)  # stale contents must not matter
     for nacc, tok in outs:
         assert np.array_equal(nacc, o["n_accepted"]) and np.array_equal(tok, o["out_token"])

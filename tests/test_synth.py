@@ -41,6 +41,8 @@ def test_deterministic_and_prefix_stable():
     assert np.array_equal(a.target_ids[:a.target_off[4]], b.target_ids)
     rows = int(b.target_off[-1]) + 4
     assert np.array_equal(a.target_probs[:rows], b.target_probs)
+    assert np.array_equal(a.u_accept[:b.target_off[-1]], b.u_accept)
+    assert np.array_equal(a.u_sample[:4], b.u_sample)
     c = synth.make(2, n_streams=4)
     assert np.array_equal(c.target_probs, b.target_probs) and np.array_equal(c.u_sample, b.u_sample)
 
