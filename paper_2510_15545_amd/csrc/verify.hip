@@ -81,9 +81,22 @@ __device__ __forceinline__ uint64_t exact_threshold(float u, uint64_t Z) {
     return T < Z ? T : Z - 1;
 }
 
-__device__ __forceinline__ uint64_t wave_sum(uint64_t v) {
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+// v + (v shifted across lanes by a DPP control); lanes without a source add 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint64_t dpp_add(uint64_t v) {
+    const uint32_t lo = __builtin_amdgcn_update_dpp(0u, (uint32_t)v, CTRL, ROW_MASK, 0xF, true);
+    const uint32_t hi = __builtin_amdgcn_update_dpp(0u, (uint32_t)(v >> 32), CTRL, ROW_MASK, 0xF, true);
+    return v + (((uint64_t)hi << 32) | lo);
+}
+
+// Sum over the wave; the total lands in lane 63 (row prefix sums, then row broadcasts).
+__device__ __forceinline__ uint64_t wave_sum_to_last(uint64_t v) {
+    v = dpp_add<0x111, 0xF>(v);  // row_shr:1
+    v = dpp_add<0x112, 0xF>(v);  // row_shr:2
+    v = dpp_add<0x114, 0xF>(v);  // row_shr:4
+    v = dpp_add<0x118, 0xF>(v);  // row_shr:8
+    v = dpp_add<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+    v = dpp_add<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
     return v;
 }
 
@@ -140,6 +153,23 @@ __device__ int block_first_argmax(const float *row, int vt, float *shv, int *shi
     const int r = shi[0];
     __syncthreads();
     return r == INT_MAX ? 0 : r;
+}
+
+// The four 16-byte loads of one lane for chunk starting at xb (guarded at the row end).
+__device__ __forceinline__ void load_chunk(const float *row, int xb, int lane, int vt, bool vec, float4 (&v)[4]) {
+    if (vec && xb + kChunk <= vt) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const float4 *>(row + xb + u * 256 + lane * 4);
+    } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int x = xb + u * 256 + lane * 4;
+            v[u].x = x < vt ? row[x] : 0.0f;
+            v[u].y = x + 1 < vt ? row[x + 1] : 0.0f;
+            v[u].z = x + 2 < vt ? row[x + 2] : 0.0f;
+            v[u].w = x + 3 < vt ? row[x + 3] : 0.0f;
+        }
+    }
 }
 
 __global__ void __launch_bounds__(kThreads) verify_stream(VParams p) {
@@ -204,40 +234,32 @@ __global__ void __launch_bounds__(kThreads) verify_stream(VParams p) {
     const int rtok = r < M ? a.target_ids[t0 + r] : -1;
     const float rq = r < M ? a.q[t0 + r] : 0.0f;
 
-    // ---- phase B: stream this workgroup's chunks, Q62 chunk sums
+    // ---- phase B: stream this workgroup's chunks (one chunk ahead), Q62 chunk sums
     const int c0 = s * p.cpw;
     const int c1 = (c0 + p.cpw) < p.nc ? (c0 + p.cpw) : p.nc;
-    for (int c = c0 + wave; c < c1; c += kWaves) {
-        const int xb = c * kChunk;
-        float4 v[4];
-        if (p.vec4 && xb + kChunk <= vt) {
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-                v[u] = *reinterpret_cast<const float4 *>(row + xb + u * 256 + lane * 4);
-        } else {
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int x = xb + u * 256 + lane * 4;
-                v[u].x = x < vt ? row[x] : 0.0f;
-                v[u].y = x + 1 < vt ? row[x + 1] : 0.0f;
-                v[u].z = x + 2 < vt ? row[x + 2] : 0.0f;
-                v[u].w = x + 3 < vt ? row[x + 3] : 0.0f;
-            }
-        }
+    const bool vec = p.vec4 != 0;
+    float4 v[4], nx[4];
+    int c = c0 + wave;
+    if (c < c1) load_chunk(row, c * kChunk, lane, vt, vec, v);
+    for (; c < c1; c += kWaves) {
+        const int cn = c + kWaves;
+        if (cn < c1) load_chunk(row, cn * kChunk, lane, vt, vec, nx);
         uint64_t acc = 0;
 #pragma unroll
         for (int u = 0; u < 4; ++u)
             acc += q62(clamp01(v[u].x)) + q62(clamp01(v[u].y)) + q62(clamp01(v[u].z)) + q62(clamp01(v[u].w));
-        acc = wave_sum(acc);
-        if (lane == 0) {
+        acc = wave_sum_to_last(acc);
+        if (lane == kWave - 1) {
+            const int xb = c * kChunk;
             if (rtok >= xb && rtok < xb + kChunk) {  // the rejected proposal loses q_r of its mass
                 const float pr = row[rtok];
                 acc += q62(clamp01(pr - rq)) - q62(clamp01(pr));
             }
             p.partials[(int64_t)b * p.nc + c] = acc;
         }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = nx[u];
     }
-
 }
 
 // One workgroup per stream: exact threshold, crossing chunk, crossing index.
@@ -245,21 +267,13 @@ __global__ void __launch_bounds__(kThreads) verify_sample(VParams p) {
     const VerifyArgs &a = p.a;
     const int b = blockIdx.x;
     const int tid = threadIdx.x;
-    const int r = p.rsel[b];
-    if (r < 0) return;  // sentinel stream, outputs already written
     __shared__ int sh_chunk, sh_tok;
     __shared__ uint64_t sh_base;
     __shared__ uint64_t sh_scan[kWaves];
     __shared__ float sh_av[kThreads];
     __shared__ int sh_ai[kThreads];
 
-    const int t0 = a.target_off[b];
-    const int M = a.target_off[b + 1] - t0;
-    const int vt = a.v_t;
-    const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
-    const int rtok = r < M ? a.target_ids[t0 + r] : -1;
-    const float rq = r < M ? a.q[t0 + r] : 0.0f;
-
+    // loads that do not depend on gamma first: the chunk sums, offsets, the uniform
     const int nc = p.nc;
     const uint64_t *part = p.partials + (int64_t)b * nc;
     const int per = (nc + kThreads - 1) / kThreads;
@@ -267,6 +281,15 @@ __global__ void __launch_bounds__(kThreads) verify_sample(VParams p) {
     const int cb = ca + per < nc ? ca + per : nc;
     uint64_t local = 0;
     for (int c = ca; c < cb; ++c) local += part[c];
+    const int r = p.rsel[b];
+    const int t0 = a.target_off[b];
+    const int M = a.target_off[b + 1] - t0;
+    const float us = a.u_sample[b];
+    if (r < 0) return;  // sentinel stream, outputs already written (uniform per workgroup)
+    const int vt = a.v_t;
+    const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
+    const int rtok = r < M ? a.target_ids[t0 + r] : -1;
+    const float rq = r < M ? a.q[t0 + r] : 0.0f;
     if (tid == 0) sh_chunk = nc;
     uint64_t Z;
     const uint64_t base = block_exclusive_scan(local, &Z, sh_scan);
@@ -275,7 +298,7 @@ __global__ void __launch_bounds__(kThreads) verify_sample(VParams p) {
     if (Z == 0) {
         token = block_first_argmax(row, vt, sh_av, sh_ai);
     } else {
-        const uint64_t T = exact_threshold(a.u_sample[b], Z);
+        const uint64_t T = exact_threshold(us, Z);
         uint64_t run = base;
         for (int c = ca; c < cb; ++c) {
             const uint64_t nx = run + part[c];
