@@ -93,7 +93,8 @@ def main():
     a_di, a_do, a_ti, a_to = t(A.draft_ids), t(A.draft_off), t(A.target_ids), t(A.target_off)
     a_maxk, a_maxm = max(1, A.max_k), max(1, A.max_m)
     npath = tt.path_capacity(A.draft_off[-1], A.target_off[-1])
-    a_out = tt.align(vd, vt, a_di, a_do, a_ti, a_to, args.w, a_maxk, a_maxm, n_path=npath)
+    a_ws = tt.align_workspace(A.n, a_maxk, a_maxm, args.w, max(A.vocab_d.max_len, A.vocab_t.max_len), dev)
+    a_out = tt.align(vd, vt, a_di, a_do, a_ti, a_to, args.w, a_maxk, a_maxm, n_path=npath, workspace=a_ws)
 
     S = stage
     s_di, s_do, s_to = t(S.draft_ids), t(S.draft_off), t(S.target_off)
@@ -118,7 +119,7 @@ def main():
     del wl0  # keep host memory for the CPU leg only where needed
 
     def do_align():
-        tt.align(vd, vt, a_di, a_do, a_ti, a_to, args.w, a_maxk, a_maxm, out=a_out)
+        tt.align(vd, vt, a_di, a_do, a_ti, a_to, args.w, a_maxk, a_maxm, out=a_out, workspace=a_ws)
 
     def do_transfer():
         tt.transfer(S.v_d, s_di, s_do, s_to, s_out[3], draft_probs, out=q)

@@ -68,8 +68,10 @@ typedef struct {
 } tt_vocab;
 
 /*
- * Workspace bytes tt_align needs for these bounds (currently always 0: the
- * alignment keeps its whole working set in LDS).  Returns TT_EUNSUPPORTED when
+ * Workspace bytes tt_align needs for these bounds: 0 when max_k <= 64 (each pair's
+ * working set stays in LDS), otherwise room for the 2-bit predecessor codes of
+ * every pair's band (n_pairs * max_k * ceil(min(max_m, 2 L + 1) / 16) * 4 bytes,
+ * L the largest band half-width the bounds allow).  Returns TT_EUNSUPPORTED when
  * the bounds need more LDS than one MI355X workgroup can hold.
  */
 int tt_align_workspace_size(int32_t n_pairs, int32_t max_k, int32_t max_m, int32_t w,
@@ -100,7 +102,9 @@ int tt_align_workspace_size(int32_t n_pairs, int32_t max_k, int32_t max_m, int32
  *                  many-to-one block, the shared token of a one-to-many block)
  * Ties between equally cheap predecessors go to the diagonal step, then to
  * (i-1, j), then to (i, j-1).
- * workspace / workspace_bytes may be NULL / 0 (see tt_align_workspace_size).
+ * workspace: device memory of tt_align_workspace_size bytes (may be NULL / 0 when
+ * that size is 0); no initialisation needed; calls that overlap in time must not
+ * share it.  TT_EWORKSPACE if it is missing or too small.
  */
 int tt_align(const tt_vocab *vd, const tt_vocab *vt, int32_t n_pairs,
              const int32_t *draft_ids, const int32_t *draft_off,

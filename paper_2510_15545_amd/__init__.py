@@ -15,7 +15,7 @@ from __future__ import annotations
 import ctypes
 import os
 
-__all__ = ["Vocab", "align", "transfer", "verify", "verify_workspace", "lib", "LIB_PATH",
+__all__ = ["Vocab", "align", "align_workspace", "transfer", "verify", "verify_workspace", "lib", "LIB_PATH",
            "TTError", "path_capacity"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtt.so")
@@ -121,17 +121,29 @@ def path_capacity(draft_off_last: int, target_off_last: int) -> int:
     return 2 * (int(draft_off_last) + int(target_off_last))
 
 
+def align_workspace(n_pairs: int, max_k: int, max_m: int, w: int, max_token_bytes: int, device="cuda"):
+    """A workspace for tt_align with these bounds (None when none is needed)."""
+    torch = _torch()
+    n = ctypes.c_size_t(0)
+    _check(lib().tt_align_workspace_size(int(n_pairs), int(max_k), int(max_m), int(w), int(max_token_bytes),
+                                         ctypes.byref(n)), "tt_align_workspace_size")
+    return torch.empty(n.value, dtype=torch.uint8, device=device) if n.value else None
+
+
 def align(vd: Vocab, vt: Vocab, draft_ids, draft_off, target_ids, target_off, w: int,
-          max_k: int, max_m: int, n_path: int | None = None, out=None, stream=None):
+          max_k: int, max_m: int, n_path: int | None = None, out=None, workspace=None, stream=None):
     """tt_align.  Returns (cost, path_len, path, map) device tensors (int32).
 
     n_path: length of the path buffer (2 * (sum K + sum M)); read from the CSR
     offsets on the host if not given (one small device->host copy).
+    workspace: from align_workspace(); allocated here when needed and not given.
     """
     torch = _torch()
     i32 = torch.int32
     n = int(draft_off.numel()) - 1
     dev = draft_off.device
+    if workspace is None:
+        workspace = align_workspace(n, max_k, max_m, w, max(vd.max_token_bytes, vt.max_token_bytes), dev)
     if out is None:
         if n_path is None:
             n_path = path_capacity(draft_off[-1].item(), target_off[-1].item())
@@ -147,7 +159,9 @@ def align(vd: Vocab, vt: Vocab, draft_ids, draft_off, target_ids, target_off, w:
                         _ptr(ti, i32, "target_ids"), _ptr(target_off, i32, "target_off"),
                         int(max_k), int(max_m), int(w),
                         _ptr(cost, i32, "cost"), _ptr(plen, i32, "path_len"),
-                        _ptr(path, i32, "path"), _ptr(mp, i32, "map"), None, 0, _stream_handle(stream))
+                        _ptr(path, i32, "path"), _ptr(mp, i32, "map"),
+                        None if workspace is None else ctypes.c_void_p(workspace.data_ptr()),
+                        0 if workspace is None else int(workspace.numel()), _stream_handle(stream))
     _check(st, "tt_align")
     return out
 

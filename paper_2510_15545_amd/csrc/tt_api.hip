@@ -37,7 +37,7 @@ int tt_align_workspace_size(int32_t n_pairs, int32_t max_k, int32_t max_m, int32
         return TT_EINVAL;
     const int tb = tt::align_token_slot(max_token_bytes);
     if (tb == 0 || tt::align_lds_bytes(max_k, max_m, w, tb) == 0) return TT_EUNSUPPORTED;
-    *bytes = 0;
+    *bytes = tt::align_workspace_bytes(n_pairs, max_k, max_m, w);
     return TT_OK;
 }
 
@@ -45,8 +45,6 @@ int tt_align(const tt_vocab *vd, const tt_vocab *vt, int32_t n_pairs, const int3
              const int32_t *draft_off, const int32_t *target_ids, const int32_t *target_off,
              int32_t max_k, int32_t max_m, int32_t w, int32_t *cost, int32_t *path_len, int32_t *path,
              int32_t *map, void *workspace, size_t workspace_bytes, void *stream) {
-    (void)workspace;
-    (void)workspace_bytes;
     if (!vocab_ok(vd) || !vocab_ok(vt) || n_pairs < 0) return TT_EINVAL;
     if (max_k < 1 || max_m < 1 || max_k > kMaxAlignLen || max_m > kMaxAlignLen) return TT_EINVAL;
     if (n_pairs == 0) return TT_OK;
@@ -70,7 +68,7 @@ int tt_align(const tt_vocab *vd, const tt_vocab *vt, int32_t n_pairs, const int3
     a.path_len = path_len;
     a.path = path;
     a.map = map;
-    return tt::launch_align(a, static_cast<hipStream_t>(stream));
+    return tt::launch_align(a, workspace, workspace_bytes, static_cast<hipStream_t>(stream));
 }
 
 int tt_transfer(int32_t n_pairs, int32_t v_d, const int32_t *draft_ids, const int32_t *draft_off,

@@ -23,7 +23,9 @@ struct AlignArgs {
 // per-workgroup LDS of gfx950.  `tb` is the token slot width chosen for the vocabularies.
 size_t align_lds_bytes(int32_t max_k, int32_t max_m, int32_t w, int tb);
 int align_token_slot(int32_t max_token_bytes);  // 8, 16, 32 or 64; 0 if unsupported
-int launch_align(const AlignArgs &a, hipStream_t stream);
+// Global workspace for the direction codes of finished 64-row strips (0 if max_k <= 64).
+size_t align_workspace_bytes(int32_t n_pairs, int32_t max_k, int32_t max_m, int32_t w);
+int launch_align(const AlignArgs &a, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 // ---------------------------------------------------------------- transfer (transfer.hip)
 struct TransferArgs {
@@ -51,7 +53,7 @@ struct VerifyArgs {
 
 // Workspace layout for tt_verify.
 struct VerifyLayout {
-    size_t zsum, rsel, partials, total;
+    size_t zsum, rsel, partials, arrivals, total;
     int32_t n_chunks;
 };
 VerifyLayout verify_layout(int32_t n_streams, int32_t v_t);

@@ -9,36 +9,44 @@
 // (one wave, 16 floats per lane, 16-byte loads).  Each chunk's residual mass is
 // accumulated in exact Q62 fixed point (R quantised by truncation), so chunk sums and
 // their prefix are independent of summation order and the sampled token is
-// bit-identical to a sequential scan.
+// bit-identical to a sequential scan.  Sampling forms Z and T = floor(u * Z) exactly,
+// scans the chunk sums to the crossing chunk, re-reads that one chunk (4 KiB) and
+// scans it to the crossing index.
 //
-// Two kernels, ordered by the stream:
-//   verify_stream  grid B x S: every workgroup of stream b recomputes gamma_b (M_b
-//                  scalar gathers), then streams its share of row gamma_b and stores one
-//                  Q62 sum per chunk.  Split 0 records gamma_b.
-//   verify_sample  grid B: forms Z and T = floor(u * Z) exactly, scans the chunk sums to
-//                  the crossing chunk, re-reads that one chunk (4 KiB) and scans it to the
-//                  crossing index.
-// The kernel boundary publishes the chunk sums; an in-kernel hand-off between
-// workgroups would need agent-scope fences, which on gfx950 write back and invalidate
-// the whole L2 of an XCD.
-//
-// Workgroup id -> (stream, split) is XCD-aware: the hardware deals workgroup ids
-// round-robin over the 8 XCDs, so XCD x receives the contiguous work range
+// Two launch shapes:
+//   row path    (at least one stream per CU): one 1024-thread workgroup per stream
+//               runs the acceptance scan once, streams its whole row with 16 waves,
+//               keeps the chunk sums in LDS and one wave samples.  One kernel.
+//   split path  (fewer streams): verify_stream over B x S workgroups (every workgroup
+//               of a stream recomputes gamma, streams its share of the row and stores
+//               chunk sums), then verify_sample with one wave per stream.  The kernel
+//               boundary publishes the chunk sums: an in-kernel hand-off between
+//               workgroups needs an agent-scope release, which on gfx950 writes back
+//               the XCD's whole L2 (one per workgroup made the kernel 5-10x slower).
+// Sampling runs in one wave with DPP prefix sums and no LDS or barriers.
+// In the split path workgroup id -> (stream, split) is XCD-aware: the hardware deals
+// workgroup ids round-robin over the 8 XCDs, so XCD x receives the contiguous work range
 // [x * G/8, (x+1) * G/8) and a stream's splits share one XCD.
 #include <climits>
 #include <cmath>
 
 #include "tt_internal.h"
 
+#ifndef TT_VERIFY_TARGET_WG
+#define TT_VERIFY_TARGET_WG 2048  // split path: workgroups to aim for
+#endif
+#ifndef TT_VERIFY_ROW_MIN_STREAMS
+#define TT_VERIFY_ROW_MIN_STREAMS 256  // row path from this many streams up
+#endif
+
 namespace tt {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
+constexpr int kSplitThreads = 256;
+constexpr int kRowThreads = 1024;
 constexpr int kChunk = 1024;
 constexpr int kXcds = 8;
-constexpr int kTargetWorkgroups = 2048;
 
 struct VParams {
     VerifyArgs a;
@@ -89,8 +97,9 @@ __device__ __forceinline__ uint64_t dpp_add(uint64_t v) {
     return v + (((uint64_t)hi << 32) | lo);
 }
 
-// Sum over the wave; the total lands in lane 63 (row prefix sums, then row broadcasts).
-__device__ __forceinline__ uint64_t wave_sum_to_last(uint64_t v) {
+// Inclusive prefix sum over the 64 lanes (prefix sums inside each row of 16 lanes, then
+// row broadcasts); lane 63 holds the total.
+__device__ __forceinline__ uint64_t wave_inclusive_scan(uint64_t v) {
     v = dpp_add<0x111, 0xF>(v);  // row_shr:1
     v = dpp_add<0x112, 0xF>(v);  // row_shr:2
     v = dpp_add<0x114, 0xF>(v);  // row_shr:4
@@ -100,59 +109,60 @@ __device__ __forceinline__ uint64_t wave_sum_to_last(uint64_t v) {
     return v;
 }
 
-// Exclusive scan over the workgroup in thread order; *total receives the full sum.
-__device__ __forceinline__ uint64_t block_exclusive_scan(uint64_t v, uint64_t *total, uint64_t *sh) {
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    uint64_t incl = v;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const uint64_t n = __shfl_up(incl, off);
-        if (lane >= off) incl += n;
-    }
-    if (lane == kWave - 1) sh[wave] = incl;
-    __syncthreads();
-    uint64_t wbase = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-        const uint64_t s = sh[w];
-        if (w < wave) wbase += s;
-        tot += s;
-    }
-    __syncthreads();
-    *total = tot;
-    return wbase + incl - v;
+__device__ __forceinline__ uint64_t lane_value(uint64_t v, int lane) {
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, lane);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
 }
 
-// First index of the maximum (NaN never wins); 0 if no element exceeds -inf.
-__device__ int block_first_argmax(const float *row, int vt, float *shv, int *shi) {
+// First index of the maximum over the row (NaN never wins); 0 if nothing exceeds -inf.
+// One wave.
+__device__ int wave_first_argmax(const float *row, int vt) {
+    const int lane = threadIdx.x % kWave;
     float bv = -INFINITY;
     int bi = INT_MAX;
-    for (int x = threadIdx.x; x < vt; x += kThreads) {
+    for (int x = lane; x < vt; x += kWave) {
         const float v = row[x];
         if (v > bv) {
             bv = v;
             bi = x;
         }
     }
-    shv[threadIdx.x] = bv;
-    shi[threadIdx.x] = bi;
-    __syncthreads();
-    for (int w = kThreads / 2; w > 0; w >>= 1) {
-        if ((int)threadIdx.x < w) {
-            const float ov = shv[threadIdx.x + w];
-            const int oi = shi[threadIdx.x + w];
-            const float mv = shv[threadIdx.x];
-            const int mi = shi[threadIdx.x];
-            if (ov > mv || (ov == mv && oi < mi)) {
-                shv[threadIdx.x] = ov;
-                shi[threadIdx.x] = oi;
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const float ov = __shfl_xor(bv, off);
+        const int oi = __shfl_xor(bi, off);
+        if (ov > bv || (ov == bv && oi < bi)) {
+            bv = ov;
+            bi = oi;
+        }
+    }
+    return bi == INT_MAX ? 0 : bi;
+}
+
+// Acceptance scan by one wave: gamma (first rejection, else M); false if the stream is
+// invalid (M outside [0, max_m] or an id outside [0, v_t)).
+__device__ __forceinline__ bool accept_scan(const VerifyArgs &a, int b, int t0, int M, int lane, int &gamma) {
+    gamma = M;
+    if (M < 0 || M > a.max_m) return false;
+    for (int base = 0; base < M; base += kWave) {
+        const int j = base + lane;
+        bool bad = false, rej = false;
+        if (j < M) {
+            const int tok = a.target_ids[t0 + j];
+            if (tok < 0 || tok >= a.v_t) {
+                bad = true;
+            } else {
+                const float pt = a.target_probs[(int64_t)(t0 + b + j) * a.target_ld + tok];
+                const float qj = a.q[t0 + j];
+                const float ratio = pt / qj;
+                rej = !((qj <= 0.0f) || (a.u_accept[t0 + j] < ratio));
             }
         }
-        __syncthreads();
+        if (__any(bad)) return false;
+        const unsigned long long rm = __ballot(rej);
+        if (rm != 0ull && gamma == M) gamma = base + __ffsll(rm) - 1;
     }
-    const int r = shi[0];
-    __syncthreads();
-    return r == INT_MAX ? 0 : r;
+    return true;
 }
 
 // The four 16-byte loads of one lane for chunk starting at xb (guarded at the row end).
@@ -172,7 +182,154 @@ __device__ __forceinline__ void load_chunk(const float *row, int xb, int lane, i
     }
 }
 
-__global__ void __launch_bounds__(kThreads) verify_stream(VParams p) {
+// Q62 sums of chunks c0 + wave, c0 + wave + stride, ... < c1 (one chunk ahead in flight);
+// lane 63 hands each sum to store(c, sum).
+template <class Store>
+__device__ __forceinline__ void stream_chunks(const float *row, int vt, bool vec, int c0, int c1, int stride,
+                                              int rtok, float rq, Store store) {
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    float4 v[4], nx[4];
+    int c = c0 + wave;
+    if (c < c1) load_chunk(row, c * kChunk, lane, vt, vec, v);
+    for (; c < c1; c += stride) {
+        const int cn = c + stride;
+        if (cn < c1) load_chunk(row, cn * kChunk, lane, vt, vec, nx);
+        uint64_t acc = 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            acc += q62(clamp01(v[u].x)) + q62(clamp01(v[u].y)) + q62(clamp01(v[u].z)) + q62(clamp01(v[u].w));
+        acc = wave_inclusive_scan(acc);
+        if (lane == kWave - 1) {
+            const int xb = c * kChunk;
+            if (rtok >= xb && rtok < xb + kChunk) {  // the rejected proposal loses q_r of its mass
+                const float pr = row[rtok];
+                acc += q62(clamp01(pr - rq)) - q62(clamp01(pr));
+            }
+            store(c, acc);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = nx[u];
+    }
+}
+
+// Inverse-CDF sample of the row from its nc chunk sums part(c), by one wave: every lane
+// returns the token and *Zout the Q62 mass.  Chunk sums are scanned lane-blocked, the
+// crossing chunk is re-read as 16 consecutive floats per lane and scanned the same way.
+template <class Part>
+__device__ int wave_sample(const float *row, int vt, int nc, Part part, float u, int rtok, float rq,
+                           uint64_t *Zout) {
+    const int lane = threadIdx.x % kWave;
+    const int per = (nc + kWave - 1) / kWave;
+    const int ca = lane * per < nc ? lane * per : nc;
+    const int cb = ca + per < nc ? ca + per : nc;
+    uint64_t local = 0;
+    for (int c = ca; c < cb; ++c) local += part(c);
+    const uint64_t incl = wave_inclusive_scan(local);
+    const uint64_t Z = lane_value(incl, kWave - 1);
+    *Zout = Z;
+    if (Z == 0) return wave_first_argmax(row, vt);
+    const uint64_t T = exact_threshold(u, Z);
+    // lane whose block of chunks holds the crossing, then the chunk inside it
+    const uint64_t excl = incl - local;
+    const unsigned long long hit = __ballot(excl <= T && T < incl);
+    if (hit == 0ull) return vt - 1;  // only if the Q62 mass wrapped (not a probability row)
+    const int owner = __ffsll(hit) - 1;
+    int cs = nc;
+    uint64_t base = 0;
+    if (lane == owner) {
+        uint64_t run = excl;
+        for (int c = ca; c < cb; ++c) {
+            const uint64_t nx = run + part(c);
+            if (run <= T && nx > T) {
+                cs = c;
+                base = run;
+                break;
+            }
+            run = nx;
+        }
+    }
+    cs = __builtin_amdgcn_readlane(cs, owner);
+    base = lane_value(base, owner);
+    // the crossing chunk: lane holds elements cs*1024 + lane*16 + [0, 16)
+    const int x0 = cs * kChunk + lane * 16;
+    uint64_t qv[16];
+    uint64_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const int x = x0 + k;
+        const float pv = x < vt ? row[x] : 0.0f;
+        qv[k] = q62(clamp01(pv - (x == rtok ? rq : 0.0f)));
+        sum += qv[k];
+    }
+    const uint64_t lincl = wave_inclusive_scan(sum) + base;
+    const uint64_t lexcl = lincl - sum;
+    const unsigned long long lhit = __ballot(lexcl <= T && T < lincl);
+    if (lhit == 0ull) return vt - 1;
+    const int tl = __ffsll(lhit) - 1;
+    int tok = vt - 1;
+    if (lane == tl) {
+        uint64_t run = lexcl;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            run += qv[k];
+            if (run > T) {
+                tok = x0 + k;
+                break;
+            }
+        }
+    }
+    return __builtin_amdgcn_readlane(tok, tl);
+}
+
+// ------------------------------------------------------------------ row path
+__global__ void __launch_bounds__(kRowThreads) verify_row(VParams p) {
+    const VerifyArgs &a = p.a;
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    extern __shared__ uint64_t sh_part[];  // nc chunk sums
+    __shared__ int sh_gamma, sh_ok;
+
+    const int t0 = a.target_off[b];
+    const int M = a.target_off[b + 1] - t0;
+    const float us = a.u_sample[b];
+    if (wave == 0) {
+        int gamma;
+        const bool ok = accept_scan(a, b, t0, M, lane, gamma);
+        if (lane == 0) {
+            sh_gamma = gamma;
+            sh_ok = ok ? 1 : 0;
+        }
+    }
+    __syncthreads();
+    if (!sh_ok) {
+        if (tid == 0) {
+            a.n_accepted[b] = -1;
+            a.out_token[b] = -1;
+            p.rsel[b] = -1;
+        }
+        return;
+    }
+    const int r = sh_gamma;
+    const int vt = a.v_t;
+    const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
+    const int rtok = r < M ? a.target_ids[t0 + r] : -1;
+    const float rq = r < M ? a.q[t0 + r] : 0.0f;
+    stream_chunks(row, vt, p.vec4 != 0, 0, p.nc, kRowThreads / kWave, rtok, rq,
+                  [&](int c, uint64_t s) { sh_part[c] = s; });
+    __syncthreads();
+    if (wave != 0) return;
+    uint64_t Z;
+    const int token = wave_sample(row, vt, p.nc, [&](int c) { return sh_part[c]; }, us, rtok, rq, &Z);
+    if (tid == 0) {
+        a.n_accepted[b] = r;
+        a.out_token[b] = token;
+        p.zsum[b] = Z;
+        p.rsel[b] = r;
+    }
+}
+
+// ------------------------------------------------------------------ split path
+__global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
     const VerifyArgs &a = p.a;
     const int G = gridDim.x;
     const int g = blockIdx.x;
@@ -180,39 +337,13 @@ __global__ void __launch_bounds__(kThreads) verify_stream(VParams p) {
     if (work >= p.work_items) return;
     const int b = work / p.splits, s = work % p.splits;
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
-
     __shared__ int sh_gamma, sh_ok;
 
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
-
-    // ---- phase A: acceptance scan (every workgroup of the stream, redundantly)
-    if (wave == 0) {
-        bool ok = M >= 0 && M <= a.max_m;
-        int gamma = M;
-        if (ok) {
-            for (int base = 0; base < M; base += kWave) {
-                const int j = base + lane;
-                bool bad = false, rej = false;
-                if (j < M) {
-                    const int tok = a.target_ids[t0 + j];
-                    if (tok < 0 || tok >= a.v_t) {
-                        bad = true;
-                    } else {
-                        const float pt = a.target_probs[(int64_t)(t0 + b + j) * a.target_ld + tok];
-                        const float qj = a.q[t0 + j];
-                        const float ratio = pt / qj;
-                        rej = !((qj <= 0.0f) || (a.u_accept[t0 + j] < ratio));
-                    }
-                }
-                if (__any(bad)) {
-                    ok = false;
-                    break;
-                }
-                const unsigned long long rm = __ballot(rej);
-                if (rm != 0ull && gamma == M) gamma = base + __ffsll(rm) - 1;
-            }
-        }
+    if (wave == 0) {  // every workgroup of the stream recomputes gamma
+        int gamma;
+        const bool ok = accept_scan(a, b, t0, M, lane, gamma);
         if (lane == 0) {
             sh_gamma = gamma;
             sh_ok = ok ? 1 : 0;
@@ -229,116 +360,32 @@ __global__ void __launch_bounds__(kThreads) verify_stream(VParams p) {
     }
     const int r = sh_gamma;
     if (s == 0 && tid == 0) p.rsel[b] = r;
-    const int vt = a.v_t;
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
     const int rtok = r < M ? a.target_ids[t0 + r] : -1;
     const float rq = r < M ? a.q[t0 + r] : 0.0f;
-
-    // ---- phase B: stream this workgroup's chunks (one chunk ahead), Q62 chunk sums
     const int c0 = s * p.cpw;
     const int c1 = (c0 + p.cpw) < p.nc ? (c0 + p.cpw) : p.nc;
-    const bool vec = p.vec4 != 0;
-    float4 v[4], nx[4];
-    int c = c0 + wave;
-    if (c < c1) load_chunk(row, c * kChunk, lane, vt, vec, v);
-    for (; c < c1; c += kWaves) {
-        const int cn = c + kWaves;
-        if (cn < c1) load_chunk(row, cn * kChunk, lane, vt, vec, nx);
-        uint64_t acc = 0;
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            acc += q62(clamp01(v[u].x)) + q62(clamp01(v[u].y)) + q62(clamp01(v[u].z)) + q62(clamp01(v[u].w));
-        acc = wave_sum_to_last(acc);
-        if (lane == kWave - 1) {
-            const int xb = c * kChunk;
-            if (rtok >= xb && rtok < xb + kChunk) {  // the rejected proposal loses q_r of its mass
-                const float pr = row[rtok];
-                acc += q62(clamp01(pr - rq)) - q62(clamp01(pr));
-            }
-            p.partials[(int64_t)b * p.nc + c] = acc;
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = nx[u];
-    }
+    uint64_t *out = p.partials + (int64_t)b * p.nc;
+    stream_chunks(row, a.v_t, p.vec4 != 0, c0, c1, kSplitThreads / kWave, rtok, rq,
+                  [&](int c, uint64_t sum) { out[c] = sum; });
 }
 
-// One workgroup per stream: exact threshold, crossing chunk, crossing index.
-__global__ void __launch_bounds__(kThreads) verify_sample(VParams p) {
+// One wave per stream: exact threshold, crossing chunk, crossing index.
+__global__ void __launch_bounds__(kWave) verify_sample(VParams p) {
     const VerifyArgs &a = p.a;
     const int b = blockIdx.x;
     const int tid = threadIdx.x;
-    __shared__ int sh_chunk, sh_tok;
-    __shared__ uint64_t sh_base;
-    __shared__ uint64_t sh_scan[kWaves];
-    __shared__ float sh_av[kThreads];
-    __shared__ int sh_ai[kThreads];
-
-    // loads that do not depend on gamma first: the chunk sums, offsets, the uniform
-    const int nc = p.nc;
-    const uint64_t *part = p.partials + (int64_t)b * nc;
-    const int per = (nc + kThreads - 1) / kThreads;
-    const int ca = tid * per < nc ? tid * per : nc;
-    const int cb = ca + per < nc ? ca + per : nc;
-    uint64_t local = 0;
-    for (int c = ca; c < cb; ++c) local += part[c];
+    const uint64_t *part = p.partials + (int64_t)b * p.nc;
     const int r = p.rsel[b];
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
     const float us = a.u_sample[b];
     if (r < 0) return;  // sentinel stream, outputs already written (uniform per workgroup)
-    const int vt = a.v_t;
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
     const int rtok = r < M ? a.target_ids[t0 + r] : -1;
     const float rq = r < M ? a.q[t0 + r] : 0.0f;
-    if (tid == 0) sh_chunk = nc;
     uint64_t Z;
-    const uint64_t base = block_exclusive_scan(local, &Z, sh_scan);
-
-    int token;
-    if (Z == 0) {
-        token = block_first_argmax(row, vt, sh_av, sh_ai);
-    } else {
-        const uint64_t T = exact_threshold(us, Z);
-        uint64_t run = base;
-        for (int c = ca; c < cb; ++c) {
-            const uint64_t nx = run + part[c];
-            if (run <= T && nx > T) atomicMin(&sh_chunk, c);
-            run = nx;
-        }
-        __syncthreads();
-        const int cs = sh_chunk;
-        if (cs < nc && ca <= cs && cs < cb) {
-            uint64_t run2 = base;
-            for (int c = ca; c < cs; ++c) run2 += part[c];
-            sh_base = run2;
-        }
-        if (tid == 0) sh_tok = INT_MAX;
-        __syncthreads();
-        if (cs < nc) {
-            const int x0 = cs * kChunk + tid * 4;
-            uint64_t qv[4];
-            uint64_t loc = 0;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const int x = x0 + k;
-                const float pv = x < vt ? row[x] : 0.0f;
-                qv[k] = q62(clamp01(pv - (x == rtok ? rq : 0.0f)));
-                loc += qv[k];
-            }
-            uint64_t tot2;
-            uint64_t pre = block_exclusive_scan(loc, &tot2, sh_scan) + sh_base;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                pre += qv[k];
-                if (pre > T) {
-                    atomicMin(&sh_tok, x0 + k);
-                    break;
-                }
-            }
-            __syncthreads();
-        }
-        token = (sh_tok == INT_MAX) ? vt - 1 : sh_tok;
-    }
+    const int token = wave_sample(row, a.v_t, p.nc, [&](int c) { return part[c]; }, us, rtok, rq, &Z);
     if (tid == 0) {
         a.n_accepted[b] = r;
         a.out_token[b] = token;
@@ -347,7 +394,7 @@ __global__ void __launch_bounds__(kThreads) verify_sample(VParams p) {
 }
 
 // Optional normalised residual row: res[x] = R(x) / fp32(Z * 2^-62), one-hot when Z = 0.
-__global__ void __launch_bounds__(kThreads) residual_write(VParams p, int rsplit) {
+__global__ void __launch_bounds__(kSplitThreads) residual_write(VParams p, int rsplit) {
     const VerifyArgs &a = p.a;
     const int b = blockIdx.x / rsplit, sidx = blockIdx.x % rsplit;
     if (a.n_accepted[b] < 0) return;
@@ -365,11 +412,11 @@ __global__ void __launch_bounds__(kThreads) residual_write(VParams p, int rsplit
     const int x0 = sidx * per;
     const int x1 = (x0 + per) < vt ? (x0 + per) : vt;
     if (Z == 0) {
-        for (int x = x0 + (int)threadIdx.x; x < x1; x += kThreads) res[x] = (x == tok) ? 1.0f : 0.0f;
+        for (int x = x0 + (int)threadIdx.x; x < x1; x += kSplitThreads) res[x] = (x == tok) ? 1.0f : 0.0f;
         return;
     }
     const float zf = (float)Z * 0x1p-62f;
-    for (int x = x0 + (int)threadIdx.x; x < x1; x += kThreads)
+    for (int x = x0 + (int)threadIdx.x; x < x1; x += kSplitThreads)
         res[x] = clamp01(row[x] - (x == rtok ? rq : 0.0f)) / zf;
 }
 
@@ -402,24 +449,34 @@ int launch_verify(const VerifyArgs &a, hipStream_t stream) {
     p.rsel = reinterpret_cast<int32_t *>(ws + L.rsel);
     p.partials = reinterpret_cast<uint64_t *>(ws + L.partials);
     p.nc = L.n_chunks;
-    // splits per stream: aim for ~kTargetWorkgroups workgroups, at least one chunk per wave
-    int max_splits = (p.nc + kWaves - 1) / kWaves;
-    int splits = (kTargetWorkgroups + a.n_streams - 1) / a.n_streams;
-    if (splits > max_splits) splits = max_splits;
-    if (splits < 1) splits = 1;
-    p.cpw = (p.nc + splits - 1) / splits;
-    p.splits = (p.nc + p.cpw - 1) / p.cpw;
-    p.work_items = a.n_streams * p.splits;
     p.vec4 = ((reinterpret_cast<uintptr_t>(a.target_probs) & 15u) == 0 && (a.target_ld % 4) == 0) ? 1 : 0;
-    const int grid = ((p.work_items + kXcds - 1) / kXcds) * kXcds;
-    hipLaunchKernelGGL(verify_stream, dim3(grid), dim3(kThreads), 0, stream, p);
-    if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
-    hipLaunchKernelGGL(verify_sample, dim3(a.n_streams), dim3(kThreads), 0, stream, p);
-    if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    const size_t row_lds = 8 * (size_t)p.nc;
+    if (a.n_streams >= TT_VERIFY_ROW_MIN_STREAMS && row_lds <= 64 * 1024) {
+        p.splits = 1;
+        p.cpw = p.nc;
+        p.work_items = a.n_streams;
+        hipLaunchKernelGGL(verify_row, dim3(a.n_streams), dim3(kRowThreads), row_lds, stream, p);
+        if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    } else {
+        // splits per stream: aim for TT_VERIFY_TARGET_WG workgroups, at least one chunk per wave
+        constexpr int kWaves = kSplitThreads / kWave;
+        int max_splits = (p.nc + kWaves - 1) / kWaves;
+        int splits = (TT_VERIFY_TARGET_WG + a.n_streams - 1) / a.n_streams;
+        if (splits > max_splits) splits = max_splits;
+        if (splits < 1) splits = 1;
+        p.cpw = (p.nc + splits - 1) / splits;
+        p.splits = (p.nc + p.cpw - 1) / p.cpw;
+        p.work_items = a.n_streams * p.splits;
+        const int grid = ((p.work_items + kXcds - 1) / kXcds) * kXcds;
+        hipLaunchKernelGGL(verify_stream, dim3(grid), dim3(kSplitThreads), 0, stream, p);
+        if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+        hipLaunchKernelGGL(verify_sample, dim3(a.n_streams), dim3(kWave), 0, stream, p);
+        if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    }
     if (a.residual != nullptr) {
         int rsplit = (a.v_t + 8191) / 8192;
         if (rsplit < 1) rsplit = 1;
-        hipLaunchKernelGGL(residual_write, dim3(a.n_streams * rsplit), dim3(kThreads), 0, stream, p, rsplit);
+        hipLaunchKernelGGL(residual_write, dim3(a.n_streams * rsplit), dim3(kSplitThreads), 0, stream, p, rsplit);
         if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
     }
     return TT_OK;

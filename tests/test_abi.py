@@ -39,7 +39,9 @@ def test_workspace_sizes_are_host_computed():
     # Q62 mass + gamma per stream, and one Q62 sum per 1024-float chunk per stream
     assert n.value >= 256 * (8 + 4) + 256 * 149 * 8
     assert L.tt_verify_workspace_size(-1, 10, ctypes.byref(n)) == tt.TT_EINVAL
-    assert L.tt_align_workspace_size(1024, 512, 512, 8, 8, ctypes.byref(n)) == 0 and n.value == 0
+    assert L.tt_align_workspace_size(256, 8, 64, 8, 8, ctypes.byref(n)) == 0 and n.value == 0
+    assert L.tt_align_workspace_size(1024, 512, 512, 8, 8, ctypes.byref(n)) == 0
+    assert n.value == 1024 * 512 * 32 * 4  # 2-bit codes for a 512-wide band row
     assert L.tt_align_workspace_size(8, 4096, 4096, -1, 8, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
     assert L.tt_align_workspace_size(8, 16, 16, 8, 65, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
 

@@ -88,3 +88,22 @@ def test_workspace_reuse_gives_identical_results():
         ws.fill_(0xA5)  # stale contents must not matter
     for nacc, tok in outs:
         assert np.array_equal(nacc, o["n_accepted"]) and np.array_equal(tok, o["out_token"])
+
+
+def test_one_workgroup_per_stream_path():
+    """Batches with at least one stream per CU take the single-kernel row path."""
+    wl = _case(1, 300)
+    g = gpu_run(wl, residual=True)
+    o = oracle_run(wl, residual=True)
+    compare_align(wl, g, o)
+    compare_verify(g, o, residual=True)
+
+
+@pytest.mark.parametrize("c", [2, 3])
+def test_full_size_workload(c):
+    """The benchmark's shapes, every stream checked (workload 3 takes the row path)."""
+    wl = _case(c, {2: None, 3: None})
+    g = gpu_run(wl)
+    o = oracle_run(wl)
+    compare_align(wl, g, o)
+    compare_verify(g, o)
