@@ -40,6 +40,36 @@ def band_cells(K, M, w):
     return total
 
 
+def verify_source_digest():
+    """sha256 over the sources of the verify kernel: counter figures taken from another
+    version of the kernel are not reported."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("verify.hip", "tt_internal.h"):
+        with open(os.path.join(ROOT, "paper_2510_15545_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def read_traffic(path, workload):
+    """HBM bytes per verify launch from a counter summary (key: value lines), or None when
+    the file is missing, covers another workload, or was taken from other kernel sources."""
+    if not path or not os.path.exists(path):
+        return None, "no counter summary"
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith((" ", "#", "|")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("workload") != workload:
+        return None, "counters cover workload %r" % kv.get("workload")
+    if kv.get("source_sha256") != verify_source_digest():
+        return None, "verify kernel changed since the counters were taken"
+    return int(kv["traffic_bytes_per_launch"]), "FETCH_SIZE x %s + WRITE_SIZE x %s" % (
+        kv.get("fetch_scale"), kv.get("write_scale"))
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -56,8 +86,8 @@ def parse():
                     help="also run one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--only", choices=["verify", "align", "transfer"], default=None,
                     help="after the timed steps, loop only this call (for profiler passes)")
-    ap.add_argument("--traffic", type=str, default=None,
-                    help="JSON file with measured HBM bytes per verify launch (from counter runs)")
+    ap.add_argument("--traffic", type=str, default=os.path.join(ROOT, "profiles", "tt_verify_counters.txt"),
+                    help="counter summary with the measured HBM bytes per verify launch")
     return ap.parse_args()
 
 
@@ -234,17 +264,16 @@ def main():
     gbs_verify = verify_bytes / (ms_verify * 1e-3) / 1e9
     cells_per_s = cells / (ms_align * 1e-3)
     acc = nacc.cpu().numpy()
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
-            traffic = json.load(f).get("verify_bytes_per_launch")
+    traffic, traffic_note = read_traffic(args.traffic, synth.SPECS[args.workload].name)
 
     times = {"align": ms_align, "transfer": ms_transfer, "verify": ms_verify}
     dominant = max(times, key=times.get)
     if dominant == "verify":
-        roof = {"kernel": "tt_verify (verify_stream + verify_sample)", "bound": "hbm", "achieved": round(gbs_verify, 1),
+        roof = {"kernel": "tt_verify (verify_row; verify_stream + verify_sample below 256 streams)",
+                "bound": "hbm", "achieved": round(gbs_verify, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs_verify / HBM_PEAK_GBS, 4),
-                "traffic": traffic, "algorithmic_bytes_per_launch": verify_bytes}
+                "traffic": traffic, "traffic_note": traffic_note,
+                "algorithmic_bytes_per_launch": verify_bytes}
     else:
         roof = {"kernel": "dtw_band_wave" if dominant == "align" else "transfer_gather",
                 "bound": "alu" if dominant == "align" else "hbm",
