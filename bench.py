@@ -41,13 +41,12 @@ def band_cells(K, M, w):
 
 
 def verify_source_digest():
-    """sha256 over the sources of the verify kernel: counter figures taken from another
-    version of the kernel are not reported."""
+    """sha256 of the verify kernel's source: counter figures taken from another version of
+    the kernel are not reported."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("verify.hip", "tt_internal.h"):
-        with open(os.path.join(ROOT, "paper_2510_15545_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    with open(os.path.join(ROOT, "paper_2510_15545_amd", "csrc", "verify.hip"), "rb") as fh:
+        h.update(fh.read())
     return h.hexdigest()
 
 

@@ -41,26 +41,24 @@
 //   sink  [64] u32                     target of the stores a lane does not need
 // with WPR = ceil(min(max_m, 2 L + 1) / 16) for the largest band half-width L the
 // bounds allow.
-#include "tt_internal.h"
+#include "dtw_common.h"
+
+#ifndef TT_ALIGN_ROWS
+#define TT_ALIGN_ROWS 1  // 0: short pairs also take the strip kernel
+#endif
 
 namespace tt {
 namespace {
 
-constexpr int kInf = 0x3fffffff;
-constexpr int kWave = 64;
+using dtw::kInf;
+using dtw::kWave;
+using dtw::read_slot;
+using dtw::stage_token;
+using dtw::token_distance;
 constexpr int kNarrow = 128;                     // widest band precomputed into the cost matrix
 constexpr int kCostGroups = (kNarrow + kWave - 1 + 3) / 4 + 1;  // four-step groups of a narrow strip, +1 prefetch
 constexpr int kRowPad = 8;                       // INF entries past column M in the row buffers
 constexpr size_t kLdsLimit = 160 * 1024 - 1024;  // gfx950 LDS per workgroup, less static use
-
-template <int TB>
-struct MaskType {
-    using type = uint32_t;
-};
-template <>
-struct MaskType<64> {
-    using type = uint64_t;
-};
 
 __host__ __device__ inline size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
 
@@ -111,86 +109,6 @@ __host__ __device__ inline LdsPlan plan_lds(int32_t max_k, int32_t max_m, int32_
     off = align16(off + 4 * kWave);
     p.total = off;
     return p;
-}
-
-// High bit of each byte of w that equals the byte broadcast in bc, compressed to 4 bits.
-__device__ __forceinline__ uint32_t byte_match4(uint32_t w, uint32_t bc) {
-    uint32_t t = w ^ bc;
-    uint32_t z = ~(((t & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | t) & 0x80808080u;
-    return (((z >> 7) * 0x00204081u) >> 21) & 0xFu;
-}
-
-// Edit distance between the packed pattern xw (m bytes) and the text bytes in yw (n bytes).
-template <int TB>
-__device__ __forceinline__ int bitparallel_distance(const uint32_t (&xw)[TB / 4], int m,
-                                                    const uint32_t (&yw)[TB / 4], int n) {
-    using M = typename MaskType<TB>::type;
-    if (m == 0) return n;
-    const M lim = (m >= (int)(8 * sizeof(M))) ? ~M(0) : ((M(1) << m) - 1);
-    const M hib = M(1) << (m - 1);
-    M vp = ~M(0), vn = 0;
-    int score = m;
-#pragma unroll
-    for (int k = 0; k < TB; ++k) {
-        if (k < n) {
-            const uint32_t c = (yw[k >> 2] >> (8 * (k & 3))) & 0xFFu;
-            const uint32_t bc = __builtin_amdgcn_perm(0u, c, 0u);  // c in all four bytes
-            M eq = 0;
-#pragma unroll
-            for (int q = 0; q < TB / 4; ++q) eq |= M(byte_match4(xw[q], bc)) << (4 * q);
-            eq &= lim;
-            const M xv = eq | vn;
-            const M xh = (((eq & vp) + vp) ^ vp) | eq;
-            M hp = vn | ~(xh | vp);
-            M hn = vp & xh;
-            score += (hp & hib) ? 1 : 0;
-            score -= (hn & hib) ? 1 : 0;
-            hp = (hp << 1) | M(1);
-            hn = hn << 1;
-            vp = hn | ~(xv | hp);
-            vn = hp & xv;
-        }
-    }
-    return score;
-}
-
-// Edit distance is symmetric: iterate over the shorter token, the longer one is the pattern.
-template <int TB>
-__device__ __forceinline__ int token_distance(const uint32_t (&aw)[TB / 4], int m,
-                                              const uint32_t (&bw)[TB / 4], int n) {
-    const bool swap = n > m;
-    uint32_t pw[TB / 4], tw[TB / 4];
-#pragma unroll
-    for (int q = 0; q < TB / 4; ++q) {
-        pw[q] = swap ? bw[q] : aw[q];
-        tw[q] = swap ? aw[q] : bw[q];
-    }
-    return bitparallel_distance<TB>(pw, swap ? n : m, tw, swap ? m : n);
-}
-
-// Loads, checks and packs token `id` of table v into an LDS slot; false if invalid.
-template <int TB>
-__device__ __forceinline__ bool stage_token(const tt_vocab &v, int32_t id, uint32_t *slot, uint8_t *len_out) {
-    if (id < 0 || id >= v.n_tokens) return false;
-    const int s = v.offsets[id];
-    const int len = v.offsets[id + 1] - s;
-    if (len < 0 || len > v.max_token_bytes || len > TB) return false;
-    uint32_t w[TB / 4];
-#pragma unroll
-    for (int q = 0; q < TB / 4; ++q) w[q] = 0;
-#pragma unroll
-    for (int k = 0; k < TB; ++k)
-        if (k < len) w[k >> 2] |= (uint32_t)v.bytes[s + k] << (8 * (k & 3));
-#pragma unroll
-    for (int q = 0; q < TB / 4; ++q) slot[q] = w[q];
-    *len_out = (uint8_t)len;
-    return true;
-}
-
-template <int TB>
-__device__ __forceinline__ void read_slot(const uint32_t *slot, uint32_t (&w)[TB / 4]) {
-#pragma unroll
-    for (int q = 0; q < TB / 4; ++q) w[q] = slot[q];
 }
 
 // C(i-1, .) from the lane below: DPP wave shift right by one lane; lane 0 gets `fill`.
@@ -536,7 +454,9 @@ size_t align_workspace_bytes(int32_t n_pairs, int32_t max_k, int32_t max_m, int3
 
 int launch_align(const AlignArgs &a, void *workspace, size_t workspace_bytes, hipStream_t stream) {
     const int mt = a.vd.max_token_bytes > a.vt.max_token_bytes ? a.vd.max_token_bytes : a.vt.max_token_bytes;
-    switch (align_token_slot(mt)) {
+    const int tb = align_token_slot(mt);
+    if (TT_ALIGN_ROWS && align_rows_fits(a.max_k, a.max_m)) return launch_align_rows(a, tb, stream);
+    switch (tb) {
         case 8: return launch_tb<8>(a, workspace, workspace_bytes, stream);
         case 16: return launch_tb<16>(a, workspace, workspace_bytes, stream);
         case 32: return launch_tb<32>(a, workspace, workspace_bytes, stream);

@@ -26,6 +26,9 @@ int align_token_slot(int32_t max_token_bytes);  // 8, 16, 32 or 64; 0 if unsuppo
 // Global workspace for the direction codes of finished 64-row strips (0 if max_k <= 64).
 size_t align_workspace_bytes(int32_t n_pairs, int32_t max_k, int32_t max_m, int32_t w);
 int launch_align(const AlignArgs &a, void *workspace, size_t workspace_bytes, hipStream_t stream);
+// Row-scan kernel for short pairs (dtw_rows.hip): used when max_k and max_m are both <= 64.
+bool align_rows_fits(int32_t max_k, int32_t max_m);
+int launch_align_rows(const AlignArgs &a, int tb, hipStream_t stream);
 
 // ---------------------------------------------------------------- transfer (transfer.hip)
 struct TransferArgs {

@@ -34,19 +34,21 @@ def upload(wl):
     return d
 
 
-def gpu_align(wl, d, w=None):
+def gpu_align(wl, d, w=None, bounds=None):
+    """tt_align over the workload; `bounds` = (max_k, max_m) passed instead of the batch's own
+    maxima (larger bounds move short pairs from the row-scan kernel to the strip kernel)."""
     w = wl.w if w is None else w
+    mk, mm = (max(1, wl.max_k), max(1, wl.max_m)) if bounds is None else bounds
     return tt.align(d["vd"], d["vt"], d["draft_ids"], d["draft_off"], d["target_ids"], d["target_off"],
-                    w, max(1, wl.max_k), max(1, wl.max_m),
-                    n_path=tt.path_capacity(wl.draft_off[-1], wl.target_off[-1]))
+                    w, mk, mm, n_path=tt.path_capacity(wl.draft_off[-1], wl.target_off[-1]))
 
 
-def gpu_run(wl, w=None, residual=False, d=None):
+def gpu_run(wl, w=None, residual=False, d=None, bounds=None):
     """align -> transfer -> verify on the GPU; returns host numpy arrays."""
     import torch
 
     d = upload(wl) if d is None else d
-    cost, plen, path, mp = gpu_align(wl, d, w)
+    cost, plen, path, mp = gpu_align(wl, d, w, bounds)
     out = {"cost": cost, "path_len": plen, "path": path, "map": mp}
     if wl.draft_probs is not None:
         q = tt.transfer(wl.v_d, d["draft_ids"], d["draft_off"], d["target_off"], mp, d["draft_probs"])

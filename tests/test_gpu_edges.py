@@ -64,9 +64,11 @@ def test_token_slot_widths(maxlen):
               list(rng.integers(0, len(toks_t), rng.integers(1, 40)))) for _ in range(40)]
     wl = workload(vd, vt, pairs, len(toks_d), len(toks_t))
     for w in (8, -1, 3):
-        g, o = gpu_run(wl, w=w), oracle_run(wl, w=w)
+        o = oracle_run(wl, w=w)
+        g = gpu_run(wl, w=w)  # row-scan kernel
         compare_align(wl, g, o)
         compare_verify(g, o)
+        compare_align(wl, gpu_run(wl, w=w, bounds=(65, 65)), o)  # strip kernel
 
 
 def test_strips_longer_than_a_wave():
@@ -81,6 +83,34 @@ def test_strips_longer_than_a_wave():
     for w in (4, 8, 16, -1, 0, 70):
         print(f"[case] strips w={w}", flush=True)
         compare_align(wl, gpu_run(wl, w=w), oracle_run(wl, w=w))
+
+
+@pytest.mark.parametrize("kernel", ["rows", "strips"])
+def test_short_pair_extremes(kernel):
+    """Pairs at the row-scan kernel's limits (K, M in {1, 63, 64}), through both alignment
+    kernels: bounds of 64 select the row-scan kernel, a bound of 65 the strip kernel."""
+    rng = np.random.default_rng(11)
+    toks = random_tokens(rng, 120, 1, 6)
+    v = vocab_of(toks)
+    shapes = ((64, 64), (1, 64), (64, 1), (1, 1), (63, 64), (64, 63), (64, 30), (30, 64), (2, 64), (64, 2))
+    pairs = [(list(rng.integers(0, len(toks), k)), list(rng.integers(0, len(toks), m))) for k, m in shapes]
+    wl = workload(v, v, pairs, len(toks), len(toks), probs=False)
+    bounds = (64, 64) if kernel == "rows" else (65, 64)
+    for w in (0, 1, 4, 8, -1, 70):
+        print(f"[case] short pair extremes kernel={kernel} w={w}", flush=True)
+        compare_align(wl, gpu_run(wl, w=w, bounds=bounds), oracle_run(wl, w=w))
+
+
+@pytest.mark.parametrize("c", [2, 3, 5])
+def test_strip_kernel_on_benchmark_shapes(c):
+    """The strip kernel stays bit-exact on the short pairs the row-scan kernel normally takes."""
+    from paper_2510_15545_amd import synth
+
+    print(f"[case] strip kernel on workload {c}", flush=True)
+    wl = synth.make(c, n_streams=16)
+    for w in (8, -1):
+        g = gpu_run(wl, w=w, bounds=(max(65, wl.max_k), max(65, wl.max_m)))
+        compare_align(wl, g, oracle_run(wl, w=w))
 
 
 def test_sentinel_pairs_and_streams():
