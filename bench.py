@@ -1,14 +1,16 @@
 """Benchmark of the TokenTiming verification hot path on one MI355X.
 
-One step = tt_align + tt_transfer + tt_verify over one batch of synthetic input
-(default: 256 streams, K=8 draft tokens, V_d=128,256, V_t=151,936, w=8).  Inputs
-are resident in HBM before timing starts.  The probability rows are replicated
-(--replicas) and consecutive steps read different replicas, so the 256 MB
-Infinity Cache cannot serve a row from the previous step.
+One step = the whole verification path (alignment, transfer, verification) over one
+batch of synthetic input (default: 256 streams, K=8 draft tokens, V_d=128,256,
+V_t=151,936, w=8), issued as tt_step (one fused kernel when the batch fits it) or, with
+--path calls, as tt_align + tt_transfer + tt_verify.  Inputs are resident in HBM before
+timing starts.  The probability rows are replicated (--replicas) and consecutive steps
+read different replicas, so the 256 MB Infinity Cache cannot serve a row from the
+previous step.
 
-Prints one JSON line: verified draft tokens/s for the step, per-kernel times, DTW
-cells/s, verify HBM GB/s against the 8 TB/s peak, and the CPU oracle timed on the
-host cores on a bounded sample of the same workload.
+Prints one JSON line: verified draft tokens/s for the step, per-call times, DTW cells/s,
+the dominant kernel against its roofline, and the CPU oracle timed on the host cores on
+a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -24,8 +26,6 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# int32 VALU lane-ops: 256 CUs x 4 SIMDs x 16 lanes per cycle x 2.4 GHz
-VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 
 
 def band_cells(K, M, w):
@@ -40,19 +40,28 @@ def band_cells(K, M, w):
     return total
 
 
-def verify_source_digest():
-    """sha256 of the verify kernel's source: counter figures taken from another version of
-    the kernel are not reported."""
+def source_digest(files):
+    """sha256 of kernel sources: counter figures taken from another version of the kernel
+    are not reported."""
     import hashlib
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2510_15545_amd", "csrc", "verify.hip"), "rb") as fh:
-        h.update(fh.read())
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2510_15545_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()
 
 
-def read_traffic(path, workload):
-    """HBM bytes per verify launch from a counter summary (key: value lines), or None when
-    the file is missing, covers another workload, or was taken from other kernel sources."""
+# sources each measured kernel is built from (a change to any of them voids its counters)
+KERNEL_SOURCES = {
+    "step_fused": ("step.hip", "dtw_rows.h", "dtw_common.h", "verify_core.h"),
+    "verify_row": ("verify.hip", "verify_core.h"),
+}
+
+
+def read_traffic(path, workload, kernel):
+    """HBM bytes per launch of `kernel` from a counter summary (key: value lines), or None
+    when the file is missing, covers another workload or kernel, or was taken from other
+    kernel sources."""
     if not path or not os.path.exists(path):
         return None, "no counter summary"
     kv = {}
@@ -63,8 +72,10 @@ def read_traffic(path, workload):
                 kv[k.strip()] = v.strip()
     if kv.get("workload") != workload:
         return None, "counters cover workload %r" % kv.get("workload")
-    if kv.get("source_sha256") != verify_source_digest():
-        return None, "verify kernel changed since the counters were taken"
+    if kv.get("kernel") != kernel:
+        return None, "counters cover kernel %r" % kv.get("kernel")
+    if kv.get("source_sha256") != source_digest(KERNEL_SOURCES[kernel]):
+        return None, "kernel changed since the counters were taken"
     return int(kv["traffic_bytes_per_launch"]), "FETCH_SIZE x %s + WRITE_SIZE x %s" % (
         kv.get("fetch_scale"), kv.get("write_scale"))
 
@@ -78,15 +89,18 @@ def parse():
     ap.add_argument("--streams", type=int, default=None, help="override the stream count")
     ap.add_argument("--w", type=int, default=8)
     ap.add_argument("--replicas", type=int, default=4)
+    ap.add_argument("--path", choices=["step", "calls"], default="step",
+                    help="step: one tt_step call per step; calls: tt_align + tt_transfer + tt_verify")
     ap.add_argument("--eager", action="store_true", help="launch every call from Python (no HIP graph)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="also run one plain device copy of this many MiB (counter calibration)")
-    ap.add_argument("--only", choices=["verify", "align", "transfer"], default=None,
+    ap.add_argument("--only", choices=["step", "verify", "align", "transfer"], default=None,
                     help="after the timed steps, loop only this call (for profiler passes)")
-    ap.add_argument("--traffic", type=str, default=os.path.join(ROOT, "profiles", "tt_verify_counters.txt"),
-                    help="counter summary with the measured HBM bytes per verify launch")
+    ap.add_argument("--traffic", type=str, default=None,
+                    help="counter summary with the measured HBM bytes per launch of the dominant kernel "
+                         "(default: profiles/<kernel>_counters.txt)")
     return ap.parse_args()
 
 
@@ -117,19 +131,22 @@ def main():
 
     # alignment inputs (the long pairs for workload 4, the stream batch otherwise)
     A = wl0
+    mtb = max(A.vocab_d.max_len, A.vocab_t.max_len)
     vd = tt.Vocab.from_host(A.vocab_d.data, A.vocab_d.offsets, A.vocab_d.max_len, dev)
     vt = tt.Vocab.from_host(A.vocab_t.data, A.vocab_t.offsets, A.vocab_t.max_len, dev)
     a_di, a_do, a_ti, a_to = t(A.draft_ids), t(A.draft_off), t(A.target_ids), t(A.target_off)
     a_maxk, a_maxm = max(1, A.max_k), max(1, A.max_m)
     npath = tt.path_capacity(A.draft_off[-1], A.target_off[-1])
-    a_ws = tt.align_workspace(A.n, a_maxk, a_maxm, args.w, max(A.vocab_d.max_len, A.vocab_t.max_len), dev)
+    a_ws = tt.align_workspace(A.n, a_maxk, a_maxm, args.w, mtb, dev)
     a_out = tt.align(vd, vt, a_di, a_do, a_ti, a_to, args.w, a_maxk, a_maxm, n_path=npath, workspace=a_ws)
 
     S = stage
-    s_di, s_do, s_to = t(S.draft_ids), t(S.draft_off), t(S.target_off)
+    s_di, s_do, s_ti, s_to = t(S.draft_ids), t(S.draft_off), t(S.target_ids), t(S.target_off)
     s_vi = t(S.verify_ids)
+    s_maxk, s_maxm = max(1, S.max_k), max(1, S.max_m)
+    s_npath = tt.path_capacity(S.draft_off[-1], S.target_off[-1])
     if args.workload == 4:  # the probability stage aligns its own short streams
-        s_out = tt.align(vd, vt, s_di, s_do, t(S.target_ids), s_to, args.w, S.max_k, S.max_m)
+        s_out = tt.align(vd, vt, s_di, s_do, s_ti, s_to, args.w, s_maxk, s_maxm, n_path=s_npath)
     else:
         s_out = a_out
     R = max(1, args.replicas)
@@ -143,8 +160,15 @@ def main():
     nacc = torch.empty(n, dtype=torch.int32, device=dev)
     tok = torch.empty(n, dtype=torch.int32, device=dev)
     ws = tt.verify_workspace(n, S.v_t, dev)
+    # tt_step aligns and verifies the same target ids: the long-pair workload's probability
+    # stage indexes its rows with other ids, so it keeps the three calls
+    step_ok = args.path == "step" and args.workload != 4
+    if step_ok:
+        st_ws = tt.step_workspace(n, S.v_t, s_maxk, s_maxm, args.w, mtb, dev)
+        st_out = (torch.empty(n, dtype=torch.int32, device=dev), torch.empty(n, dtype=torch.int32, device=dev),
+                  torch.empty(max(1, s_npath), dtype=torch.int32, device=dev),
+                  torch.empty(max(1, int(S.target_off[-1])), dtype=torch.int32, device=dev), q, nacc, tok, None)
     torch.cuda.synchronize()
-    host_rows_bytes = S.target_probs.nbytes
     del wl0  # keep host memory for the CPU leg only where needed
 
     def do_align():
@@ -154,70 +178,22 @@ def main():
         tt.transfer(S.v_d, s_di, s_do, s_to, s_out[3], draft_probs, out=q)
 
     def do_verify(r):
-        tt.verify(S.v_t, s_vi, s_to, q, target_probs[r], ua, us, max(0, S.max_m), workspace=ws,
-                  out=(nacc, tok, None))
+        tt.verify(S.v_t, s_vi, s_to, q, target_probs[r], ua, us, s_maxm, workspace=ws, out=(nacc, tok, None))
 
-    def step(r):
+    def do_step(r):
+        tt.step(vd, vt, S.v_d, S.v_t, s_di, s_do, s_ti, s_to, args.w, s_maxk, s_maxm, draft_probs,
+                target_probs[r], ua, us, workspace=st_ws, out=st_out)
+
+    def calls(r):
         do_align()
         if args.workload == 4:
-            tt.align(vd, vt, s_di, s_do, t_short_ids, s_to, args.w, S.max_k, S.max_m, out=s_out)
+            tt.align(vd, vt, s_di, s_do, s_ti, s_to, args.w, s_maxk, s_maxm, out=s_out)
         do_transfer()
         do_verify(r)
 
-    t_short_ids = t(S.target_ids) if args.workload == 4 else None
+    step = do_step if step_ok else calls
 
-    for i in range(args.warmup):
-        step(i % R)
-    torch.cuda.synchronize()
-
-    graphs = None
-    if not args.eager:
-        graphs = []
-        cap = torch.cuda.Stream()
-        cap.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(cap):
-            for r in range(R):
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g, stream=cap):
-                    step(r)
-                graphs.append(g)
-        torch.cuda.current_stream().wait_stream(cap)
-        for r in range(R):
-            graphs[r].replay()
-        torch.cuda.synchronize()
-
-    def run_steps(k):
-        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        s0.record()
-        for i in range(k):
-            if graphs is not None:
-                graphs[i % R].replay()
-            else:
-                step(i % R)
-        s1.record()
-        torch.cuda.synchronize()
-        return s0.elapsed_time(s1) / k
-
-    ms_step = run_steps(args.steps)
-    ms_eager = None
-    if graphs is not None:
-        graphs_saved, graphs = graphs, None
-        ms_eager = run_steps(max(20, args.steps // 4))
-        graphs = graphs_saved
-
-    # per-call averages: each call alone, 20 back to back inside one HIP graph (rotating
-    # replicas for verify), replayed; events on the stream the graph runs on
-    def kernel_ms(fn, k=20, reps=10):
-        if args.eager:
-            s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda.synchronize()
-            s0.record()
-            for i in range(k * reps):
-                fn(i)
-            s1.record()
-            torch.cuda.synchronize()
-            return s0.elapsed_time(s1) / (k * reps)
+    def graph_of(fn, k):
         g = torch.cuda.CUDAGraph()
         cap = torch.cuda.Stream()
         cap.wait_stream(torch.cuda.current_stream())
@@ -228,6 +204,56 @@ def main():
         torch.cuda.current_stream().wait_stream(cap)
         g.replay()
         torch.cuda.synchronize()
+        return g
+
+    def run_steps(fn, k):
+        """ms per step over k steps: one HIP graph per replica, replayed in turn."""
+        graphs = None if args.eager else [graph_of(lambda i, r=r: fn(r), 1) for r in range(R)]
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s0.record()
+        for i in range(k):
+            if graphs is None:
+                fn(i % R)
+            else:
+                graphs[i % R].replay()
+        s1.record()
+        torch.cuda.synchronize()
+        return s0.elapsed_time(s1) / k
+
+    for i in range(args.warmup):
+        step(i % R)
+        if step_ok:
+            calls(i % R)
+    torch.cuda.synchronize()
+
+    ms_step = run_steps(step, args.steps)
+    ms_calls = run_steps(calls, args.steps) if step_ok else ms_step
+    step_outputs = None
+    if step_ok:  # the fused path's results must equal the three calls' on this input
+        do_step(0)
+        torch.cuda.synchronize()
+        step_outputs = (nacc.clone(), tok.clone(), st_out[0].clone())
+        calls(0)
+        torch.cuda.synchronize()
+        if not (torch.equal(step_outputs[0], nacc) and torch.equal(step_outputs[1], tok) and
+                torch.equal(step_outputs[2], s_out[0])):
+            print("tt_step and the three calls disagree", file=sys.stderr)
+            sys.exit(3)
+
+    # per-call averages: each call alone, 20 back to back inside one HIP graph (rotating
+    # replicas), replayed; HIP events on the stream the graph runs on
+    def kernel_ms(fn, k=20, reps=10):
+        if args.eager:
+            s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            s0.record()
+            for i in range(k * reps):
+                fn(i)
+            s1.record()
+            torch.cuda.synchronize()
+            return s0.elapsed_time(s1) / (k * reps)
+        g = graph_of(fn, k)
         s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s0.record()
         for _ in range(reps):
@@ -236,15 +262,14 @@ def main():
         torch.cuda.synchronize()
         return s0.elapsed_time(s1) / (k * reps)
 
-    ms_verify = kernel_ms(lambda i: do_verify(i % R))
-    ms_align = kernel_ms(lambda i: do_align())
-    ms_transfer = kernel_ms(lambda i: do_transfer())
-    if args.only == "verify":
-        kernel_ms(lambda i: do_verify(i % R), 200)
-    elif args.only == "align":
-        kernel_ms(lambda i: do_align(), 200)
-    elif args.only == "transfer":
-        kernel_ms(lambda i: do_transfer(), 200)
+    times = {"align": kernel_ms(lambda i: do_align()), "transfer": kernel_ms(lambda i: do_transfer()),
+             "verify": kernel_ms(lambda i: do_verify(i % R))}
+    if step_ok:
+        times["step"] = kernel_ms(lambda i: do_step(i % R))
+    if args.only:
+        fn = {"step": lambda i: do_step(i % R), "verify": lambda i: do_verify(i % R),
+              "align": lambda i: do_align(), "transfer": lambda i: do_transfer()}[args.only]
+        kernel_ms(fn, 200)
 
     if args.copy_calib_mb:
         src = torch.empty(args.copy_calib_mb * (1 << 20) // 4, dtype=torch.float32, device=dev).fill_(1.0)
@@ -257,27 +282,42 @@ def main():
     Ka = np.diff(A.draft_off)
     Ma = np.diff(A.target_off)
     cells = band_cells(Ka, Ma, args.w)
+    Ks = np.diff(S.draft_off)
     m_s = np.diff(S.target_off)
     verify_bytes = int(n * 4 * S.v_t + 16 * int(m_s.sum()) + 12 * n)
     draft_tokens = int(S.draft_off[-1])
-    gbs_verify = verify_bytes / (ms_verify * 1e-3) / 1e9
-    cells_per_s = cells / (ms_align * 1e-3)
     acc = nacc.cpu().numpy()
-    traffic, traffic_note = read_traffic(args.traffic, synth.SPECS[args.workload].name)
+    gbs_verify = verify_bytes / (times["verify"] * 1e-3) / 1e9
+    cells_per_s = cells / (times["align"] * 1e-3)
+    wl_name = synth.SPECS[args.workload].name
 
-    times = {"align": ms_align, "transfer": ms_transfer, "verify": ms_verify}
-    dominant = max(times, key=times.get)
-    if dominant == "verify":
-        roof = {"kernel": "tt_verify (verify_row; verify_stream + verify_sample below 256 streams)",
-                "bound": "hbm", "achieved": round(gbs_verify, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs_verify / HBM_PEAK_GBS, 4),
-                "traffic": traffic, "traffic_note": traffic_note,
-                "algorithmic_bytes_per_launch": verify_bytes}
+    if step_ok and synth_fits_fused(S):
+        # algorithmic bytes of one fused launch: the verify stream (one row per stream, t_j,
+        # P_t(t_j), u_j per position, u_sample, n_accepted, out_token), the alignment reads
+        # (offsets, ids, the tokens' table offsets and bytes, one draft probability per
+        # draft token) and its writes (cost, path_len, path, map, q)
+        plen = st_out[1].cpu().numpy()
+        tok_bytes = (np.diff(A.vocab_d.offsets)[S.draft_ids].sum() + np.diff(A.vocab_t.offsets)[S.target_ids].sum())
+        step_bytes = int(n * 4 * S.v_t + 12 * int(m_s.sum()) + 12 * n + 16 * n + 8 * int(Ks.sum() + m_s.sum()) +
+                         int(tok_bytes) + 8 * int(Ks.sum()) + 8 * n + 8 * int(plen.sum()) +
+                         8 * int(m_s.sum()))
+        kname, kbytes, kms = "step_fused", step_bytes, times["step"]
     else:
-        roof = {"kernel": "dtw_band_wave" if dominant == "align" else "transfer_gather",
-                "bound": "alu" if dominant == "align" else "hbm",
-                "achieved": round(cells_per_s / 1e9, 3), "unit": "Gcells/s", "peak": None, "frac": None,
-                "traffic": None, "note": "see DESIGN.md for the ALU roofline of the alignment kernel"}
+        kname, kbytes, kms = "verify_row" if n >= 256 else "verify_stream + verify_sample", verify_bytes, \
+            times["verify"]
+    dominant_calls = max(("align", "transfer", "verify"), key=lambda k: times[k])
+    traffic_path = args.traffic or os.path.join(ROOT, "profiles", kname.split()[0] + "_counters.txt")
+    traffic, traffic_note = read_traffic(traffic_path, wl_name, kname) if kname in KERNEL_SOURCES else \
+        (None, "no counters for this kernel")
+    if kname == "step_fused" or dominant_calls == "verify":
+        gbs = kbytes / (kms * 1e-3) / 1e9
+        roof = {"kernel": kname, "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic, "traffic_note": traffic_note,
+                "algorithmic_bytes_per_launch": kbytes, "launch_us": round(kms * 1e3, 2)}
+    else:
+        roof = {"kernel": "dtw_band_wave", "bound": "alu", "achieved": round(cells_per_s / 1e9, 3),
+                "unit": "Gcells/s", "peak": None, "frac": None, "traffic": None,
+                "note": "see DESIGN.md for the ALU roofline of the alignment kernel"}
 
     result = {
         "metric": "verified draft tokens/s + DTW cells/s at V_t=151,936; verify HBM GB/s vs peak",
@@ -287,12 +327,13 @@ def main():
         "ms_per_step": round(ms_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32+i64", "data": "synthetic",
-        "config": {"workload": synth.SPECS[args.workload].name, "streams": n,
+        "config": {"workload": wl_name, "streams": n,
                    "draft_tokens_per_step": draft_tokens, "target_positions": int(m_s.sum()),
                    "v_t": S.v_t, "v_d": S.v_d, "w": args.w, "replicas": R,
-                   "launch": "eager" if graphs is None else "hip-graph"},
+                   "path": "tt_step" if step_ok else "tt_align+tt_transfer+tt_verify",
+                   "launch": "eager" if args.eager else "hip-graph"},
+        "three_call_ms_per_step": round(ms_calls, 5),
         "kernels_ms": {k: round(v, 5) for k, v in times.items()},
-        "eager_ms_per_step": None if ms_eager is None else round(ms_eager, 5),
         "dtw": {"band_cells": cells, "cells_per_s": round(cells_per_s, 1),
                 "full_cells": int((Ka * Ma).sum())},
         "verify": {"GBps": round(gbs_verify, 1), "frac_of_peak": round(gbs_verify / HBM_PEAK_GBS, 4),
@@ -303,8 +344,15 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(args, S, A, nacc, tok, s_out, a_out)
+        nacc_step = step_outputs[0] if step_outputs is not None else nacc
+        tok_step = step_outputs[1] if step_outputs is not None else tok
+        result["cpu_baseline"] = cpu_baseline(args, S, A, nacc_step, tok_step, s_out, a_out)
     print(json.dumps(result), flush=True)
+
+
+def synth_fits_fused(S):
+    """The fused kernel's shape conditions (mirrors the library's dispatch rule)."""
+    return S.max_k <= 64 and S.max_m <= 64 and S.n >= 256 and (S.v_t + 1023) // 1024 * 8 <= 64 * 1024
 
 
 def cpu_baseline(args, S, A, nacc, tok, s_out, a_out):

@@ -170,8 +170,10 @@ int tt_verify_workspace_size(int32_t n_streams, int32_t v_t, size_t *bytes);
  * workspace: device memory of tt_verify_workspace_size bytes (per-chunk Q62
  * sums and per-stream scratch); it needs no initialisation.  Calls that overlap
  * in time must not share it.
- * Launches: one streaming kernel over B x S workgroups, one sampling kernel over
- * B workgroups, and (if residual != NULL) one kernel writing the residual rows.
+ * Launches: with at least 256 streams (one per compute unit) and rows of at most
+ * 8M floats, one kernel with a workgroup per stream; otherwise one streaming kernel
+ * over B x S workgroups and one sampling kernel.  If residual != NULL, one more
+ * kernel writes the residual rows.
  */
 int tt_verify(int32_t n_streams, int32_t v_t,
               const int32_t *target_ids, const int32_t *target_off, const float *q,
@@ -179,6 +181,41 @@ int tt_verify(int32_t n_streams, int32_t v_t,
               const float *u_accept, const float *u_sample, int32_t max_m,
               int32_t *n_accepted, int32_t *out_token, float *residual,
               void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Workspace bytes tt_step needs: the larger of tt_align_workspace_size and
+ * tt_verify_workspace_size for the same arguments (the two stages run one after
+ * the other and share it).
+ */
+int tt_step_workspace_size(int32_t n_streams, int32_t v_t, int32_t max_k, int32_t max_m, int32_t w,
+                           int32_t max_token_bytes, size_t *bytes);
+
+/*
+ * tt_step -- the whole verification path of one decode step: tt_align, then
+ * tt_transfer, then tt_verify, with the same arguments and the same outputs as
+ * those three calls made in sequence on `stream` (the target ids that are
+ * aligned are also the ids verified against the target rows, and max_m bounds
+ * both stages).  Sec. 4.1 / Alg. 1 / App. H (alignment), Alg. 2 / App. A.2
+ * (transfer), Sec. 3, Sec. 4.2.2-4.2.3, App. D Alg. 4 (verification).
+ *
+ * When max_k <= 64, max_m <= 64, n_streams >= 256 and the verify rows have at
+ * most 8M floats, the path runs as ONE kernel with a workgroup per stream: the
+ * pair is aligned in LDS, map and q never leave the chip before they are used,
+ * and the selected target row is read once.  Otherwise it issues the three
+ * calls' kernels in order.  Every output array (cost, path_len, path, map, q,
+ * n_accepted, out_token, residual) is written exactly as by the three calls.
+ * workspace: tt_step_workspace_size bytes, no initialisation needed.
+ */
+int tt_step(const tt_vocab *vd, const tt_vocab *vt, int32_t n_streams, int32_t v_d, int32_t v_t,
+            const int32_t *draft_ids, const int32_t *draft_off,
+            const int32_t *target_ids, const int32_t *target_off,
+            int32_t max_k, int32_t max_m, int32_t w,
+            const float *draft_probs, int64_t draft_ld,
+            const float *target_probs, int64_t target_ld,
+            const float *u_accept, const float *u_sample,
+            int32_t *cost, int32_t *path_len, int32_t *path, int32_t *map, float *q,
+            int32_t *n_accepted, int32_t *out_token, float *residual,
+            void *workspace, size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

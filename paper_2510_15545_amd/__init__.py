@@ -61,6 +61,11 @@ def lib():
         L.tt_verify_workspace_size.restype = ctypes.c_int
         L.tt_verify.argtypes = [i32, i32, P, P, P, P, i64, P, P, i32, P, P, P, P, sz, P]
         L.tt_verify.restype = ctypes.c_int
+        L.tt_step_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz)]
+        L.tt_step_workspace_size.restype = ctypes.c_int
+        L.tt_step.argtypes = [VP, VP, i32, i32, i32, P, P, P, P, i32, i32, i32, P, i64, P, i64, P, P,
+                              P, P, P, P, P, P, P, P, P, sz, P]
+        L.tt_step.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -221,4 +226,56 @@ def verify(v_t: int, target_ids, target_off, q, target_probs, u_accept, u_sample
                          _ptr(tok, i32, "out_token"), _ptr(res, f32, "residual", allow_none=True),
                          ctypes.c_void_p(workspace.data_ptr()), int(workspace.numel()), _stream_handle(stream))
     _check(st, "tt_verify")
+    return out
+
+
+def step_workspace(n_streams: int, v_t: int, max_k: int, max_m: int, w: int, max_token_bytes: int,
+                   device="cuda"):
+    """A workspace for tt_step (reusable by calls that do not overlap in time)."""
+    torch = _torch()
+    n = ctypes.c_size_t(0)
+    _check(lib().tt_step_workspace_size(int(n_streams), int(v_t), int(max_k), int(max_m), int(w),
+                                        int(max_token_bytes), ctypes.byref(n)), "tt_step_workspace_size")
+    return torch.empty(max(1, n.value), dtype=torch.uint8, device=device)
+
+
+def step(vd: Vocab, vt: Vocab, v_d: int, v_t: int, draft_ids, draft_off, target_ids, target_off, w: int,
+         max_k: int, max_m: int, draft_probs, target_probs, u_accept, u_sample, n_path: int | None = None,
+         workspace=None, residual: bool = False, out=None, stream=None):
+    """tt_step (align + transfer + verify).  Returns
+    (cost, path_len, path, map, q, n_accepted, out_token, residual or None)."""
+    torch = _torch()
+    i32, f32 = torch.int32, torch.float32
+    n = int(draft_off.numel()) - 1
+    dev = draft_off.device
+    for name, t in (("draft_probs", draft_probs), ("target_probs", target_probs)):
+        if t.dim() != 2 or t.stride(1) != 1 or t.dtype != f32 or not t.is_cuda:
+            raise ValueError(name + " must be a 2-D row-major float32 device tensor")
+    if workspace is None:
+        workspace = step_workspace(n, v_t, max_k, max_m, w, max(vd.max_token_bytes, vt.max_token_bytes), dev)
+    if out is None:
+        if n_path is None:
+            n_path = path_capacity(draft_off[-1].item(), target_off[-1].item())
+        m_total = max(1, int(target_ids.numel()))
+        out = (torch.empty(n, dtype=i32, device=dev), torch.empty(n, dtype=i32, device=dev),
+               torch.empty(max(1, n_path), dtype=i32, device=dev), torch.empty(m_total, dtype=i32, device=dev),
+               torch.empty(m_total, dtype=f32, device=dev), torch.empty(n, dtype=i32, device=dev),
+               torch.empty(n, dtype=i32, device=dev),
+               torch.zeros((n, target_probs.stride(0)), dtype=f32, device=dev) if residual else None)
+    cost, plen, path, mp, q, nacc, tok, res = out
+    di = draft_ids if draft_ids.numel() else torch.zeros(1, dtype=i32, device=dev)
+    ti = target_ids if target_ids.numel() else torch.zeros(1, dtype=i32, device=dev)
+    ua = u_accept if u_accept.numel() else torch.zeros(1, dtype=f32, device=dev)
+    st = lib().tt_step(ctypes.byref(vd._c), ctypes.byref(vt._c), n, int(v_d), int(v_t),
+                       _ptr(di, i32, "draft_ids"), _ptr(draft_off, i32, "draft_off"),
+                       _ptr(ti, i32, "target_ids"), _ptr(target_off, i32, "target_off"),
+                       int(max_k), int(max_m), int(w),
+                       ctypes.c_void_p(draft_probs.data_ptr()), int(draft_probs.stride(0)),
+                       ctypes.c_void_p(target_probs.data_ptr()), int(target_probs.stride(0)),
+                       _ptr(ua, f32, "u_accept"), _ptr(u_sample, f32, "u_sample"),
+                       _ptr(cost, i32, "cost"), _ptr(plen, i32, "path_len"), _ptr(path, i32, "path"),
+                       _ptr(mp, i32, "map"), _ptr(q, f32, "q"), _ptr(nacc, i32, "n_accepted"),
+                       _ptr(tok, i32, "out_token"), _ptr(res, f32, "residual", allow_none=True),
+                       ctypes.c_void_p(workspace.data_ptr()), int(workspace.numel()), _stream_handle(stream))
+    _check(st, "tt_step")
     return out

@@ -76,20 +76,29 @@ __device__ __forceinline__ int token_distance(const uint32_t (&aw)[TB / 4], int 
 }
 
 // Loads, checks and packs token `id` of table v into an LDS slot; false if invalid.
+// The token's bytes come from the aligned dwords that overlap them, all loads issued
+// together (a dword holding one of the token's bytes lies in the same page as that byte).
 template <int TB>
 __device__ __forceinline__ bool stage_token(const tt_vocab &v, int32_t id, uint32_t *slot, uint8_t *len_out) {
     if (id < 0 || id >= v.n_tokens) return false;
     const int s = v.offsets[id];
     const int len = v.offsets[id + 1] - s;
     if (len < 0 || len > v.max_token_bytes || len > TB) return false;
-    uint32_t w[TB / 4];
+    const uint8_t *bp = v.bytes + s;
+    const int mis = (int)(reinterpret_cast<uintptr_t>(bp) & 3u);
+    const uint32_t sh = (uint32_t)mis * 8;
+    const int nd = len > 0 ? ((mis + len - 1) >> 2) + 1 : 0;  // dwords touched, <= TB / 4 + 1
+    const uint32_t *d = reinterpret_cast<const uint32_t *>(bp - mis);
+    uint32_t raw[TB / 4 + 1];
 #pragma unroll
-    for (int q = 0; q < TB / 4; ++q) w[q] = 0;
+    for (int q = 0; q < TB / 4 + 1; ++q) raw[q] = q < nd ? d[q] : 0u;
 #pragma unroll
-    for (int k = 0; k < TB; ++k)
-        if (k < len) w[k >> 2] |= (uint32_t)v.bytes[s + k] << (8 * (k & 3));
-#pragma unroll
-    for (int q = 0; q < TB / 4; ++q) slot[q] = w[q];
+    for (int q = 0; q < TB / 4; ++q) {
+        const uint32_t word = __builtin_amdgcn_alignbit(raw[q + 1], raw[q], sh);
+        const int keep = len - 4 * q;  // bytes of the token in this word
+        const uint32_t mask = keep >= 4 ? ~0u : (keep <= 0 ? 0u : ((1u << (8 * keep)) - 1u));
+        slot[q] = word & mask;
+    }
     *len_out = (uint8_t)len;
     return true;
 }

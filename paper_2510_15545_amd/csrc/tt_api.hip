@@ -3,6 +3,10 @@
 // host-visible argument is invalid.
 #include "tt_internal.h"
 
+#ifndef TT_STEP_FUSED
+#define TT_STEP_FUSED 1  // 0: tt_step always issues the three calls' kernels
+#endif
+
 namespace {
 
 constexpr int32_t kMaxAlignLen = 4096;   // bound on K_b / M_b accepted by tt_align
@@ -122,6 +126,86 @@ int tt_verify(int32_t n_streams, int32_t v_t, const int32_t *target_ids, const i
     a.workspace = workspace;
     a.workspace_bytes = workspace_bytes;
     return tt::launch_verify(a, static_cast<hipStream_t>(stream));
+}
+
+int tt_step_workspace_size(int32_t n_streams, int32_t v_t, int32_t max_k, int32_t max_m, int32_t w,
+                           int32_t max_token_bytes, size_t *bytes) {
+    if (bytes == nullptr || v_t < 1 || max_m > kMaxVerifyLen) return TT_EINVAL;
+    size_t ab = 0, vb = 0;
+    const int st = tt_align_workspace_size(n_streams, max_k, max_m, w, max_token_bytes, &ab);
+    if (st != TT_OK) return st;
+    if (tt_verify_workspace_size(n_streams, v_t, &vb) != TT_OK) return TT_EINVAL;
+    *bytes = ab > vb ? ab : vb;
+    return TT_OK;
+}
+
+int tt_step(const tt_vocab *vd, const tt_vocab *vt, int32_t n_streams, int32_t v_d, int32_t v_t,
+            const int32_t *draft_ids, const int32_t *draft_off, const int32_t *target_ids,
+            const int32_t *target_off, int32_t max_k, int32_t max_m, int32_t w, const float *draft_probs,
+            int64_t draft_ld, const float *target_probs, int64_t target_ld, const float *u_accept,
+            const float *u_sample, int32_t *cost, int32_t *path_len, int32_t *path, int32_t *map, float *q,
+            int32_t *n_accepted, int32_t *out_token, float *residual, void *workspace, size_t workspace_bytes,
+            void *stream) {
+    // the union of the three calls' host checks, all before anything is launched
+    if (!vocab_ok(vd) || !vocab_ok(vt) || n_streams < 0) return TT_EINVAL;
+    if (max_k < 1 || max_m < 1 || max_k > kMaxAlignLen || max_m > kMaxAlignLen) return TT_EINVAL;
+    if (v_d < 1 || draft_ld < v_d || v_t < 1 || target_ld < v_t || max_m > kMaxVerifyLen) return TT_EINVAL;
+    if (n_streams == 0) return TT_OK;
+    if (!draft_ids || !draft_off || !target_ids || !target_off || !cost || !path_len || !path || !map ||
+        !draft_probs || !q || !target_probs || !u_accept || !u_sample || !n_accepted || !out_token)
+        return TT_EINVAL;
+    const int32_t mt = vd->max_token_bytes > vt->max_token_bytes ? vd->max_token_bytes : vt->max_token_bytes;
+    const int tb = tt::align_token_slot(mt);
+    if (tb == 0 || tt::align_lds_bytes(max_k, max_m, w, tb) == 0) return TT_EUNSUPPORTED;
+    size_t need = 0;
+    if (tt_step_workspace_size(n_streams, v_t, max_k, max_m, w, mt, &need) != TT_OK) return TT_EUNSUPPORTED;
+    if (workspace == nullptr || workspace_bytes < need) return TT_EWORKSPACE;
+
+    tt::StepArgs s;
+    s.al.vd = *vd;
+    s.al.vt = *vt;
+    s.al.n_pairs = n_streams;
+    s.al.draft_ids = draft_ids;
+    s.al.draft_off = draft_off;
+    s.al.target_ids = target_ids;
+    s.al.target_off = target_off;
+    s.al.max_k = max_k;
+    s.al.max_m = max_m;
+    s.al.w = w;
+    s.al.cost = cost;
+    s.al.path_len = path_len;
+    s.al.path = path;
+    s.al.map = map;
+    s.tr.n_pairs = n_streams;
+    s.tr.v_d = v_d;
+    s.tr.draft_ids = draft_ids;
+    s.tr.draft_off = draft_off;
+    s.tr.target_off = target_off;
+    s.tr.map = map;
+    s.tr.draft_probs = draft_probs;
+    s.tr.draft_ld = draft_ld;
+    s.tr.q = q;
+    s.ve.n_streams = n_streams;
+    s.ve.v_t = v_t;
+    s.ve.target_ids = target_ids;
+    s.ve.target_off = target_off;
+    s.ve.q = q;
+    s.ve.target_probs = target_probs;
+    s.ve.target_ld = target_ld;
+    s.ve.u_accept = u_accept;
+    s.ve.u_sample = u_sample;
+    s.ve.max_m = max_m;
+    s.ve.n_accepted = n_accepted;
+    s.ve.out_token = out_token;
+    s.ve.residual = residual;
+    s.ve.workspace = workspace;
+    s.ve.workspace_bytes = workspace_bytes;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (TT_STEP_FUSED && tt::step_fused_fits(s, tb)) return tt::launch_step_fused(s, tb, st);
+    int rc = tt::launch_align(s.al, workspace, workspace_bytes, st);
+    if (rc == TT_OK) rc = tt::launch_transfer(s.tr, st);
+    if (rc == TT_OK) rc = tt::launch_verify(s.ve, st);
+    return rc;
 }
 
 }  // extern "C"

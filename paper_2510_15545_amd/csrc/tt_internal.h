@@ -54,12 +54,29 @@ struct VerifyArgs {
     size_t workspace_bytes;
 };
 
-// Workspace layout for tt_verify.
+// Workspace layout for tt_verify: Q62 mass Z and selected row r per stream, Q62 sums of
+// every 1024-float chunk of every stream's row.
 struct VerifyLayout {
-    size_t zsum, rsel, partials, arrivals, total;
+    size_t zsum, rsel, partials, total;
     int32_t n_chunks;
 };
 VerifyLayout verify_layout(int32_t n_streams, int32_t v_t);
 int launch_verify(const VerifyArgs &a, hipStream_t stream);
+// True when tt_verify runs one workgroup per stream (enough streams to fill the chip and
+// the row's chunk sums fit in LDS); the fused step kernel uses the same shape.
+bool verify_row_path(int32_t n_streams, int32_t v_t);
+// Normalised residual rows from Z and r in the workspace (written by a previous launch).
+int launch_verify_residual(const VerifyArgs &a, hipStream_t stream);
+
+// ---------------------------------------------------------------- fused step (step.hip)
+struct StepArgs {
+    AlignArgs al;     // alignment inputs and outputs
+    TransferArgs tr;  // transfer inputs and q (n_pairs, ids, offsets and map shared with al)
+    VerifyArgs ve;    // verification inputs and outputs (q = tr.q, target ids = al.target_ids)
+};
+// One launch for align + transfer + verify when the batch fits both the row-scan alignment
+// and the one-workgroup-per-stream verification; TT_EUNSUPPORTED otherwise.
+bool step_fused_fits(const StepArgs &s, int tb);
+int launch_step_fused(const StepArgs &s, int tb, hipStream_t stream);
 
 }  // namespace tt

@@ -44,6 +44,14 @@ def test_workspace_sizes_are_host_computed():
     assert n.value == 1024 * 512 * 32 * 4  # 2-bit codes for a 512-wide band row
     assert L.tt_align_workspace_size(8, 4096, 4096, -1, 8, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
     assert L.tt_align_workspace_size(8, 16, 16, 8, 65, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
+    # tt_step shares one workspace between its stages: the larger of the two
+    a, v = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    for args in ((256, 151936, 8, 30, 8, 8), (1024, 151936, 512, 512, 8, 8), (4, 32000, 100, 100, -1, 16)):
+        assert L.tt_step_workspace_size(*args, ctypes.byref(n)) == 0
+        assert L.tt_align_workspace_size(args[0], args[2], args[3], args[4], args[5], ctypes.byref(a)) == 0
+        assert L.tt_verify_workspace_size(args[0], args[1], ctypes.byref(v)) == 0
+        assert n.value == max(a.value, v.value)
+    assert L.tt_step_workspace_size(8, 10, 4096, 4096, -1, 8, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
 
 
 def test_invalid_arguments_return_before_launch():
@@ -72,6 +80,20 @@ def test_invalid_arguments_return_before_launch():
                        dummy, 0, None) == tt.TT_EWORKSPACE
     assert L.tt_verify(1, 10, None, dummy, dummy, dummy, 10, dummy, dummy, 4, dummy, dummy, None,
                        dummy, 1 << 20, None) == tt.TT_EINVAL
+
+    def step(vd=ctypes.byref(v), n=1, v_d=10, v_t=10, ld_d=10, ld_t=10, max_m=4, ids=dummy, ws=1 << 30):
+        return L.tt_step(vd, ctypes.byref(v), n, v_d, v_t, ids, dummy, dummy, dummy, 4, max_m, 8,
+                         dummy, ld_d, dummy, ld_t, dummy, dummy, dummy, dummy, dummy, dummy, dummy,
+                         dummy, dummy, None, dummy, ws, None)
+    assert step(vd=None) == tt.TT_EINVAL
+    assert step(n=-1) == tt.TT_EINVAL
+    assert step(ld_d=9) == tt.TT_EINVAL
+    assert step(ld_t=9) == tt.TT_EINVAL
+    assert step(max_m=0) == tt.TT_EINVAL
+    assert step(ids=None) == tt.TT_EINVAL
+    assert step(ws=16) == tt.TT_EWORKSPACE
+    assert step(vd=ctypes.byref(big)) == tt.TT_EUNSUPPORTED
+    assert step(n=0) == tt.TT_OK
 
 
 def test_binding_refuses_host_tensors():
