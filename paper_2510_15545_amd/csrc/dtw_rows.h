@@ -14,14 +14,17 @@
 //     inside a row are a (min, +) prefix scan.  Out-of-band cells are infinite.
 //   * A cell's predecessor is (i, j-1) iff C(i, j-1) < min(C(i-1, j-1), C(i-1, j)), else
 //     the diagonal iff C(i-1, j-1) <= C(i-1, j), else (i-1, j).  One wave runs the row
-//     recurrence and leaves C in LDS; then every wave turns rows of C into two 64-bit
-//     column masks per row ("not a left move", "diagonal move") with ballots.
-//   * Backtrack: inside row i the path runs left from its entry column e to the highest
+//     recurrence and leaves C in LDS.
+//   * Inside row i the optimal path runs left from its entry column e to the highest
 //     column x <= e whose move is not a left move, then enters row i-1 at x - 1
-//     (diagonal) or x.  That is one find-last-set per row on the scalar unit.
-//   * Row i covers columns [x_i, e_i]; each row's lane writes its path cells and the map
-//     entries of its columns (a column shared with the row below by an (i-1, j) move
-//     belongs to the higher row: the map holds the largest draft index).
+//     (diagonal) or x.  Every wave tabulates, for its rows and every possible e, that
+//     x and the next entry column (two ballots per row give the move masks); the
+//     backtrack is then one LDS lookup per row.
+//   * Row i covers columns [x_i, e_i], x_i non-decreasing in i.  Path cell q lies in the
+//     last row whose run starts at or before q, and column j maps to the last row whose
+//     run starts at or before j (a column shared by two rows through an (i-1, j) move
+//     belongs to the higher one: the map holds the largest draft index).  Both are
+//     prefix maxima over LDS arrays filled with atomic max, written lane-parallel.
 #pragma once
 
 #include <climits>
@@ -43,7 +46,10 @@ struct Lds {
     uint32_t tslot[kMaxSide * (TB / 4)];
     uint32_t dslot[kMaxSide * (TB / 4)];
     int cm[(kMaxSide + 1) * kCmLd];     // C(i, j) at [i * 65 + j], i, j = 0..64
-    uint64_t nl[kMaxSide], dg[kMaxSide];  // move masks of row i at [i - 1]
+    int rowmax[2 * kMaxSide];           // path index -> row starting there (scratch)
+    int colmax[kMaxSide + 1];           // column -> last row whose segment starts there (scratch)
+    uint8_t ftab[kMaxSide * kCmLd];     // row i, entry column e: entry column of row i - 1
+    uint8_t xtab[kMaxSide * kCmLd];     // row i, entry column e: first column of row i's run
     uint8_t tlen[kMaxSide];
     uint8_t dlen[kMaxSide];
     uint8_t cost[kMaxSide * kMaxSide];  // d(i, j) at [(i-1) * 64 + j - 1]
@@ -86,6 +92,19 @@ __device__ __forceinline__ uint64_t lane_u64(uint64_t v, int lane) {
     const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, lane);
     const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), lane);
     return ((uint64_t)hi << 32) | lo;
+}
+
+// Workgroup-wide OR of per-thread flag bits through one barrier: every wave leaves its
+// votes in LDS (votes[nwaves]).
+__device__ __forceinline__ int block_or(int flags, int *votes, int nwaves) {
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    int v = 0;
+    for (int bit = 1; bit <= 2; bit <<= 1) v |= __any(flags & bit) ? bit : 0;
+    if (lane == 0) votes[wave] = v;
+    __syncthreads();
+    int all = 0;
+    for (int w = 0; w < nwaves; ++w) all |= votes[w];
+    return all;
 }
 
 // Band half-width: |i - j| <= L with L = max(w, |K - M|), capped at max(K, M) (w < 0: no band).
@@ -172,11 +191,12 @@ __device__ __forceinline__ int recurrence(Lds<TB> &s, int K, int M, int L) {
     return __builtin_amdgcn_readlane(cprev, M - 1);
 }
 
-// Every wave: the move masks of rows wave + 1, wave + 1 + nwaves, ... from C in LDS.
+// Every wave: for rows wave + 1, wave + 1 + nwaves, ... and every entry column e, the
+// first column x of the row's run and the entry column of the row below, from C in LDS.
 template <int TB>
 __device__ __forceinline__ void moves(Lds<TB> &s, int K, int M, int L, int wave, int nwaves) {
     const int lane = threadIdx.x % kWave;
-    const int j = lane + 1;
+    const int j = lane + 1;  // also the entry column e tabulated by this lane
     for (int i = 1 + wave; i <= K; i += nwaves) {
         const bool inb = j <= M && j >= i - L && j <= i + L;
         const int diag = s.cm[(i - 1) * kCmLd + j - 1];
@@ -185,52 +205,73 @@ __device__ __forceinline__ void moves(Lds<TB> &s, int K, int M, int L, int wave,
         const bool not_left = !(left < min(diag, up));
         const uint64_t nl = __ballot(inb && not_left);
         const uint64_t dg = __ballot(inb && not_left && diag <= up);
-        if (lane == 0) {
-            s.nl[i - 1] = nl;
-            s.dg[i - 1] = dg;
+        const uint64_t cand = nl & (j >= 64 ? ~0ull : ((1ull << j) - 1));
+        const int x = cand ? 64 - __clzll(cand) : 0;  // highest not-left column <= e
+        const int f = x > 0 ? (((dg >> (x - 1)) & 1ull) ? x - 1 : x) : 0;
+        s.xtab[(i - 1) * kCmLd + j] = (uint8_t)x;
+        s.ftab[(i - 1) * kCmLd + j] = (uint8_t)f;
+        if (lane == 0) {  // entry column 0: the walk has ended
+            s.xtab[(i - 1) * kCmLd] = 0;
+            s.ftab[(i - 1) * kCmLd] = 0;
         }
     }
 }
 
-// One wave: backtrack from (K, M) over the move masks, then cost, path_len, path and map
-// of pair b.  When map_lds is given, map_lds[j - 1] also receives i*(j) (0-based).
+__device__ __forceinline__ int scan_max(int v) {
+    v = max(v, dpp_from<0x111, 0xF>(v, INT_MIN));
+    v = max(v, dpp_from<0x112, 0xF>(v, INT_MIN));
+    v = max(v, dpp_from<0x114, 0xF>(v, INT_MIN));
+    v = max(v, dpp_from<0x118, 0xF>(v, INT_MIN));
+    v = max(v, dpp_from<0x142, 0xA>(v, INT_MIN));
+    v = max(v, dpp_from<0x143, 0xC>(v, INT_MIN));
+    return v;
+}
+
+// One wave: backtrack from (K, M) through the tables, then cost, path_len, path and map of
+// pair b.  Returns i*(j) (0-based) in lane j - 1 for j <= M, -1 in the other lanes.
 template <int TB>
-__device__ __forceinline__ void backtrack(const AlignArgs &a, const Lds<TB> &s, int b, int d0, int K, int t0,
-                                          int M, int total, int *map_lds) {
+__device__ __forceinline__ int backtrack(const AlignArgs &a, Lds<TB> &s, int b, int d0, int K, int t0, int M,
+                                         int total) {
     const int lane = threadIdx.x % kWave;
-    const uint64_t nl_mask = lane < K ? s.nl[lane] : 0ull;  // row lane + 1
-    const uint64_t dg_mask = lane < K ? s.dg[lane] : 0ull;
-    int e = M, n = 0;
-    int seg_x = 1, seg_e = 0;  // row lane + 1 covers columns [seg_x, seg_e] (empty if unvisited)
+    // entry column of every row, walking down from (K, M); 0 once the walk has ended
+    int e = M, ent = 0;
     for (int i = K; i >= 1; --i) {
-        const uint64_t nl = lane_u64(nl_mask, i - 1);
-        const uint64_t dg = lane_u64(dg_mask, i - 1);
-        const uint64_t cand = nl & (e >= 64 ? ~0ull : ((1ull << e) - 1));  // e = 0: nothing left
-        const int x = cand ? 64 - __clzll(cand) : 0;  // highest not-left column <= e; 0 if none
-        seg_x = (lane == i - 1 && x > 0) ? x : seg_x;
-        seg_e = (lane == i - 1 && x > 0) ? e : seg_e;
-        n += x > 0 ? e - x + 1 : 0;
-        e = x > 0 ? (((dg >> (x - 1)) & 1ull) ? x - 1 : x) : 0;
+        ent = (lane == i - 1) ? e : ent;
+        e = s.ftab[(i - 1) * kCmLd + e];
     }
+    // row lane + 1 covers columns [x, ent]
+    const int x = (lane < K && ent > 0) ? s.xtab[lane * kCmLd + ent] : 0;
+    const int len = x > 0 ? ent - x + 1 : 0;
+    const int incl = scan_add(len);
+    const int off = incl - len;
+    const int n = __builtin_amdgcn_readlane(incl, kWave - 1);
     if (lane == 0) {
         a.cost[b] = total;
         a.path_len[b] = n;
     }
-    // each row's lane writes its cells; the column it shares with the row below through an
-    // (i-1, j) move is that row's map entry
-    const int len = seg_e - seg_x + 1;  // 0 for rows the walk never reached
-    const int off = scan_add(len) - len;
-    const int x_up = __builtin_amdgcn_update_dpp(0, seg_x, 0x130 /* wave_shl:1 */, 0xF, 0xF, false);
-    const int len_up = __builtin_amdgcn_update_dpp(0, len, 0x130 /* wave_shl:1 */, 0xF, 0xF, false);
-    const int mlen = (lane + 1 < K && len > 0 && len_up > 0 && x_up == seg_e) ? len - 1 : len;
-    int2 *pp = reinterpret_cast<int2 *>(a.path + 2 * ((size_t)d0 + (size_t)t0));
-    for (int k = 0; __any(k < len); ++k) {
-        if (k < len) pp[off + k] = make_int2(lane, seg_x - 1 + k);
-        if (k < mlen) {
-            a.map[t0 + seg_x - 1 + k] = lane;
-            if (map_lds != nullptr) map_lds[seg_x - 1 + k] = lane;
-        }
+    s.rowmax[lane] = -1;
+    s.rowmax[lane + kWave] = -1;
+    s.colmax[lane] = -1;
+    if (len > 0) {
+        atomicMax(&s.rowmax[off], lane);
+        atomicMax(&s.colmax[x - 1], lane);
     }
+    // path cell q: the last row starting at or before q (two passes of 64 cells)
+    int2 *pp = reinterpret_cast<int2 *>(a.path + 2 * ((size_t)d0 + (size_t)t0));
+    int carry = -1;
+    for (int q0 = 0; q0 < n; q0 += kWave) {
+        const int q = q0 + lane;
+        const int row = max(scan_max(s.rowmax[q0 + lane]), carry);
+        carry = __builtin_amdgcn_readlane(row, kWave - 1);
+        const int r = row < 0 ? 0 : row;
+        const int rx = __shfl(x, r);
+        const int ro = __shfl(off, r);
+        if (q < n) pp[q] = make_int2(r, rx - 1 + (q - ro));
+    }
+    // column j: the last row whose run starts at or before j
+    const int mj = scan_max(s.colmax[lane]);
+    if (lane < M) a.map[t0 + lane] = mj;
+    return lane < M ? mj : -1;
 }
 
 }  // namespace rows

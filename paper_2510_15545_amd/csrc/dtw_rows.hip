@@ -16,8 +16,9 @@ __global__ void __launch_bounds__(kThreads) dtw_rows(AlignArgs a) {
     const int t0 = a.target_off[b], M = a.target_off[b + 1] - t0;
 
     const bool shape_ok = K >= 1 && K <= a.max_k && M >= 1 && M <= a.max_m;
+    __shared__ int votes[kThreads / rows::kWave];
     const int bad = shape_ok ? rows::stage<TB>(a, s, d0, K, t0, M, tid, kThreads) : 1;
-    if (__syncthreads_or(bad)) {
+    if (rows::block_or(bad, votes, kThreads / rows::kWave)) {
         if (tid == 0) {
             a.cost[b] = -1;
             a.path_len[b] = 0;
@@ -35,7 +36,7 @@ __global__ void __launch_bounds__(kThreads) dtw_rows(AlignArgs a) {
     __syncthreads();
     rows::moves<TB>(s, K, M, L, wave, kThreads / rows::kWave);
     __syncthreads();
-    if (wave == 0) rows::backtrack<TB>(a, s, b, d0, K, t0, M, total, nullptr);
+    if (wave == 0) rows::backtrack<TB>(a, s, b, d0, K, t0, M, total);
 }
 
 template <int TB>

@@ -46,7 +46,7 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     __shared__ float pt[rows::kMaxSide];   // P_t(t_j) on target row j
     __shared__ float ua[rows::kMaxSide];   // acceptance uniforms
     __shared__ int tid_t[rows::kMaxSide];  // target ids
-    __shared__ int mapl[rows::kMaxSide];   // i*(j) of every target position
+    __shared__ int sh_votes[kThreads / kWave];
     __shared__ int sh_gamma, sh_ok, sh_rtok;
     __shared__ float sh_rq;
     extern __shared__ uint64_t sh_part[];  // Q62 chunk sums of the selected row
@@ -61,25 +61,30 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     const bool vshape_ok = M >= 0 && M <= ve.max_m;  // max_m <= 64 here
     int bad = shape_ok ? 0 : 1, vbad = vshape_ok ? 0 : 1;
     if (shape_ok && tid < kStageThreads) bad = rows::stage<TB>(al, s, d0, K, t0, M, tid, kStageThreads);
-    if (shape_ok && tid >= kDraftPrefetch && tid < kDraftPrefetch + K) {
+    // the probability gathers stay in registers until just before step 3, so the barriers
+    // of step 2 do not wait for them
+    const bool pd_thread = shape_ok && tid >= kDraftPrefetch && tid < kDraftPrefetch + K;
+    const bool pt_thread = vshape_ok && tid >= kTargetPrefetch && tid < kTargetPrefetch + M;
+    float pv = __builtin_nanf(""), uv = 0.0f;
+    int tok = 0;
+    if (pd_thread) {
         const int i = tid - kDraftPrefetch;
         const int id = al.draft_ids[d0 + i];
-        pd[i] = (id >= 0 && id < tr.v_d) ? tr.draft_probs[(int64_t)(d0 + i) * tr.draft_ld + id]
-                                         : __builtin_nanf("");
+        if (id >= 0 && id < tr.v_d) pv = tr.draft_probs[(int64_t)(d0 + i) * tr.draft_ld + id];
     }
-    if (vshape_ok && tid >= kTargetPrefetch && tid < kTargetPrefetch + M) {
+    if (pt_thread) {
         const int j = tid - kTargetPrefetch;
-        const int tok = al.target_ids[t0 + j];
+        tok = al.target_ids[t0 + j];
         if (tok < 0 || tok >= ve.v_t) {
             vbad = 1;
         } else {
-            tid_t[j] = tok;
-            pt[j] = ve.target_probs[(int64_t)(t0 + b + j) * ve.target_ld + tok];
-            ua[j] = ve.u_accept[t0 + j];
+            pv = ve.target_probs[(int64_t)(t0 + b + j) * ve.target_ld + tok];
+            uv = ve.u_accept[t0 + j];
         }
     }
-    const bool align_ok = !__syncthreads_or(bad);
-    const bool verify_ok = !__syncthreads_or(vbad);
+    const int all_votes = rows::block_or((bad ? 1 : 0) | (vbad ? 2 : 0), sh_votes, kThreads / kWave);
+    const bool align_ok = (all_votes & 1) == 0;
+    const bool verify_ok = (all_votes & 2) == 0;
 
     // ---- 2. token distances, cumulative cost, move masks
     const int L = rows::band_half_width(K, M, al.w);
@@ -91,15 +96,20 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
         if (wave == 0) total = rows::recurrence<TB>(s, K, M, L);
         __syncthreads();
         rows::moves<TB>(s, K, M, L, wave, kThreads / kWave);
-        __syncthreads();
     }
+    if (pd_thread) pd[tid - kDraftPrefetch] = pv;
+    if (pt_thread) {
+        tid_t[tid - kTargetPrefetch] = tok;
+        pt[tid - kTargetPrefetch] = pv;
+        ua[tid - kTargetPrefetch] = uv;
+    }
+    __syncthreads();
 
     // ---- 3. backtrack, transfer and acceptance (one wave)
     if (wave == 0) {
         float qj = __builtin_nanf("");  // q of position lane (lanes < M)
         if (align_ok) {
-            rows::backtrack<TB>(al, s, b, d0, K, t0, M, total, mapl);
-            const int mi = lane < M ? mapl[lane] : -1;  // written by this wave above
+            const int mi = rows::backtrack<TB>(al, s, b, d0, K, t0, M, total);
             if (mi >= 0 && mi < K) qj = pd[mi];
         } else {
             if (lane == 0) {
