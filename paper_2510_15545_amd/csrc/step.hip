@@ -55,6 +55,7 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     const int d0 = al.draft_off[b], K = al.draft_off[b + 1] - d0;
     const int t0 = al.target_off[b], M = al.target_off[b + 1] - t0;
+    const float us = ve.u_sample[b];  // needed only by the sampler, loaded while the rest runs
 
     // ---- 1. staging and prefetch
     const bool shape_ok = K >= 1 && K <= al.max_k && M >= 1 && M <= al.max_m;
@@ -153,7 +154,7 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     if (wave != 0) return;
     uint64_t Z;
     const int token =
-        vcore::wave_sample(row, vt, p.nc, [&](int c) { return sh_part[c]; }, ve.u_sample[b], rtok, rq, &Z);
+        vcore::wave_sample(row, vt, p.nc, p.vec4 != 0, [&](int c) { return sh_part[c]; }, us, rtok, rq, &Z);
     if (tid == 0) {
         ve.n_accepted[b] = r;
         ve.out_token[b] = token;

@@ -120,7 +120,7 @@ __global__ void __launch_bounds__(kRowThreads) verify_row(VParams p) {
     __syncthreads();
     if (wave != 0) return;
     uint64_t Z;
-    const int token = wave_sample(row, vt, p.nc, [&](int c) { return sh_part[c]; }, us, rtok, rq, &Z);
+    const int token = wave_sample(row, vt, p.nc, p.vec4 != 0, [&](int c) { return sh_part[c]; }, us, rtok, rq, &Z);
     if (tid == 0) {
         a.n_accepted[b] = r;
         a.out_token[b] = token;
@@ -186,7 +186,7 @@ __global__ void __launch_bounds__(kWave) verify_sample(VParams p) {
     const int rtok = r < M ? a.target_ids[t0 + r] : -1;
     const float rq = r < M ? a.q[t0 + r] : 0.0f;
     uint64_t Z;
-    const int token = wave_sample(row, a.v_t, p.nc, [&](int c) { return part[c]; }, us, rtok, rq, &Z);
+    const int token = wave_sample(row, a.v_t, p.nc, p.vec4 != 0, [&](int c) { return part[c]; }, us, rtok, rq, &Z);
     if (tid == 0) {
         a.n_accepted[b] = r;
         a.out_token[b] = token;

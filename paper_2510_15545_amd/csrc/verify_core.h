@@ -184,17 +184,28 @@ __device__ __forceinline__ void stream_chunks(const float *row, int vt, bool vec
 }
 
 // Inverse-CDF sample of the row from its nc chunk sums part(c), by one wave: every lane
-// returns the token and *Zout the Q62 mass.  Chunk sums are scanned lane-blocked, the
-// crossing chunk is re-read as 16 consecutive floats per lane and scanned the same way.
+// returns the token and *Zout the Q62 mass.  Chunk sums are scanned lane-blocked (lane l
+// holds chunks [l * per, (l + 1) * per)), the crossing chunk is re-read as 16 consecutive
+// floats per lane and scanned the same way.  Searches inside a lane are branch-free counts.
 template <class Part>
-__device__ inline int wave_sample(const float *row, int vt, int nc, Part part, float u, int rtok, float rq,
-                           uint64_t *Zout) {
+__device__ inline int wave_sample(const float *row, int vt, int nc, bool vec, Part part, float u, int rtok,
+                                  float rq, uint64_t *Zout) {
+    constexpr int kPerMax = 4;  // chunk sums kept in registers per lane (rows up to 256K floats)
     const int lane = threadIdx.x % kWave;
     const int per = (nc + kWave - 1) / kWave;
     const int ca = lane * per < nc ? lane * per : nc;
     const int cb = ca + per < nc ? ca + per : nc;
+    uint64_t ps[kPerMax];
     uint64_t local = 0;
-    for (int c = ca; c < cb; ++c) local += part(c);
+    if (per <= kPerMax) {
+#pragma unroll
+        for (int k = 0; k < kPerMax; ++k) {
+            ps[k] = ca + k < cb ? part(ca + k) : 0ull;
+            local += ps[k];
+        }
+    } else {
+        for (int c = ca; c < cb; ++c) local += part(c);
+    }
     const uint64_t incl = wave_inclusive_scan(local);
     const uint64_t Z = lane_value(incl, kWave - 1);
     *Zout = Z;
@@ -205,17 +216,24 @@ __device__ inline int wave_sample(const float *row, int vt, int nc, Part part, f
     const unsigned long long hit = __ballot(excl <= T && T < incl);
     if (hit == 0ull) return vt - 1;  // only if the Q62 mass wrapped (not a probability row)
     const int owner = __ffsll(hit) - 1;
-    int cs = nc;
-    uint64_t base = 0;
-    if (lane == owner) {
+    int cs = ca;
+    uint64_t base = excl;
+    if (per <= kPerMax) {
+        uint64_t run = excl;
+#pragma unroll
+        for (int k = 0; k < kPerMax; ++k) {  // chunks of this lane wholly at or below T
+            const bool below = ca + k < cb && run + ps[k] <= T;
+            cs += below ? 1 : 0;
+            base = below ? run + ps[k] : base;
+            run += ps[k];
+        }
+    } else if (lane == owner) {
         uint64_t run = excl;
         for (int c = ca; c < cb; ++c) {
             const uint64_t nx = run + part(c);
-            if (run <= T && nx > T) {
-                cs = c;
-                base = run;
-                break;
-            }
+            if (nx > T) break;
+            cs = c + 1;
+            base = nx;
             run = nx;
         }
     }
@@ -223,13 +241,26 @@ __device__ inline int wave_sample(const float *row, int vt, int nc, Part part, f
     base = lane_value(base, owner);
     // the crossing chunk: lane holds elements cs*1024 + lane*16 + [0, 16)
     const int x0 = cs * kChunk + lane * 16;
+    float pv[16];
+    if (vec && x0 + 16 <= vt) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 t = *reinterpret_cast<const float4 *>(row + x0 + 4 * q);
+            pv[4 * q] = t.x;
+            pv[4 * q + 1] = t.y;
+            pv[4 * q + 2] = t.z;
+            pv[4 * q + 3] = t.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) pv[k] = x0 + k < vt ? row[x0 + k] : 0.0f;
+    }
     uint64_t qv[16];
     uint64_t sum = 0;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
         const int x = x0 + k;
-        const float pv = x < vt ? row[x] : 0.0f;
-        qv[k] = q62(clamp01(pv - (x == rtok ? rq : 0.0f)));
+        qv[k] = x < vt ? q62(clamp01(pv[k] - (x == rtok ? rq : 0.0f))) : 0ull;
         sum += qv[k];
     }
     const uint64_t lincl = wave_inclusive_scan(sum) + base;
@@ -237,19 +268,15 @@ __device__ inline int wave_sample(const float *row, int vt, int nc, Part part, f
     const unsigned long long lhit = __ballot(lexcl <= T && T < lincl);
     if (lhit == 0ull) return vt - 1;
     const int tl = __ffsll(lhit) - 1;
-    int tok = vt - 1;
-    if (lane == tl) {
-        uint64_t run = lexcl;
+    // in the crossing lane: the number of leading elements whose inclusive prefix is <= T
+    uint64_t run = lexcl;
+    int k_at = 0;
 #pragma unroll
-        for (int k = 0; k < 16; ++k) {
-            run += qv[k];
-            if (run > T) {
-                tok = x0 + k;
-                break;
-            }
-        }
+    for (int k = 0; k < 16; ++k) {
+        run += qv[k];
+        k_at += run <= T ? 1 : 0;
     }
-    return __builtin_amdgcn_readlane(tok, tl);
+    return __builtin_amdgcn_readlane(x0 + k_at, tl);
 }
 
 }  // namespace vcore
