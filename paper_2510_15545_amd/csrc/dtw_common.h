@@ -109,5 +109,29 @@ __device__ __forceinline__ void read_slot(const uint32_t *slot, uint32_t (&w)[TB
     for (int q = 0; q < TB / 4; ++q) w[q] = slot[q];
 }
 
+// Workgroup-wide OR of per-thread flag bits through one barrier: every wave leaves its
+// votes in LDS (votes[nwaves]).
+__device__ __forceinline__ int block_or(int flags, int *votes, int nwaves) {
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    int v = 0;
+    for (int bit = 1; bit <= 2; bit <<= 1) v |= __any(flags & bit) ? bit : 0;
+    if (lane == 0) votes[wave] = v;
+    __syncthreads();
+    int all = 0;
+    for (int w = 0; w < nwaves; ++w) all |= votes[w];
+    return all;
+}
+
+// Inclusive prefix sum over the 64 lanes (DPP: rows of 16 lanes, then row broadcasts).
+__device__ __forceinline__ int wave_prefix_sum(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+    return v;
+}
+
 }  // namespace dtw
 }  // namespace tt

@@ -94,19 +94,6 @@ __device__ __forceinline__ uint64_t lane_u64(uint64_t v, int lane) {
     return ((uint64_t)hi << 32) | lo;
 }
 
-// Workgroup-wide OR of per-thread flag bits through one barrier: every wave leaves its
-// votes in LDS (votes[nwaves]).
-__device__ __forceinline__ int block_or(int flags, int *votes, int nwaves) {
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    int v = 0;
-    for (int bit = 1; bit <= 2; bit <<= 1) v |= __any(flags & bit) ? bit : 0;
-    if (lane == 0) votes[wave] = v;
-    __syncthreads();
-    int all = 0;
-    for (int w = 0; w < nwaves; ++w) all |= votes[w];
-    return all;
-}
-
 // Band half-width: |i - j| <= L with L = max(w, |K - M|), capped at max(K, M) (w < 0: no band).
 __device__ __forceinline__ int band_half_width(int K, int M, int w) {
     const int mx = K > M ? K : M;

@@ -18,7 +18,7 @@ __global__ void __launch_bounds__(kThreads) dtw_rows(AlignArgs a) {
     const bool shape_ok = K >= 1 && K <= a.max_k && M >= 1 && M <= a.max_m;
     __shared__ int votes[kThreads / rows::kWave];
     const int bad = shape_ok ? rows::stage<TB>(a, s, d0, K, t0, M, tid, kThreads) : 1;
-    if (rows::block_or(bad, votes, kThreads / rows::kWave)) {
+    if (dtw::block_or(bad, votes, kThreads / rows::kWave)) {
         if (tid == 0) {
             a.cost[b] = -1;
             a.path_len[b] = 0;

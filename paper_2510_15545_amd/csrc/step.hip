@@ -83,7 +83,7 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
             uv = ve.u_accept[t0 + j];
         }
     }
-    const int all_votes = rows::block_or((bad ? 1 : 0) | (vbad ? 2 : 0), sh_votes, kThreads / kWave);
+    const int all_votes = dtw::block_or((bad ? 1 : 0) | (vbad ? 2 : 0), sh_votes, kThreads / kWave);
     const bool align_ok = (all_votes & 1) == 0;
     const bool verify_ok = (all_votes & 2) == 0;
 

@@ -77,10 +77,13 @@ def test_strips_longer_than_a_wave():
     toks = random_tokens(rng, 200, 1, 4)
     v = vocab_of(toks)
     pairs = []
-    for k, m in ((65, 64), (64, 65), (130, 129), (200, 60), (60, 200), (128, 128), (1, 300), (300, 1)):
+    # band widths up to and past the widest precomputed band (512 cells per row): 64-row
+    # strips whose band shifts one column per row span up to W + 126 sweep steps
+    for k, m in ((65, 64), (64, 65), (130, 129), (200, 60), (60, 200), (128, 128), (1, 300), (300, 1),
+                 (150, 100), (100, 150), (200, 210), (300, 520), (260, 520), (520, 300)):
         pairs.append((list(rng.integers(0, len(toks), k)), list(rng.integers(0, len(toks), m))))
     wl = workload(v, v, pairs, len(toks), len(toks), probs=False)
-    for w in (4, 8, 16, -1, 0, 70):
+    for w in (4, 8, 16, -1, 0, 40, 70):
         print(f"[case] strips w={w}", flush=True)
         compare_align(wl, gpu_run(wl, w=w), oracle_run(wl, w=w))
 
