@@ -68,11 +68,14 @@ typedef struct {
 } tt_vocab;
 
 /*
- * Workspace bytes tt_align needs for these bounds: 0 when max_k <= 64 (each pair's
- * working set stays in LDS), otherwise room for the 2-bit predecessor codes of
- * every pair's band (n_pairs * max_k * ceil(min(max_m, 2 L + 1) / 16) * 4 bytes,
- * L the largest band half-width the bounds allow).  Returns TT_EUNSUPPORTED when
- * the bounds need more LDS than one MI355X workgroup can hold.
+ * Workspace bytes tt_align needs for these bounds: 0 when max_k <= 64 and
+ * max_m <= 64 (each pair's working set stays in LDS), otherwise room for the
+ * 2-bit predecessor codes of every pair's band (n_pairs * max_k *
+ * (ceil(min(max_m, 2 L + 1) / 16) + 1) * 4 bytes, L the largest band half-width
+ * the bounds allow).  Returns TT_EUNSUPPORTED when the bounds need more LDS than
+ * one MI355X workgroup can hold (token bytes (max_k + max_m) * slot, the slot
+ * being max_token_bytes rounded up to 8, 16, 32 or 64, plus
+ * 9 * (max_k + max_m) + about 11 KB).
  */
 int tt_align_workspace_size(int32_t n_pairs, int32_t max_k, int32_t max_m, int32_t w,
                             int32_t max_token_bytes, size_t *bytes);

@@ -1,51 +1,51 @@
-// Dynamic Token Warping on gfx950 for pairs of any length: one 1024-thread workgroup
-// per (draft, proxy-target) pair.
+// Dynamic Token Warping on gfx950 for pairs of any length: one 256-thread workgroup per
+// (draft, proxy-target) pair, small enough in LDS that several pairs share a compute unit.
 //
-// Computes Alg. 1 of the paper (cumulative cost C over draft x target tokens with
-// the Sakoe-Chiba band, Sec. 4.1) using the byte-level Levenshtein token distance
-// of App. H, then the backtrack from (K, M) and the mapping of App. A.2.
+// Computes Alg. 1 of the paper (cumulative cost C over draft x target tokens with the
+// Sakoe-Chiba band, Sec. 4.1) using the byte-level Levenshtein token distance of App. H,
+// then the backtrack from (K, M) and the mapping of App. A.2.
 //
 // Work decomposition:
-//   * Staging: every thread loads one token (draft or target) -- id, byte offsets,
-//     bytes -- validates it and packs it into a fixed-width LDS slot.
+//   * Staging: every thread loads tokens (draft or target) -- id, byte offsets, bytes --
+//     validates them and packs each into a fixed-width LDS slot.
 //   * Draft rows are processed in strips of 64 with lane r of wave 0 owning row
 //     i = i0 + r.  Wave 0 sweeps the strip's anti-diagonals: at step t lane r finishes
-//     cell (i0 + r, jfirst + t - r).  C(i-1, j) arrives from lane r-1 through a DPP wave
+//     cell (i0 + r, jlo(i0) + t - r).  C(i-1, j) arrives from lane r-1 through a DPP wave
 //     shift (lane 0 takes the previous strip's last row from LDS through the shift's
 //     fill operand), C(i-1, j-1) is the value received one step earlier and C(i, j-1)
 //     is the lane's own previous value.  The step is branch-free.
-//   * Token distances: for bands up to the planned width (512 cells per row when LDS
-//     allows) the distances of a strip are evaluated cell-parallel into an LDS byte
-//     matrix laid out by sweep step (one dword per lane holds four consecutive steps),
-//     double-buffered: while wave 0 sweeps strip s, waves 1-15 fill the buffer of strip
-//     s + 1.  The sweep runs four steps per dword with the next dword and lane 0's next
-//     four row-above values prefetched.  Wider bands: wave 0 evaluates each distance in
-//     place during the sweep.
-//   * Token distance: the bit-parallel edit-distance recurrence (Myers 1999, in
-//     Hyyro's 2001 global-distance form) with the longer token as the pattern (one
-//     bit per byte, at most 64) and the shorter one as the text; per-byte match masks
-//     come from SWAR byte comparison of the packed pattern.
-//   * Each cell's predecessor choice is a 2-bit code, 16 per dword, row-major inside
-//     the band.  The current strip's codes live in LDS; finished strips are parked in
-//     the caller's workspace and brought back strip by strip during the backtrack.
+//   * Token distances: the strip's steps are cut into chunks of 64.  While wave 0 sweeps
+//     chunk c, waves 1-3 evaluate the distances of chunk c + 1 into the other half of a
+//     double buffer ([lane][step / 4] dwords, one byte per step, bit 7 set for cells
+//     outside the band so the sweep needs no band arithmetic).  One barrier per chunk.
+//   * Token distance: the bit-parallel edit-distance recurrence (Myers 1999, in Hyyro's
+//     2001 global-distance form) with the longer token as the pattern (one bit per byte,
+//     at most 64) and the shorter one as the text; per-byte match masks come from SWAR
+//     byte comparison of the packed pattern.
+//   * Each cell's predecessor choice is two bits (up: C(i-1, j) < C(i-1, j-1); left:
+//     C(i, j-1) below both), shifted into a per-lane register, 16 steps per dword, and
+//     stored straight from registers into the caller's workspace, row-major by draft row.
 //   * Backtrack (wave 0), one row per step: inside row i the path runs left from its
-//     entry column to the highest column whose move is not a left move (a find-last-set
-//     over the 2-bit codes, 16 per dword), then enters row i-1.  The codes of every row
-//     are first gathered into the freed cost buffers when they fit (else the strips are
-//     fetched back one by one).  Path cells and map entries are then written by all
-//     threads with binary searches over the rows' runs.
+//     entry column to the highest column whose move is not a left move,
+//     then enters row i-1.  One lane walks: per row it reads the code word holding the
+//     entry cell, masks the steps past it and takes the lowest set bit of the not-left
+//     flags (the highest column).  The other waves stage the next strip's code words
+//     into LDS meanwhile (rows of more than 64 words are read from the workspace).  Path
+//     cells and map entries are then written by all threads with binary searches over
+//     the rows' runs.
 //
 // LDS layout (bytes, each region 16-byte aligned):
 //   tslot [max_m][TB] / tlen [max_m]   target token bytes and lengths
 //   dslot [max_k][TB] / dlen [max_k]   draft token bytes and lengths
-//   row0, row1 [max_m+8] int32         C of the row above the strip (double-buffered,
-//                                      padded so four-step groups may read past M)
-//   cost  2 x [groups][64] u32        token distances of a strip, [step/4][lane], double-buffered
-//   scode [64][WPR] u32                direction codes of the current strip
-//   path  [max_k+max_m] u32            backtracked cells (i << 16 | j), reverse order
-//   sink  [64] u32                     target of the stores a lane does not need
-// with WPR = ceil(min(max_m, 2 L + 1) / 16) for the largest band half-width L the
-// bounds allow.
+//   row0, row1 [64 + max_m + 136] int32 C of the row above the strip / of the strip's last
+//                                      row, by column with a 64-entry front pad
+//   cost  2 x [64][17] u32             token distances of a chunk, double-buffered; during
+//                                      the backtrack two strips of code words (2 x [64][RW])
+//                                      when RW <= 64
+//   path  [max_k] x 2 u32              per row: run (first column << 16 | entry column),
+//                                      then the index of its first path cell
+// Workspace: per pair max_k rows of RW = ceil(W / 16) + 1 code words, W the widest band
+// row the bounds allow.
 #include "dtw_common.h"
 
 #ifndef TT_ALIGN_ROWS
@@ -60,23 +60,26 @@ using dtw::kWave;
 using dtw::read_slot;
 using dtw::stage_token;
 using dtw::token_distance;
-constexpr int kThreads = 1024;                   // wave 0 sweeps, the other waves precompute distances
-constexpr int kPrecomp = 512;                    // widest band whose distances are precomputed per strip
-constexpr int kRowPad = 8;                       // INF entries past column M in the row buffers
+// Workgroup size: wave 0 sweeps and walks, the other waves evaluate distances.  Eight waves
+// at 64 VGPRs keep four workgroups on a compute unit; the register-hungry wide token slots
+// use four.
+template <int TB>
+constexpr int band_threads() {
+    return TB <= 16 ? 512 : 256;
+}
+constexpr int kChunk = 64;                       // sweep steps per cost chunk
+constexpr int kGroups = kChunk / 4;              // cost dwords per lane and chunk
+constexpr int kCostStride = kGroups + 1;         // dwords per lane in a chunk buffer (odd: no bank conflicts)
+constexpr int kRowFront = 64;                    // row buffers hold columns -64 .. max_m + 135
+constexpr int kRowBack = 136;
 constexpr size_t kLdsLimit = 160 * 1024 - 1024;  // gfx950 LDS per workgroup, less static use
+constexpr uint32_t kOutOfBand = 0x80808080u;     // four cost bytes with the out-of-band bit
 
 __host__ __device__ inline size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
 
 struct LdsPlan {
-    size_t tslot, tlen, dslot, dlen, row0, row1, cost, cost_bytes, scode, path, sink, total;
-    int wpr_max;
-    int cost_w;  // widest band (cells per row) the two cost buffers hold
+    size_t tslot, tlen, dslot, dlen, row0, row1, cost, path, total;
 };
-
-// Four-step groups of a 64-row strip sweep over a band of width w: the band's columns
-// shift by up to one per row, so a strip spans up to w + 126 steps (+1 group for the
-// prefetch).
-__host__ __device__ inline int cost_groups(int w) { return (w + 2 * (kWave - 1) + 3) / 4 + 1; }
 
 __host__ __device__ inline int band_half_width_bound(int32_t max_k, int32_t max_m, int32_t w) {
     int mx = max_k > max_m ? max_k : max_m;
@@ -86,17 +89,16 @@ __host__ __device__ inline int band_half_width_bound(int32_t max_k, int32_t max_
     return L < mx ? L : mx;
 }
 
-__host__ __device__ inline int words_per_row_bound(int32_t max_k, int32_t max_m, int32_t w) {
+// Code words stored per draft row: a band row of W cells starts anywhere inside a word.
+__host__ __device__ inline int row_words_bound(int32_t max_k, int32_t max_m, int32_t w) {
     const long long L = band_half_width_bound(max_k, max_m, w);
     long long W = 2 * L + 1;
     if (W > max_m) W = max_m;
-    return (int)((W + 15) / 16);
+    return (int)((W + 15) / 16) + 1;
 }
 
-__host__ __device__ inline LdsPlan plan_lds_with(int32_t max_k, int32_t max_m, int32_t w, int tb, int cost_w) {
+__host__ __device__ inline LdsPlan plan_lds(int32_t max_k, int32_t max_m, int32_t w, int tb) {
     LdsPlan p;
-    p.wpr_max = words_per_row_bound(max_k, max_m, w);
-    const size_t strip_rows = max_k < kWave ? (size_t)max_k : kWave;
     size_t off = 0;
     p.tslot = off;
     off = align16(off + (size_t)max_m * tb);
@@ -107,217 +109,145 @@ __host__ __device__ inline LdsPlan plan_lds_with(int32_t max_k, int32_t max_m, i
     p.dlen = off;
     off = align16(off + (size_t)max_k);
     p.row0 = off;
-    off = align16(off + 4 * ((size_t)max_m + 1 + kRowPad));
+    off = align16(off + 4 * ((size_t)kRowFront + max_m + kRowBack));
     p.row1 = off;
-    off = align16(off + 4 * ((size_t)max_m + 1 + kRowPad));
-    // distances of a strip, by sweep step, double-buffered (bands up to cost_w cells per row)
-    p.cost_w = cost_w;
-    p.cost_bytes = cost_w > 0 ? align16(4 * (size_t)kWave * cost_groups(cost_w)) : 0;
+    off = align16(off + 4 * ((size_t)kRowFront + max_m + kRowBack));
+    // distances of two chunks during the sweep; two strips of code words during the
+    // backtrack when a row has at most 64 of them
+    const int rw = row_words_bound(max_k, max_m, w);
+    const size_t cost_bytes = 2 * 4 * (size_t)kWave * kCostStride;
+    const size_t stage_bytes = rw <= kWave ? 2 * 4 * (size_t)kWave * rw : 0;
     p.cost = off;
-    off = align16(off + 2 * p.cost_bytes);
-    p.scode = off;
-    off = align16(off + 4 * strip_rows * (size_t)p.wpr_max);
-    p.path = off;  // per row: run (first column << 16 | entry column), then path offset
+    off = align16(off + (cost_bytes > stage_bytes ? cost_bytes : stage_bytes));
+    p.path = off;
     off = align16(off + 8 * (size_t)max_k);
-    p.sink = off;
-    off = align16(off + 4 * kWave);
     p.total = off;
     return p;
 }
 
-// The plan with the widest precomputed band (at most kPrecomp cells per row) that fits in
-// LDS; bands wider than the chosen width are swept with distances evaluated in place.
-__host__ __device__ inline LdsPlan plan_lds(int32_t max_k, int32_t max_m, int32_t w, int tb) {
-    const long long lb = band_half_width_bound(max_k, max_m, w);
-    const long long wband = (2 * lb + 1) < max_m ? (2 * lb + 1) : max_m;  // cells per row, at most
-    int cost_w = (int)(wband < kPrecomp ? wband : kPrecomp);
-    LdsPlan p = plan_lds_with(max_k, max_m, w, tb, cost_w);
-    while (p.total > kLdsLimit && cost_w > 0) {
-        cost_w = cost_w > 32 ? cost_w / 2 : 0;
-        p = plan_lds_with(max_k, max_m, w, tb, cost_w);
-    }
-    return p;
-}
-
-// C(i-1, .) from the lane below: DPP wave shift right by one lane; lane 0 gets `fill`.
-__device__ __forceinline__ int from_lane_below(int v, int fill) {
-    return __builtin_amdgcn_update_dpp(fill, v, 0x138 /* wave_shr:1 */, 0xF, 0xF, false);
-}
-
-__device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
-
 struct Band {
-    int K, M, L, W, WPR;
+    int K, M, L, W;
     __device__ __forceinline__ int jlo(int i) const { return (i - L) > 1 ? (i - L) : 1; }
     __device__ __forceinline__ int jhi(int i) const { return (i + L) < M ? (i + L) : M; }
 };
 
-// One sweep step for lane = row: combine the three predecessors of the cell, record the
-// 2-bit choice and the cell value.  `rv` is lane 0's C(i0-1, j) (the fill of the shift).
-struct SweepState {
-    int cur, above_prev, lastc;
-    uint32_t cw;
-    int o;  // band offset of this lane's cell at the current step
+// Geometry of the strip starting at draft row i0.
+struct Strip {
+    int i0, R, jfirst, nchunks;
 };
 
-__device__ __forceinline__ void sweep_step(SweepState &st, int d, int rv, int width, int j, int M, bool last_row,
-                                           uint32_t *mycode, uint32_t *sink, int *rowOut) {
-    const int lane = threadIdx.x;
-    const bool inb = (unsigned)st.o < (unsigned)width;
-    const int above = from_lane_below(st.cur, rv);  // C(i-1, j)
-    const int diagv = st.above_prev;                // C(i-1, j-1)
-    st.above_prev = above;
-    const int left = st.cur;                        // C(i, j-1)
-    // ties: diagonal, then (i-1, j), then (i, j-1)
-    const int m1 = above < diagv ? above : diagv;
-    const int c1 = above < diagv ? 1 : 0;
-    const int best = left < m1 ? left : m1;
-    const int code = left < m1 ? 2 : c1;
-    const int nc = d + best;
-    st.cur = inb ? nc : kInf;
-    st.lastc = inb ? nc : st.lastc;
-    const uint32_t keep = ((st.o & 15) == 0) ? 0u : st.cw;
-    st.cw = inb ? (keep | ((uint32_t)code << (2 * (st.o & 15)))) : st.cw;
-    uint32_t *cdst = inb ? (mycode + (st.o >> 4)) : (sink + lane);
-    *cdst = st.cw;
-    int *rdst = (last_row && j >= 0 && j <= M) ? (rowOut + j) : reinterpret_cast<int *>(sink + lane);
-    *rdst = st.cur;
-    ++st.o;
+__device__ __forceinline__ Strip strip_at(const Band &g, int s) {
+    Strip st;
+    st.i0 = 1 + s * kWave;
+    st.R = (g.K - st.i0 + 1) < kWave ? (g.K - st.i0 + 1) : kWave;
+    st.jfirst = g.jlo(st.i0);
+    const int steps = (g.jhi(st.i0 + st.R - 1) - st.jfirst + 1) + st.R - 1;
+    st.nchunks = (steps + kChunk - 1) / kChunk;
+    return st;
 }
 
-// Narrow strip: distances precomputed in `cost` as [step/4][lane] dwords.
-__device__ __forceinline__ void sweep_strip_narrow(const Band &g, int i0, int rows, const int *rowIn, int *rowOut,
-                                                   const uint32_t *cost, uint32_t *scode, uint32_t *sink,
-                                                   int &cost_km) {
-    const int lane = threadIdx.x;
-    const int i = i0 + lane;
-    const bool act = lane < rows;
-    const int myjlo = g.jlo(i);
-    const int width = act ? g.jhi(i) - myjlo + 1 : 0;
-    const int jfirst = g.jlo(i0);
-    const int jlast = g.jhi(i0 + rows - 1);
-    const int steps = (jlast - jfirst + 1) + rows - 1;
-    const int groups = (steps + 3) >> 2;
-    uint32_t *mycode = scode + lane * g.WPR;
-    const bool last_row = act && lane == rows - 1;
-
-    SweepState st;
-    st.cur = kInf;
-    st.lastc = kInf;
-    st.above_prev = (lane == 0) ? rowIn[jfirst - 1] : kInf;  // only lane 0 sees a finite C(i-1, j-1)
-    st.cw = 0;
-    st.o = jfirst - lane - myjlo;
-    uint32_t dw = cost[lane];
-    // lane 0 runs past column M at the end of the strip: those reads hit the INF pad at M+1
-    const int jcap = g.M + 1;
-    int r0 = rowIn[min(jfirst, jcap)], r1 = rowIn[min(jfirst + 1, jcap)];
-    int r2 = rowIn[min(jfirst + 2, jcap)], r3 = rowIn[min(jfirst + 3, jcap)];
-    for (int q = 0; q < groups; ++q) {
-        // prefetch the next group (the buffers are padded for the read past the end)
-        const uint32_t dwn = cost[(q + 1) * kWave + lane];
-        const int jn = jfirst + 4 * (q + 1);
-        const int n0 = rowIn[min(jn, jcap)], n1 = rowIn[min(jn + 1, jcap)];
-        const int n2 = rowIn[min(jn + 2, jcap)], n3 = rowIn[min(jn + 3, jcap)];
-        const int jb = jfirst + 4 * q - lane;
-        sweep_step(st, (int)(dw & 0xFFu), r0, width, jb, g.M, last_row, mycode, sink, rowOut);
-        sweep_step(st, (int)((dw >> 8) & 0xFFu), r1, width, jb + 1, g.M, last_row, mycode, sink, rowOut);
-        sweep_step(st, (int)((dw >> 16) & 0xFFu), r2, width, jb + 2, g.M, last_row, mycode, sink, rowOut);
-        sweep_step(st, (int)(dw >> 24), r3, width, jb + 3, g.M, last_row, mycode, sink, rowOut);
-        dw = dwn;
-        r0 = n0;
-        r1 = n1;
-        r2 = n2;
-        r3 = n3;
-    }
-    if (act && i == g.K) cost_km = st.lastc;
-}
-
-// Wide strip: each step evaluates the token distance of the lane's cell in place.
+// Token distances of chunk T0 / 64 of strip st: cell (i0 + r, jfirst + t - r) for
+// t in [T0, T0 + 64) goes to byte t & 3 of dword buf[r][(t - T0) / 4]; out-of-band
+// cells get 0x80.  Threads h, h + nh, ... each take four consecutive steps of one row.
 template <int TB>
-__device__ __forceinline__ void sweep_strip_wide(const Band &g, int i0, int rows, const int *rowIn, int *rowOut,
-                                                 const uint32_t *tslot, const uint8_t *tlen, const uint32_t *dslot,
-                                                 const uint8_t *dlen, uint32_t *scode, uint32_t *sink, int &cost_km) {
-    const int lane = threadIdx.x;
-    const int i = i0 + lane;
-    const bool act = lane < rows;
-    const int myjlo = g.jlo(i);
-    const int width = act ? g.jhi(i) - myjlo + 1 : 0;
-    const int jfirst = g.jlo(i0);
-    const int jlast = g.jhi(i0 + rows - 1);
-    const int steps = (jlast - jfirst + 1) + rows - 1;
-    uint32_t *mycode = scode + lane * g.WPR;
-    const bool last_row = act && lane == rows - 1;
-
-    uint32_t xw[TB / 4];
-    read_slot<TB>(dslot + (act ? i - 1 : 0) * (TB / 4), xw);
-    const int xm = act ? dlen[i - 1] : 0;
-
-    SweepState st;
-    st.cur = kInf;
-    st.lastc = kInf;
-    st.above_prev = (lane == 0) ? rowIn[jfirst - 1] : kInf;
-    st.cw = 0;
-    st.o = jfirst - lane - myjlo;
-    uint32_t yw[TB / 4];
-    int jc = clampi(jfirst - lane, 1, g.M);
-    read_slot<TB>(tslot + (jc - 1) * (TB / 4), yw);
-    int yn = tlen[jc - 1];
-    const int jcap = g.M + 1;  // lane 0 runs past column M at the end: the INF pad
-    int rv = rowIn[min(jfirst, jcap)];
-    for (int t = 0; t < steps; ++t) {
-        const int j = jfirst + t - lane;
-        const int d = token_distance<TB>(xw, xm, yw, yn);
-        const int rvn = rowIn[min(jfirst + t + 1, jcap)];
-        jc = clampi(j + 1, 1, g.M);
-        uint32_t ywn[TB / 4];
-        read_slot<TB>(tslot + (jc - 1) * (TB / 4), ywn);
-        const int ynn = tlen[jc - 1];
-        sweep_step(st, d, rv, width, j, g.M, last_row, mycode, sink, rowOut);
-        rv = rvn;
-#pragma unroll
-        for (int q = 0; q < TB / 4; ++q) yw[q] = ywn[q];
-        yn = ynn;
-    }
-    if (act && i == g.K) cost_km = st.lastc;
-}
-
-// Token distances of the band cells of the strip starting at row i0 into `cost`, laid out by
-// sweep step (cell (i0 + r, j) at step t = j - jlo(i0) + r, byte t & 3 of dword
-// [t / 4][r]); threads tid, tid + nthr, ... each take one cell.
-template <int TB>
-__device__ __forceinline__ void strip_costs(const Band &g, int i0, int rows, uint8_t *cost, const uint32_t *tslot,
-                                            const uint8_t *tlen, const uint32_t *dslot, const uint8_t *dlen, int tid,
-                                            int nthr) {
-    const int ncell = rows * g.W;
-    const float invW = 1.0f / (float)g.W;
-    const int jfirst = g.jlo(i0);
-    for (int idx = tid; idx < ncell; idx += nthr) {
-        int r = (int)((float)idx * invW);
-        int c = idx - r * g.W;
-        if (c < 0) {
-            --r;
-            c += g.W;
-        } else if (c >= g.W) {
-            ++r;
-            c -= g.W;
-        }
-        const int i = i0 + r;
-        const int j = g.jlo(i) + c;
-        if (j <= g.jhi(i)) {
-            uint32_t xw[TB / 4], yw[TB / 4];
+__device__ __forceinline__ void chunk_costs(const Band &g, const Strip &st, int T0, uint32_t *buf,
+                                            const uint32_t *tslot, const uint8_t *tlen, const uint32_t *dslot,
+                                            const uint8_t *dlen, int h, int nh) {
+    for (int item = h; item < st.R * kGroups; item += nh) {
+        const int r = item / kGroups, gq = item % kGroups;
+        const int i = st.i0 + r;
+        const int jl = g.jlo(i), jh = g.jhi(i);
+        const int jb = st.jfirst + T0 + 4 * gq - r;  // column of the item's first step
+        uint32_t packed = kOutOfBand;
+        if (jb <= jh && jb + 3 >= jl) {
+            uint32_t xw[TB / 4];
             read_slot<TB>(dslot + (i - 1) * (TB / 4), xw);
-            read_slot<TB>(tslot + (j - 1) * (TB / 4), yw);
-            const int t = j - jfirst + r;
-            cost[((t >> 2) * kWave + r) * 4 + (t & 3)] = (uint8_t)token_distance<TB>(xw, dlen[i - 1], yw, tlen[j - 1]);
+            const int xm = dlen[i - 1];
+            for (int u = 0; u < 4; ++u) {
+                const int j = jb + u;
+                if (j >= jl && j <= jh) {
+                    uint32_t yw[TB / 4];
+                    read_slot<TB>(tslot + (j - 1) * (TB / 4), yw);
+                    const uint32_t d = (uint32_t)token_distance<TB>(xw, xm, yw, tlen[j - 1]);
+                    packed = (packed & ~(0xFFu << (8 * u))) | (d << (8 * u));
+                }
+            }
         }
+        buf[r * kCostStride + gq] = packed;
+    }
+}
+
+// Per-lane state of the strip sweep (wave 0, lane r = row i0 + r).
+struct Sweep {
+    int cur;         // C of the lane's latest cell
+    int above_prev;  // C(i-1, j-1) of the next cell
+    uint32_t cw;     // predecessor codes of the latest 16 steps
+    uint32_t oob;    // kOutOfBand for lanes past the strip's last row
+    int kr0;         // first stored code word of the row (in steps / 16 of the strip)
+    bool act, last;
+    uint32_t *prow;  // the row's code words in the workspace
+};
+
+// Steps T0 .. T0 + 63 of the sweep.  rowIn / rowOut point at column 0 of the row buffers,
+// which are infinite past column M far enough for lane 0's reads of C(i0 - 1, j).
+__device__ __forceinline__ void sweep_chunk(Sweep &sw, const uint32_t *buf, const int *rowIn, int *rowOut, int T0,
+                                            int jfirst, int rw) {
+    const int lane = threadIdx.x;
+    const uint32_t *myc = buf + lane * kCostStride;
+    const int *rin = rowIn + jfirst + T0;  // lane 0's C(i0 - 1, j) at the chunk's steps
+    uint32_t dw = myc[0] | sw.oob;
+    int rv[4] = {rin[0], rin[1], rin[2], rin[3]};
+#pragma unroll
+    for (int gq = 0; gq < kGroups; ++gq) {
+        // the next group's inputs (the last group reads the buffer's pad column)
+        const uint32_t dwn = myc[gq + 1] | sw.oob;
+        const int rvn[4] = {rin[4 * gq + 4], rin[4 * gq + 5], rin[4 * gq + 6], rin[4 * gq + 7]};
+        int c[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int d = ((int)(dw << (24 - 8 * u))) >> 24;  // negative outside the band
+            const int above = __builtin_amdgcn_update_dpp(rv[u], sw.cur, 0x138 /* wave_shr:1 */, 0xF, 0xF, false);
+            const int diag = sw.above_prev;
+            sw.above_prev = above;
+            // ties: diagonal, then (i-1, j), then (i, j-1); each choice bit is the sign of a
+            // difference shifted into the code word (values stay below 2^31)
+            const int m1 = above < diag ? above : diag;
+            sw.cw = __builtin_amdgcn_alignbit(sw.cw, (uint32_t)(above - diag), 31);  // up
+            sw.cw = __builtin_amdgcn_alignbit(sw.cw, (uint32_t)(sw.cur - m1), 31);   // left
+            const int best = sw.cur < m1 ? sw.cur : m1;
+            sw.cur = d < 0 ? kInf : d + best;
+            c[u] = sw.cur;
+        }
+        // keep the code word current every group: left to itself the compiler defers the
+        // choice bits of 16 steps to the store and holds all their operands live
+        asm volatile("" : "+v"(sw.cw));
+        if (sw.last) {  // the strip's last row feeds the next strip
+            int *dst = rowOut + (jfirst + T0 + 4 * gq - lane);
+            dst[0] = c[0];
+            dst[1] = c[1];
+            dst[2] = c[2];
+            dst[3] = c[3];
+        }
+        if ((gq & 3) == 3) {  // 16 steps make code word k of the row
+            const int k = (T0 >> 4) + (gq >> 2) - sw.kr0;
+            if (sw.act && (unsigned)k < (unsigned)rw) sw.prow[k] = sw.cw;
+        }
+        dw = dwn;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) rv[u] = rvn[u];
     }
 }
 
 template <int TB>
-__global__ void __launch_bounds__(kThreads) dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride) {
+__global__ void __launch_bounds__(band_threads<TB>()) __attribute__((amdgpu_waves_per_eu(band_threads<TB>() / 64)))
+dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
+                                                     int rw) {
+    constexpr int kThreads = band_threads<TB>();
+    constexpr int kHelpers = kThreads - kWave;
     extern __shared__ __align__(16) uint8_t lds[];
     const int b = blockIdx.x;
-    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int tid = threadIdx.x, lane = tid % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: wave-level branches stay scalar
     const int d0 = a.draft_off[b], K = a.draft_off[b + 1] - d0;
     const int t0 = a.target_off[b], M = a.target_off[b + 1] - t0;
 
@@ -325,16 +255,15 @@ __global__ void __launch_bounds__(kThreads) dtw_band(AlignArgs a, LdsPlan lp, ui
     uint8_t *tlen = lds + lp.tlen;
     uint32_t *dslot = reinterpret_cast<uint32_t *>(lds + lp.dslot);
     uint8_t *dlen = lds + lp.dlen;
-    int *rowIn = reinterpret_cast<int *>(lds + lp.row0);
-    int *rowOut = reinterpret_cast<int *>(lds + lp.row1);
-    uint8_t *costbuf[2] = {lds + lp.cost, lds + lp.cost + lp.cost_bytes};
-    uint32_t *scode = reinterpret_cast<uint32_t *>(lds + lp.scode);
-    uint32_t *pathbuf = reinterpret_cast<uint32_t *>(lds + lp.path);
-    uint32_t *sink = reinterpret_cast<uint32_t *>(lds + lp.sink);
-    __shared__ int s_cost;
+    int *rowIn = reinterpret_cast<int *>(lds + lp.row0) + kRowFront;
+    int *rowOut = reinterpret_cast<int *>(lds + lp.row1) + kRowFront;
+    uint32_t *costbuf = reinterpret_cast<uint32_t *>(lds + lp.cost);  // two halves of kWave * kCostStride
+    uint32_t *seg = reinterpret_cast<uint32_t *>(lds + lp.path);  // [K]: first column << 16 | entry column
+    uint32_t *poff = seg + a.max_k;                               // [K]: index of the row's first path cell
     __shared__ int votes[kThreads / kWave];
+    __shared__ int s_imin, s_n;
 
-    // ---- staging + validation: one token (draft or target) per thread
+    // ---- staging + validation: one token (draft or target) per thread and pass
     const bool shape_ok = K >= 1 && K <= a.max_k && M >= 1 && M <= a.max_m;
     int bad = shape_ok ? 0 : 1;
     if (shape_ok) {
@@ -362,163 +291,144 @@ __global__ void __launch_bounds__(kThreads) dtw_band(AlignArgs a, LdsPlan lp, ui
     g.L = (a.w < 0) ? mx : (a.w > abs(K - M) ? a.w : abs(K - M));
     if (g.L > mx) g.L = mx;
     g.W = (2 * g.L + 1 < M) ? 2 * g.L + 1 : M;
-    g.WPR = (g.W + 15) >> 4;
-    const bool pre = g.W <= lp.cost_w;  // distances precomputed strip by strip
     const int nstrips = (K + kWave - 1) / kWave;
-    uint32_t *parked = gcodes + (size_t)b * gcode_stride;  // codes of finished strips (K > 64 only)
+    uint32_t *parked = gcodes + (size_t)b * gcode_stride;  // code words of row i at (i - 1) * rw
 
-    // ---- strips of 64 rows: wave 0 sweeps strip s while the other waves compute the
-    // distances of strip s + 1 into the other buffer
-    if (pre) strip_costs<TB>(g, 1, K < kWave ? K : kWave, costbuf[0], tslot, tlen, dslot, dlen, tid, kThreads);
+    // ---- chunked sweep: wave 0 sweeps a chunk while waves 1-3 evaluate the next one
+    if (wave == 0) {
+        for (int j = lane - kRowFront; j < M + kRowBack; j += kWave) {
+            rowIn[j] = (j == 0) ? 0 : kInf;  // C(0, j)
+            rowOut[j] = kInf;
+        }
+    }
+    Strip st = strip_at(g, 0);
+    chunk_costs<TB>(g, st, 0, costbuf, tslot, tlen, dslot, dlen, tid, kThreads);
+    __syncthreads();
     // the sweep is the critical path: its wave wins issue arbitration on its SIMD
     if (wave == 0) __builtin_amdgcn_s_setprio(3);
-    for (int j = tid; j <= M + kRowPad; j += kThreads) rowIn[j] = (j == 0) ? 0 : kInf;  // C(0, j)
-    __syncthreads();
-    int cost_km = kInf;
+    int gidx = 0;  // chunks swept so far (selects the buffer half)
+    Sweep sw;
     for (int s = 0; s < nstrips; ++s) {
-        const int i0 = 1 + s * kWave;
-        const int rows = (K - i0 + 1) < kWave ? (K - i0 + 1) : kWave;
         if (wave == 0) {
-            for (int j = lane; j <= M + kRowPad; j += kWave) rowOut[j] = kInf;
-            if (pre)
-                sweep_strip_narrow(g, i0, rows, rowIn, rowOut, reinterpret_cast<const uint32_t *>(costbuf[s & 1]),
-                                   scode, sink, cost_km);
-            else
-                sweep_strip_wide<TB>(g, i0, rows, rowIn, rowOut, tslot, tlen, dslot, dlen, scode, sink, cost_km);
-            if (s + 1 < nstrips) {  // park this strip's codes; the last strip stays in LDS
-                for (int e = lane; e < rows * g.WPR; e += kWave) parked[(size_t)(i0 - 1) * g.WPR + e] = scode[e];
-            }
-        } else if (pre && s + 1 < nstrips) {
-            const int i1 = i0 + kWave;
-            const int rows1 = (K - i1 + 1) < kWave ? (K - i1 + 1) : kWave;
-            strip_costs<TB>(g, i1, rows1, costbuf[(s + 1) & 1], tslot, tlen, dslot, dlen, tid - kWave,
-                            kThreads - kWave);
+            const int i = st.i0 + lane;
+            sw.act = lane < st.R;
+            sw.last = lane == st.R - 1;
+            sw.oob = sw.act ? 0u : kOutOfBand;
+            sw.kr0 = sw.act ? (g.jlo(i) - st.jfirst + lane) >> 4 : 0;
+            sw.prow = parked + (size_t)(sw.act ? i - 1 : 0) * rw;
+            sw.cur = kInf;
+            sw.above_prev = (lane == 0) ? rowIn[st.jfirst - 1] : kInf;
+            sw.cw = 0;
         }
-        __syncthreads();
-        int *tmp = rowIn;
+        const Strip nxt = (s + 1 < nstrips) ? strip_at(g, s + 1) : st;
+        for (int c = 0; c < st.nchunks; ++c) {
+            uint32_t *cur_buf = costbuf + (gidx & 1) * kWave * kCostStride;
+            uint32_t *next_buf = costbuf + ((gidx + 1) & 1) * kWave * kCostStride;
+            if (wave == 0) {
+                sweep_chunk(sw, cur_buf, rowIn, rowOut, c * kChunk, st.jfirst, rw);
+            } else if (c + 1 < st.nchunks) {
+                chunk_costs<TB>(g, st, (c + 1) * kChunk, next_buf, tslot, tlen, dslot, dlen, tid - kWave, kHelpers);
+            } else if (s + 1 < nstrips) {
+                chunk_costs<TB>(g, nxt, 0, next_buf, tslot, tlen, dslot, dlen, tid - kWave, kHelpers);
+            }
+            __syncthreads();
+            ++gidx;
+        }
+        int *tmp = rowIn;  // the strip's last row is the next strip's row above
         rowIn = rowOut;
         rowOut = tmp;
+        if (wave == 0 && s + 1 < nstrips) {
+            for (int j = lane - kRowFront; j < M + kRowBack; j += kWave) rowOut[j] = kInf;
+        }
+        st = nxt;
     }
-    if (wave == 0 && lane == (K - 1) % kWave) s_cost = cost_km;
-    // every row's codes in one LDS matrix when they fit in the (now free) cost buffers:
-    // the parked strips come back in parallel, the last strip is still in scode
-    const size_t code_words = (size_t)K * g.WPR;
-    uint32_t *codes = reinterpret_cast<uint32_t *>(lds + lp.cost);
-    const bool all_codes = 4 * code_words <= 2 * lp.cost_bytes;
-    if (all_codes) {
-        const size_t last0 = (size_t)(nstrips - 1) * kWave * g.WPR;  // first word of the last strip
-        for (size_t e = tid; e < code_words; e += kThreads)
-            codes[e] = e < last0 ? parked[e] : scode[e - last0];
-    }
-    __syncthreads();
-    uint32_t *seg = pathbuf;              // [K]: first column << 16 | entry column (0: not on the path)
-    uint32_t *poff = pathbuf + a.max_k;   // [K]: index of the row's first path cell
-    __shared__ int s_imin, s_n;
 
     // ---- backtrack (wave 0): inside row i the path runs left from its entry column e to
     // the highest column x <= e whose move is not (i, j-1); it enters row i-1 at x - 1
     // after a diagonal move and at x after an (i-1, j) move
-    if (wave == 0) {
-        if (lane == 0) a.cost[b] = s_cost;
-        int e = M, i = K;
-        if (all_codes && g.WPR <= kWave) {
-            // lane l holds code word l of a row; two rows are searched per iteration while
-            // the next two are read, and the runs are buffered one per lane (row i in lane
-            // (i - 1) % 64) and flushed to LDS every 64 rows, so the walk is branch-free
-            auto row_words = [&](int r) {  // code word `lane` of row r (0 past the band or row 0)
-                return (r >= 1 && lane < g.WPR) ? codes[(size_t)(r - 1) * g.WPR + lane] : 0u;
-            };
-            uint32_t segbuf = 0;
-            bool live = true;
-            auto walk_row = [&](int r, uint32_t cur) {
-                const int jl = g.jlo(r);
-                const int c = e - jl;  // band offset of the entry column
-                const int we = c >> 4, p15 = c & 15;
-                const uint32_t nl = 0x55555555u & ~((cur >> 1) & ~cur);  // low bit of codes other than 2
-                const uint32_t pm = p15 == 15 ? 0xFFFFFFFFu : ((1u << (2 * p15 + 2)) - 1u);
-                const uint32_t m = nl & (lane < we ? 0xFFFFFFFFu : (lane == we ? pm : 0u));
-                const unsigned long long has = __ballot(m != 0u);
-                const int lw = has ? 63 - __clzll(has) : 0;
-                const uint32_t mw = __builtin_amdgcn_readlane(m, lw);
-                const uint32_t ww = __builtin_amdgcn_readlane(cur, lw);
-                const int hb = 31 - __clz(mw | 1u);
-                const int x = jl + lw * 16 + (hb >> 1);
-                segbuf = (lane == ((r - 1) & (kWave - 1))) ? (((uint32_t)x << 16) | (uint32_t)e) : segbuf;
-                if (((r - 1) & (kWave - 1)) == 0 && r - 1 + lane < K) seg[r - 1 + lane] = segbuf;
-                // has == 0 never happens: a run of (i, j-1) moves ends inside the band
-                live = has != 0ull;
-                e = ((ww >> hb) & 3u) == 0u ? x - 1 : x;
-            };
-            uint32_t c0 = row_words(K), c1 = row_words(K - 1);
-            for (; i >= 1; i -= 2) {
-                const uint32_t n0 = row_words(i - 2), n1 = row_words(i - 3);
-                walk_row(i, c0);
-                if (!live) break;  // row i is not on the path
-                if (e < 1 || i == 1) {
-                    --i;
-                    break;
-                }
-                walk_row(i - 1, c1);
-                if (!live) {
-                    --i;
-                    break;
-                }
-                if (e < 1) {
-                    i -= 2;
-                    break;
-                }
-                c0 = n0;
-                c1 = n1;
+    __builtin_amdgcn_s_waitcnt(0);  // wave 0's code-word stores are complete before they are read back
+    int e = M;      // entry column of the row being walked (lane 0 of wave 0)
+    int first = 1;  // first row on the path
+    // Lane 0 walks rows rtop down to i0 of one strip; word(rr, k) is code word k of row
+    // i0 + rr.  Returns true while the path goes on below the strip.
+    auto walk_strip = [&](int i0, int rtop, auto word) -> bool {
+        const int jf = g.jlo(i0);
+        for (int r = rtop; r >= i0; --r) {
+            const int rr = r - i0;
+            const int kr0 = (g.jlo(r) - jf + rr) >> 4;
+            const int te = e - jf + rr;  // sweep step of the entry cell
+            int k = (te >> 4) - kr0;
+            if (k < 0 || k >= rw) {  // never: the entry column lies inside the row's band
+                first = r + 1;
+                return false;
             }
-            // the partial block of rows the walk ended in
-            const int rl = i + 1;  // last row written: rows rl.. are in seg or segbuf
-            const int blk = (rl - 1) & ~(kWave - 1);
-            if (rl >= 1 && ((rl - 1) & (kWave - 1)) != 0) {
-                const int r = blk + lane;
-                if (r >= rl - 1 && r < K && r < blk + kWave) seg[r] = segbuf;
+            uint32_t w = word(rr, k);
+            // cells whose move is not (i, j-1), at steps <= te
+            uint32_t m = ~w & 0x55555555u & (0xFFFFFFFFu << (30 - 2 * (te & 15)));
+            while (m == 0u && k > 0) {  // the run continues into the word below
+                --k;
+                w = word(rr, k);
+                m = ~w & 0x55555555u;
             }
-            if (i < 0) i = 0;
-        } else {
-            int strip = nstrips - 1;  // strip held in scode when the codes are not all in LDS
-            for (; i >= 1; --i) {
-                const uint32_t *rc;
-                if (all_codes) {
-                    rc = codes + (size_t)(i - 1) * g.WPR;
-                } else {
-                    if (i < 1 + strip * kWave) {  // fetch the strip above from the workspace
-                        --strip;
-                        for (int e2 = lane; e2 < kWave * g.WPR; e2 += kWave)
-                            scode[e2] = parked[(size_t)strip * kWave * g.WPR + e2];
-                    }
-                    rc = scode + (size_t)(i - 1 - strip * kWave) * g.WPR;
-                }
-                const int jl = g.jlo(i);
-                const int c = e - jl;
-                int w = c >> 4;
-                const int p15 = c & 15;
-                uint32_t word = rc[w];
-                uint32_t m = 0x55555555u & ~((word >> 1) & ~word) &
-                             (p15 == 15 ? 0xFFFFFFFFu : ((1u << (2 * p15 + 2)) - 1u));
-                while (m == 0 && w > 0) {
-                    --w;
-                    word = rc[w];
-                    m = 0x55555555u & ~((word >> 1) & ~word);
-                }
-                if (m == 0) break;  // never taken
-                const int hb = 31 - __clz(m);
-                const int x = jl + w * 16 + (hb >> 1);
-                if (lane == 0) seg[i - 1] = ((uint32_t)x << 16) | (uint32_t)e;
-                e = ((word >> hb) & 3u) == 0u ? x - 1 : x;
-                if (e < 1) {
-                    --i;
-                    break;
-                }
+            if (m == 0u) {  // never: the band's first cell is not a left move
+                first = r + 1;
+                return false;
+            }
+            const int pos = __builtin_ctz(m);
+            const int x = jf + 16 * (kr0 + k) + ((30 - pos) >> 1) - rr;
+            seg[r - 1] = ((uint32_t)x << 16) | (uint32_t)e;
+            e = ((w >> (pos + 1)) & 1u) ? x : x - 1;
+            if (e < 1 || r == 1) {
+                first = r;
+                return false;
             }
         }
-        // rows 1..i are not on the path (only if the walk broke off); path offsets for the rest
-        const int imin = i + 1;
+        return true;
+    };
+    if (rw <= kWave) {
+        // each strip's code words are staged into the freed cost buffers by the other waves
+        // while wave 0 walks the strip below it in the other half
+        uint32_t *stg = costbuf;
+        auto copy_strip = [&](int s, int h, int nh) {
+            const int i0 = 1 + s * kWave;
+            const int R = (K - i0 + 1) < kWave ? (K - i0 + 1) : kWave;
+            const uint32_t *src = parked + (size_t)(i0 - 1) * rw;
+            uint32_t *dst = stg + (s & 1) * kWave * rw;
+            for (int e2 = h; e2 < R * rw; e2 += nh) dst[e2] = src[e2];
+        };
+        copy_strip(nstrips - 1, tid, kThreads);
+        __syncthreads();
+        bool walking = true;  // uniform over wave 0
+        for (int s = nstrips - 1; s >= 0; --s) {
+            if (wave != 0) {
+                if (s >= 1) copy_strip(s - 1, tid - kWave, kHelpers);
+            } else if (walking) {
+                const int i0 = 1 + s * kWave;
+                const uint32_t *half = stg + (s & 1) * kWave * rw;
+                int more = 1;
+                if (lane == 0) {
+                    const int rtop = (K < i0 + kWave - 1) ? K : i0 + kWave - 1;
+                    more = walk_strip(i0, rtop, [&](int rr, int k) { return half[rr * rw + k]; }) ? 1 : 0;
+                }
+                walking = __builtin_amdgcn_readfirstlane(more) != 0;
+            }
+            __syncthreads();
+        }
+    } else if (wave == 0 && lane == 0) {
+        // rows of more than 64 code words: read straight from the workspace
+        for (int s = nstrips - 1; s >= 0; --s) {
+            const int i0 = 1 + s * kWave;
+            const int rtop = (K < i0 + kWave - 1) ? K : i0 + kWave - 1;
+            auto word = [&](int rr, int k) { return parked[(size_t)(i0 - 1 + rr) * rw + k]; };
+            if (!walk_strip(i0, rtop, word)) break;
+        }
+    }
+    if (wave == 0) {
+        if (lane == 0) a.cost[b] = rowIn[M];  // C(K, M), from the last strip's last row
+        first = __builtin_amdgcn_readfirstlane(first);
+        // rows first..K are on the path: path offsets
         int carry = 0;
-        for (int r0 = imin - 1; r0 < K; r0 += kWave) {
+        for (int r0 = first - 1; r0 < K; r0 += kWave) {
             const int r = r0 + lane;
             const uint32_t sv = r < K ? seg[r] : 0u;
             const int len = r < K ? (int)(sv & 0xFFFFu) - (int)(sv >> 16) + 1 : 0;
@@ -527,13 +437,14 @@ __global__ void __launch_bounds__(kThreads) dtw_band(AlignArgs a, LdsPlan lp, ui
             carry = __builtin_amdgcn_readlane(incl, kWave - 1);
         }
         if (lane == 0) {
-            s_imin = imin;
+            s_imin = first;
             s_n = carry;
             a.path_len[b] = carry;
         }
     }
     __syncthreads();
-    const int imin = s_imin, n = s_n;
+    const int imin = s_imin;
+    const int n = s_n < K + M - 1 ? s_n : K + M - 1;  // a path has at most K + M - 1 cells
     // ---- path cells and map entries, all threads: binary searches over the rows' runs
     int32_t *pp = a.path + 2 * ((size_t)d0 + (size_t)t0);
     for (int q = tid; q < n; q += kThreads) {
@@ -562,18 +473,16 @@ template <int TB>
 int launch_tb(const AlignArgs &a, void *workspace, size_t workspace_bytes, hipStream_t stream) {
     const LdsPlan lp = plan_lds(a.max_k, a.max_m, a.w, TB);
     if (lp.total > kLdsLimit) return TT_EUNSUPPORTED;
-    const size_t stride = (size_t)a.max_k * (size_t)lp.wpr_max;  // parked code words per pair
-    uint32_t *gcodes = nullptr;
-    if (a.max_k > kWave) {
-        if (workspace == nullptr || workspace_bytes < 4 * stride * (size_t)a.n_pairs) return TT_EWORKSPACE;
-        gcodes = static_cast<uint32_t *>(workspace);
-    }
+    const int rw = row_words_bound(a.max_k, a.max_m, a.w);
+    const size_t stride = (size_t)a.max_k * (size_t)rw;  // code words per pair
+    if (workspace == nullptr || workspace_bytes < 4 * stride * (size_t)a.n_pairs) return TT_EWORKSPACE;
     if (lp.total > 64 * 1024) {
         if (hipFuncSetAttribute(reinterpret_cast<const void *>(&dtw_band<TB>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lp.total) != hipSuccess)
             return TT_ELAUNCH;
     }
-    hipLaunchKernelGGL(dtw_band<TB>, dim3(a.n_pairs), dim3(kThreads), lp.total, stream, a, lp, gcodes, stride);
+    hipLaunchKernelGGL(dtw_band<TB>, dim3(a.n_pairs), dim3(band_threads<TB>()), lp.total, stream, a, lp,
+                       static_cast<uint32_t *>(workspace), stride, rw);
     return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
 }
 
@@ -594,8 +503,8 @@ size_t align_lds_bytes(int32_t max_k, int32_t max_m, int32_t w, int tb) {
 }
 
 size_t align_workspace_bytes(int32_t n_pairs, int32_t max_k, int32_t max_m, int32_t w) {
-    if (max_k <= kWave) return 0;
-    return 4 * (size_t)n_pairs * (size_t)max_k * (size_t)words_per_row_bound(max_k, max_m, w);
+    if (TT_ALIGN_ROWS && align_rows_fits(max_k, max_m)) return 0;
+    return 4 * (size_t)n_pairs * (size_t)max_k * (size_t)row_words_bound(max_k, max_m, w);
 }
 
 int launch_align(const AlignArgs &a, void *workspace, size_t workspace_bytes, hipStream_t stream) {

@@ -20,45 +20,56 @@ struct MaskType<64> {
     using type = uint64_t;
 };
 
-// High bit of each byte of w that equals the byte broadcast in bc, compressed to 4 bits.
-__device__ __forceinline__ uint32_t byte_match4(uint32_t w, uint32_t bc) {
-    uint32_t t = w ^ bc;
-    uint32_t z = ~(((t & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | t) & 0x80808080u;
-    return (((z >> 7) * 0x00204081u) >> 21) & 0xFu;
+// Bit k set where byte k of the packed pattern xw equals the byte broadcast in bc.  Equal
+// bytes are found exactly by SWAR (0x80 in each byte of w ^ bc that is zero); v_dot4 then
+// gathers the four flags of a dword into four mask bits (byte weights 1, 2, 4, 8 times 0x80).
+template <int TB>
+__device__ __forceinline__ typename MaskType<TB>::type match_mask(const uint32_t (&xw)[TB / 4], uint32_t bc) {
+    using M = typename MaskType<TB>::type;
+    M eq = 0;
+#pragma unroll
+    for (int p = 0; p < TB / 8; ++p) {
+        uint32_t acc = 0;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const uint32_t t = xw[2 * p + h] ^ bc;
+            const uint32_t z = ~(((t & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | t) & 0x80808080u;
+            acc = __builtin_amdgcn_udot4(z, h ? 0x80402010u : 0x08040201u, acc, false);
+        }
+        eq |= M(acc >> 7) << (8 * p);
+    }
+    return eq;
 }
 
-// Edit distance between the packed pattern xw (m bytes) and the text bytes in yw (n bytes).
+__device__ __forceinline__ int popcount(uint32_t v) { return __popc(v); }
+__device__ __forceinline__ int popcount(uint64_t v) { return __popcll(v); }
+
+// Edit distance between the packed pattern xw (m bytes) and the text bytes in yw (n bytes):
+// Myers' bit-parallel recurrence over the text with the top row D(0, j) = j.  The distance
+// is read at the end from the last column's vertical deltas: D(m, n) = n + #(+1) - #(-1).
 template <int TB>
 __device__ __forceinline__ int bitparallel_distance(const uint32_t (&xw)[TB / 4], int m,
                                                     const uint32_t (&yw)[TB / 4], int n) {
     using M = typename MaskType<TB>::type;
     if (m == 0) return n;
     const M lim = (m >= (int)(8 * sizeof(M))) ? ~M(0) : ((M(1) << m) - 1);
-    const M hib = M(1) << (m - 1);
     M vp = ~M(0), vn = 0;
-    int score = m;
 #pragma unroll
     for (int k = 0; k < TB; ++k) {
         if (k < n) {
-            const uint32_t c = (yw[k >> 2] >> (8 * (k & 3))) & 0xFFu;
-            const uint32_t bc = __builtin_amdgcn_perm(0u, c, 0u);  // c in all four bytes
-            M eq = 0;
-#pragma unroll
-            for (int q = 0; q < TB / 4; ++q) eq |= M(byte_match4(xw[q], bc)) << (4 * q);
-            eq &= lim;
+            const uint32_t bc = __builtin_amdgcn_perm(0u, yw[k >> 2], (uint32_t)(k & 3) * 0x01010101u);
+            const M eq = match_mask<TB>(xw, bc) & lim;
             const M xv = eq | vn;
             const M xh = (((eq & vp) + vp) ^ vp) | eq;
             M hp = vn | ~(xh | vp);
             M hn = vp & xh;
-            score += (hp & hib) ? 1 : 0;
-            score -= (hn & hib) ? 1 : 0;
             hp = (hp << 1) | M(1);
             hn = hn << 1;
             vp = hn | ~(xv | hp);
             vn = hp & xv;
         }
     }
-    return score;
+    return n + popcount(vp & lim) - popcount(vn & lim);
 }
 
 // Edit distance is symmetric: iterate over the shorter token, the longer one is the pattern.

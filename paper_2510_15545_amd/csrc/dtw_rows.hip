@@ -27,7 +27,7 @@ __global__ void __launch_bounds__(kThreads) dtw_rows(AlignArgs a) {
         return;
     }
     const int L = rows::band_half_width(K, M, a.w);
-    const int wave = tid / rows::kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / rows::kWave);  // uniform per wave
     rows::init_border<TB>(s, tid, kThreads);
     rows::costs<TB>(s, K, M, L, tid, kThreads);
     __syncthreads();

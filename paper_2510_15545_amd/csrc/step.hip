@@ -52,7 +52,8 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     extern __shared__ uint64_t sh_part[];  // Q62 chunk sums of the selected row
 
     const int b = blockIdx.x;
-    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int tid = threadIdx.x, lane = tid % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: wave-level branches stay scalar
     const int d0 = al.draft_off[b], K = al.draft_off[b + 1] - d0;
     const int t0 = al.target_off[b], M = al.target_off[b + 1] - t0;
     const float us = ve.u_sample[b];  // needed only by the sampler, loaded while the rest runs

@@ -86,7 +86,8 @@ __device__ __forceinline__ bool accept_scan(const VerifyArgs &a, int b, int t0, 
 __global__ void __launch_bounds__(kRowThreads) verify_row(VParams p) {
     const VerifyArgs &a = p.a;
     const int b = blockIdx.x;
-    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int tid = threadIdx.x, lane = tid % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: wave-level branches stay scalar
     extern __shared__ uint64_t sh_part[];  // nc chunk sums
     __shared__ int sh_gamma, sh_ok;
 
@@ -137,7 +138,8 @@ __global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
     const int work = (g % kXcds) * (G / kXcds) + g / kXcds;
     if (work >= p.work_items) return;
     const int b = work / p.splits, s = work % p.splits;
-    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int tid = threadIdx.x, lane = tid % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: wave-level branches stay scalar
     __shared__ int sh_gamma, sh_ok;
 
     const int t0 = a.target_off[b];

@@ -155,7 +155,7 @@ __device__ __forceinline__ void sum_chunk(const float4 (&v)[4], const float *row
 template <class Store>
 __device__ __forceinline__ void stream_chunks(const float *row, int vt, bool vec, int c0, int c1, int stride,
                                               int rtok, float rq, Store store) {
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     int c = c0 + wave;
 #if TT_VERIFY_PREFETCH >= 2
     float4 v0[4], v1[4], v2[4];

@@ -41,8 +41,12 @@ def test_workspace_sizes_are_host_computed():
     assert L.tt_verify_workspace_size(-1, 10, ctypes.byref(n)) == tt.TT_EINVAL
     assert L.tt_align_workspace_size(256, 8, 64, 8, 8, ctypes.byref(n)) == 0 and n.value == 0
     assert L.tt_align_workspace_size(1024, 512, 512, 8, 8, ctypes.byref(n)) == 0
-    assert n.value == 1024 * 512 * 32 * 4  # 2-bit codes for a 512-wide band row
-    assert L.tt_align_workspace_size(8, 4096, 4096, -1, 8, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
+    assert n.value == 1024 * 512 * 33 * 4  # 2-bit codes for a 512-wide band row starting mid-word
+    assert L.tt_align_workspace_size(8, 4096, 4096, -1, 8, ctypes.byref(n)) == 0
+    assert n.value == 8 * 4096 * 257 * 4
+    # short pairs in a batch with one long target still take the strip kernel's workspace
+    assert L.tt_align_workspace_size(4, 8, 100, 8, 8, ctypes.byref(n)) == 0 and n.value == 4 * 8 * 8 * 4
+    assert L.tt_align_workspace_size(8, 4096, 4096, -1, 16, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
     assert L.tt_align_workspace_size(8, 16, 16, 8, 65, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
     # tt_step shares one workspace between its stages: the larger of the two
     a, v = ctypes.c_size_t(0), ctypes.c_size_t(0)
@@ -51,7 +55,7 @@ def test_workspace_sizes_are_host_computed():
         assert L.tt_align_workspace_size(args[0], args[2], args[3], args[4], args[5], ctypes.byref(a)) == 0
         assert L.tt_verify_workspace_size(args[0], args[1], ctypes.byref(v)) == 0
         assert n.value == max(a.value, v.value)
-    assert L.tt_step_workspace_size(8, 10, 4096, 4096, -1, 8, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
+    assert L.tt_step_workspace_size(8, 10, 4096, 4096, -1, 16, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
 
 
 def test_invalid_arguments_return_before_launch():
