@@ -27,9 +27,9 @@
 //     stored straight from registers into the caller's workspace, row-major by draft row.
 //   * Backtrack (wave 0), one row per step: inside row i the path runs left from its
 //     entry column to the highest column whose move is not a left move,
-//     then enters row i-1.  One lane walks: per row it reads the code word holding the
-//     entry cell, masks the steps past it and takes the lowest set bit of the not-left
-//     flags (the highest column).  The other waves stage the next strip's code words
+//     then enters row i-1.  The walk runs in scalar registers: per row the code word
+//     holding the entry cell is read (an LDS broadcast), the steps past it are masked and
+//     the lowest set bit of the not-left flags gives the highest column.  The other waves stage the next strip's code words
 //     into LDS meanwhile (rows of more than 64 words are read from the workspace).  Path
 //     cells and map entries are then written by all threads with binary searches over
 //     the rows' runs.
@@ -148,7 +148,9 @@ __device__ __forceinline__ Strip strip_at(const Band &g, int s) {
 
 // Token distances of chunk T0 / 64 of strip st: cell (i0 + r, jfirst + t - r) for
 // t in [T0, T0 + 64) goes to byte t & 3 of dword buf[r][(t - T0) / 4]; out-of-band
-// cells get 0x80.  Threads h, h + nh, ... each take four consecutive steps of one row.
+// cells get 0x80.  Threads h, h + nh, ... each take four consecutive steps of one row, and
+// consecutive threads consecutive steps: a wave's lanes then leave the band together
+// (rows in consecutive lanes would diverge at every band edge).
 template <int TB>
 __device__ __forceinline__ void chunk_costs(const Band &g, const Strip &st, int T0, uint32_t *buf,
                                             const uint32_t *tslot, const uint8_t *tlen, const uint32_t *dslot,
@@ -347,43 +349,52 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
     // the highest column x <= e whose move is not (i, j-1); it enters row i-1 at x - 1
     // after a diagonal move and at x after an (i-1, j) move
     __builtin_amdgcn_s_waitcnt(0);  // wave 0's code-word stores are complete before they are read back
-    int e = M;      // entry column of the row being walked (lane 0 of wave 0)
+    int e = M;      // entry column of the row being walked (uniform over wave 0)
     int first = 1;  // first row on the path
-    // Lane 0 walks rows rtop down to i0 of one strip; word(rr, k) is code word k of row
-    // i0 + rr.  Returns true while the path goes on below the strip.
+    // Wave 0 walks rows rtop down to i0 of one strip with uniform (scalar) state; word(rr, k)
+    // is code word k of row i0 + rr, read by every lane at the same address.  The run of
+    // row i0 + l is recorded in lane l and the strip's records are written at the end.
+    // Returns true while the path goes on below the strip.
     auto walk_strip = [&](int i0, int rtop, auto word) -> bool {
         const int jf = g.jlo(i0);
-        for (int r = rtop; r >= i0; --r) {
+        uint32_t rec = 0;
+        bool more = true;
+        int r = rtop;
+        for (; r >= i0; --r) {
             const int rr = r - i0;
             const int kr0 = (g.jlo(r) - jf + rr) >> 4;
             const int te = e - jf + rr;  // sweep step of the entry cell
             int k = (te >> 4) - kr0;
             if (k < 0 || k >= rw) {  // never: the entry column lies inside the row's band
-                first = r + 1;
-                return false;
+                more = false;
+                break;
             }
-            uint32_t w = word(rr, k);
+            uint32_t w = __builtin_amdgcn_readfirstlane(word(rr, k));
             // cells whose move is not (i, j-1), at steps <= te
             uint32_t m = ~w & 0x55555555u & (0xFFFFFFFFu << (30 - 2 * (te & 15)));
             while (m == 0u && k > 0) {  // the run continues into the word below
                 --k;
-                w = word(rr, k);
+                w = __builtin_amdgcn_readfirstlane(word(rr, k));
                 m = ~w & 0x55555555u;
             }
             if (m == 0u) {  // never: the band's first cell is not a left move
-                first = r + 1;
-                return false;
+                more = false;
+                break;
             }
             const int pos = __builtin_ctz(m);
             const int x = jf + 16 * (kr0 + k) + ((30 - pos) >> 1) - rr;
-            seg[r - 1] = ((uint32_t)x << 16) | (uint32_t)e;
+            rec = lane == rr ? (((uint32_t)x << 16) | (uint32_t)e) : rec;
             e = ((w >> (pos + 1)) & 1u) ? x : x - 1;
             if (e < 1 || r == 1) {
-                first = r;
-                return false;
+                more = false;
+                --r;
+                break;
             }
         }
-        return true;
+        // rows r + 1 .. rtop were walked
+        if (lane + i0 > r && lane + i0 <= rtop) seg[i0 - 1 + lane] = rec;
+        if (!more) first = r + 1;
+        return more;
     };
     if (rw <= kWave) {
         // each strip's code words are staged into the freed cost buffers by the other waves
@@ -405,16 +416,12 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
             } else if (walking) {
                 const int i0 = 1 + s * kWave;
                 const uint32_t *half = stg + (s & 1) * kWave * rw;
-                int more = 1;
-                if (lane == 0) {
-                    const int rtop = (K < i0 + kWave - 1) ? K : i0 + kWave - 1;
-                    more = walk_strip(i0, rtop, [&](int rr, int k) { return half[rr * rw + k]; }) ? 1 : 0;
-                }
-                walking = __builtin_amdgcn_readfirstlane(more) != 0;
+                const int rtop = (K < i0 + kWave - 1) ? K : i0 + kWave - 1;
+                walking = walk_strip(i0, rtop, [&](int rr, int k) { return half[rr * rw + k]; });
             }
             __syncthreads();
         }
-    } else if (wave == 0 && lane == 0) {
+    } else if (wave == 0) {
         // rows of more than 64 code words: read straight from the workspace
         for (int s = nstrips - 1; s >= 0; --s) {
             const int i0 = 1 + s * kWave;
@@ -425,7 +432,6 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
     }
     if (wave == 0) {
         if (lane == 0) a.cost[b] = rowIn[M];  // C(K, M), from the last strip's last row
-        first = __builtin_amdgcn_readfirstlane(first);
         // rows first..K are on the path: path offsets
         int carry = 0;
         for (int r0 = first - 1; r0 < K; r0 += kWave) {
