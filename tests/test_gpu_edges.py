@@ -88,6 +88,23 @@ def test_strips_longer_than_a_wave():
         compare_align(wl, gpu_run(wl, w=w), oracle_run(wl, w=w))
 
 
+def test_band_rows_wider_than_a_wave_of_code_words():
+    """Band rows of more than 64 code words (W > 1008 cells): the backtrack reads code words
+    from the workspace instead of staging strips in LDS, and a run may cross many words."""
+    rng = np.random.default_rng(11)
+    toks = random_tokens(rng, 120, 1, 4)
+    v = vocab_of(toks)
+    pairs = []
+    for k, m in ((100, 1100), (1100, 100), (1030, 1050), (700, 1100), (1, 1100), (1100, 1)):
+        pairs.append((list(rng.integers(0, len(toks), k)), list(rng.integers(0, len(toks), m))))
+    # long runs of one repeated draft token make the path cross whole code words in one row
+    pairs.append(([3] * 40, list(rng.integers(0, len(toks), 1100))))
+    wl = workload(v, v, pairs, len(toks), len(toks), probs=False)
+    for w in (8, -1):
+        print(f"[case] wide rows w={w}", flush=True)
+        compare_align(wl, gpu_run(wl, w=w), oracle_run(wl, w=w))
+
+
 @pytest.mark.parametrize("kernel", ["rows", "strips"])
 def test_short_pair_extremes(kernel):
     """Pairs at the row-scan kernel's limits (K, M in {1, 63, 64}), through both alignment
