@@ -146,6 +146,41 @@ __device__ __forceinline__ Strip strip_at(const Band &g, int s) {
     return st;
 }
 
+// Edit distance between two tokens of at most 32 bytes: Myers' recurrence with the longer
+// token as the pattern (32-bit masks) and D(0, j) = j, read at the end from the vertical
+// deltas (as in the shared distance).  The loop over the shorter token's bytes leaves once
+// no lane of the wave has bytes left; lanes already done keep their state.
+template <int TB>
+__device__ __forceinline__ uint32_t short_distance(const uint32_t (&aw)[TB / 4], int m, const uint32_t *y, int n) {
+    uint32_t bw[TB / 4], pw[TB / 4], tw[TB / 4];
+    read_slot<TB>(y, bw);
+    const bool swap = n > m;
+#pragma unroll
+    for (int q = 0; q < TB / 4; ++q) {
+        pw[q] = swap ? bw[q] : aw[q];
+        tw[q] = swap ? aw[q] : bw[q];
+    }
+    const int pm = swap ? n : m, tn = swap ? m : n;
+    const uint32_t lim = pm >= 32 ? 0xFFFFFFFFu : ((1u << pm) - 1u);
+    uint32_t vp = 0xFFFFFFFFu, vn = 0;
+#pragma unroll
+    for (int k = 0; k < TB; ++k) {
+        const bool act = k < tn;
+        if (!__any(act)) break;
+        const uint32_t bc = __builtin_amdgcn_perm(0u, tw[k >> 2], (uint32_t)(k & 3) * 0x01010101u);
+        const uint32_t eq = dtw::match_mask<TB>(pw, bc) & lim;
+        const uint32_t xv = eq | vn;
+        const uint32_t xh = (((eq & vp) + vp) ^ vp) | eq;
+        const uint32_t hp = ((vn | ~(xh | vp)) << 1) | 1u;
+        const uint32_t hn = (vp & xh) << 1;
+        const uint32_t nvp = hn | ~(xv | hp);
+        const uint32_t nvn = hp & xv;
+        vp = act ? nvp : vp;
+        vn = act ? nvn : vn;
+    }
+    return (uint32_t)(tn + __popc(vp & lim) - __popc(vn & lim));
+}
+
 // Token distances of chunk T0 / 64 of strip st: cell (i0 + r, jfirst + t - r) for
 // t in [T0, T0 + 64) goes to byte t & 3 of dword buf[r][(t - T0) / 4]; out-of-band
 // cells get 0x80.  Threads h, h + nh, ... each take four consecutive steps of one row, and
@@ -165,12 +200,18 @@ __device__ __forceinline__ void chunk_costs(const Band &g, const Strip &st, int 
             uint32_t xw[TB / 4];
             read_slot<TB>(dslot + (i - 1) * (TB / 4), xw);
             const int xm = dlen[i - 1];
+#pragma unroll 1
             for (int u = 0; u < 4; ++u) {
                 const int j = jb + u;
                 if (j >= jl && j <= jh) {
-                    uint32_t yw[TB / 4];
-                    read_slot<TB>(tslot + (j - 1) * (TB / 4), yw);
-                    const uint32_t d = (uint32_t)token_distance<TB>(xw, xm, yw, tlen[j - 1]);
+                    uint32_t d;
+                    if constexpr (TB <= 32) {
+                        d = short_distance<TB>(xw, xm, tslot + (j - 1) * (TB / 4), tlen[j - 1]);
+                    } else {
+                        uint32_t yw[TB / 4];
+                        read_slot<TB>(tslot + (j - 1) * (TB / 4), yw);
+                        d = (uint32_t)token_distance<TB>(xw, xm, yw, tlen[j - 1]);
+                    }
                     packed = (packed & ~(0xFFu << (8 * u))) | (d << (8 * u));
                 }
             }
