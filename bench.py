@@ -55,13 +55,16 @@ def source_digest(files):
 KERNEL_SOURCES = {
     "step_fused": ("step.hip", "dtw_rows.h", "dtw_common.h", "verify_core.h"),
     "verify_row": ("verify.hip", "verify_core.h"),
+    "dtw_band": ("dtw.hip", "dtw_common.h"),
 }
+# int32 VALU issue peak of MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (a wave64 instruction
+# occupies its SIMD four cycles), in lane-operations per second
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 
 
-def read_traffic(path, workload, kernel):
-    """HBM bytes per launch of `kernel` from a counter summary (key: value lines), or None
-    when the file is missing, covers another workload or kernel, or was taken from other
-    kernel sources."""
+def read_counters(path, workload, kernel):
+    """key: value lines of a counter summary, or (None, reason) when the file is missing,
+    covers another workload or kernel, or was taken from other kernel sources."""
     if not path or not os.path.exists(path):
         return None, "no counter summary"
     kv = {}
@@ -76,6 +79,15 @@ def read_traffic(path, workload, kernel):
         return None, "counters cover kernel %r" % kv.get("kernel")
     if kv.get("source_sha256") != source_digest(KERNEL_SOURCES[kernel]):
         return None, "kernel changed since the counters were taken"
+    return kv, ""
+
+
+def read_traffic(path, workload, kernel):
+    """HBM bytes per launch of `kernel` from a counter summary (key: value lines), or None
+    when the summary does not apply (see read_counters)."""
+    kv, why = read_counters(path, workload, kernel)
+    if kv is None:
+        return None, why
     return int(kv["traffic_bytes_per_launch"]), "FETCH_SIZE x %s + WRITE_SIZE x %s" % (
         kv.get("fetch_scale"), kv.get("write_scale"))
 
@@ -328,9 +340,16 @@ def main():
                 "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic, "traffic_note": traffic_note,
                 "algorithmic_bytes_per_launch": kbytes, "launch_us": round(kms * 1e3, 2)}
     else:
-        roof = {"kernel": "dtw_band_wave", "bound": "alu", "achieved": round(cells_per_s / 1e9, 3),
-                "unit": "Gcells/s", "peak": None, "frac": None, "traffic": None,
-                "note": "see DESIGN.md for the ALU roofline of the alignment kernel"}
+        # the strip alignment kernel is bound by VALU issue: executed VALU lane-operations per
+        # second (instruction count from the SQ counter summary) against the VALU peak
+        kv, why = read_counters(os.path.join(ROOT, "profiles", "dtw_band_counters.txt"), wl_name, "dtw_band")
+        tops = None if kv is None else int(kv["valu_instructions_per_launch"]) * 64 / (times["align"] * 1e-3) / 1e12
+        roof = {"kernel": "dtw_band", "bound": "alu",
+                "achieved": None if tops is None else round(tops, 3), "peak": round(VALU_PEAK_TOPS, 2),
+                "unit": "TOP/s (VALU lane-ops)", "frac": None if tops is None else round(tops / VALU_PEAK_TOPS, 4),
+                "traffic": None, "cells_per_s": round(cells_per_s, 1), "launch_us": round(times["align"] * 1e3, 2),
+                "counter_note": why or "SQ_INSTS_VALU x 64 lanes per launch",
+                "lds_bank_conflict_rate": None if kv is None else float(kv["lds_bank_conflict_rate"])}
 
     result = {
         "metric": "verified draft tokens/s + DTW cells/s at V_t=151,936; verify HBM GB/s vs peak",
