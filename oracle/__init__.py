@@ -58,6 +58,8 @@ def lib():
         L.orc_verify.restype = None
         L.orc_verify_dense.argtypes = [i32, P, P, i32, f32, f32, P]
         L.orc_verify_dense.restype = i32
+        L.orc_sd_verify.argtypes = [i32, i32, P, P, P, i64, P, i64, P, P, i32, P, P, P, P, ctypes.c_int]
+        L.orc_sd_verify.restype = None
         L.orc_threshold.argtypes = [f32, u64]
         L.orc_threshold.restype = u64
         _lib = L
@@ -154,6 +156,35 @@ def verify_dense(p, qd, x, u_accept, u_sample):
     tok = lib().orc_verify_dense(len(p), _p(p), _p(qd), int(x), float(u_accept), float(u_sample),
                                  ctypes.byref(acc))
     return int(tok), int(acc.value)
+
+
+def sd_verify(v, draft_ids, off, draft_probs, target_probs, u_accept, u_sample, max_m=None,
+              residual=False, n_threads=None):
+    """App. D Alg. 4 with dense proposals over one vocabulary, for a batch of streams.
+
+    draft_ids/off: CSR drafted tokens; draft_probs row off[b]+j is the dense proposal of
+    drafted position j; target_probs row off[b]+b+j (j = 0..M_b) the target distribution.
+    Returns (n_accepted, out_token, residual or None, Z)."""
+    draft_ids = _c(draft_ids, np.int32)
+    off = _c(off, np.int32)
+    draft_probs = _c(draft_probs, np.float32)
+    target_probs = _c(target_probs, np.float32)
+    u_accept = _c(u_accept, np.float32)
+    u_sample = _c(u_sample, np.float32)
+    n = len(off) - 1
+    if max_m is None:
+        max_m = int(np.max(np.diff(off))) if n > 0 else 0
+    nacc = np.zeros(n, np.int32)
+    tok = np.zeros(n, np.int32)
+    z = np.zeros(n, np.uint64)
+    res = np.zeros((n, target_probs.shape[1]), np.float32) if residual else None
+    ids = draft_ids if draft_ids.size else np.zeros(1, np.int32)
+    dp = draft_probs if draft_probs.size else np.zeros((1, 1), np.float32)
+    ua = u_accept if u_accept.size else np.zeros(1, np.float32)
+    lib().orc_sd_verify(n, int(v), _p(ids), _p(off), _p(dp), dp.shape[1], _p(target_probs),
+                        target_probs.shape[1], _p(ua), _p(u_sample), int(max_m), _p(nacc), _p(tok),
+                        _p(res), _p(z), n_threads or threads_default())
+    return nacc, tok, res, z
 
 
 def threshold(u: float, Z: int) -> int:

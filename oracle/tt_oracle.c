@@ -21,6 +21,8 @@
  *   verify            Sec. 3 "Standard Speculative Sampling", Sec. 4.2.2 acceptance
  *                     rule, Sec. 4.2.3 / Alg. 2 bonus sample, App. D Alg. 4
  *                     (residual "modified distribution")
+ *   orc_sd_verify     App. D Alg. 4 with dense proposals over one vocabulary (standard
+ *                     speculative decoding, the homogeneous-vocabulary case)
  *
  * Readings where the paper is silent or ambiguous (each is listed in the design
  * notes of the repository):
@@ -408,6 +410,105 @@ int32_t orc_verify_dense(int32_t V, const float *p, const float *qd, int32_t x, 
     int32_t tok = (Z == 0) ? first_argmax(p, V) : sample_quantised(Rq, V, Z, u_sample);
     free(Rq);
     return tok;
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Standard speculative sampling over one vocabulary (App. D Alg. 4) for a batch of
+ * streams: the homogeneous-vocabulary case, where the proposal of drafted position j is
+ * the draft model's whole distribution q_j over the same V tokens as the target.
+ *
+ * Stream b drafted M_b = off[b+1] - off[b] tokens x_j = draft_ids[off[b] + j], each
+ * sampled from the dense row q_j = draft_probs[off[b] + j].  The target model scored the
+ * M_b + 1 prefixes: p_j = target_probs[off[b] + b + j], j = 0..M_b.
+ *   1. Alg. 4's loop: position j is kept when p_j(x_j) > q_j(x_j), or else with
+ *      probability p_j(x_j) / q_j(x_j).  With u_j = u_accept[off[b] + j] in [0, 1) both
+ *      cases are "u_j < p_j(x_j) / q_j(x_j)" (fp32 quotient); q_j(x_j) <= 0 keeps the
+ *      token (the quotient is +inf), as in the one-hot reading.  gamma = the first
+ *      position not kept, else M_b.
+ *   2. The modified distribution: after a rejection at r = gamma < M_b it is
+ *      max(0, p_r - q_r) (clamped to [0, 1], NaN -> 0), after full acceptance the plain
+ *      bonus row p_{M_b}.
+ *   3. The next token is drawn from it with u_sample[b] by the exact Q62 inverse CDF
+ *      (same quantisation, threshold and tie rules as orc_verify).
+ * A stream with M_b outside [0, max_m] or a drafted id outside [0, V) gets -1 outputs. */
+typedef struct {
+    int32_t V;
+    const int32_t *draft_ids, *off;
+    const float *draft_probs;
+    int64_t draft_ld;
+    const float *target_probs;
+    int64_t target_ld;
+    const float *u_accept, *u_sample;
+    int32_t max_m;
+    int32_t *n_accepted, *out_token;
+    float *residual;
+    uint64_t *z_out;
+} orc_sd_ctx;
+
+static void orc_sd_stream(orc_sd_ctx *c, int32_t b) {
+    int32_t o = c->off[b];
+    int32_t M = c->off[b + 1] - o;
+    int ok = M >= 0 && M <= c->max_m;
+    for (int32_t j = 0; ok && j < M; ++j) ok = c->draft_ids[o + j] >= 0 && c->draft_ids[o + j] < c->V;
+    if (!ok) {
+        c->n_accepted[b] = -1;
+        c->out_token[b] = -1;
+        if (c->z_out) c->z_out[b] = 0;
+        return;
+    }
+    /* step 1: keep drafted tokens until the first rejection */
+    int32_t gamma = M;
+    for (int32_t j = 0; j < M; ++j) {
+        int32_t x = c->draft_ids[o + j];
+        float p = c->target_probs[(int64_t)(o + b + j) * c->target_ld + x];
+        float qx = c->draft_probs[(int64_t)(o + j) * c->draft_ld + x];
+        float ratio = p / qx;
+        int keep = (qx <= 0.0f) || (c->u_accept[o + j] < ratio);
+        if (!keep) {
+            gamma = j;
+            break;
+        }
+    }
+    /* step 2: the modified distribution */
+    int32_t r = gamma;
+    const float *prow = c->target_probs + (int64_t)(o + b + r) * c->target_ld;
+    const float *qrow = (r < M) ? c->draft_probs + (int64_t)(o + r) * c->draft_ld : NULL;
+    int64_t V = c->V;
+    uint64_t *Rq = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)V);
+    uint64_t Z = 0;
+    for (int64_t y = 0; y < V; ++y) {
+        float R = residual_value(prow[y], qrow ? qrow[y] : 0.0f);
+        Rq[y] = (uint64_t)(R * 0x1p62f); /* Q62, truncating */
+        Z += Rq[y];
+    }
+    /* step 3: the next token */
+    int32_t token = (Z == 0) ? first_argmax(prow, V) : sample_quantised(Rq, V, Z, c->u_sample[b]);
+    c->n_accepted[b] = gamma;
+    c->out_token[b] = token;
+    if (c->z_out) c->z_out[b] = Z;
+    if (c->residual) {
+        float *res = c->residual + (int64_t)b * c->target_ld;
+        if (Z == 0) {
+            for (int64_t y = 0; y < V; ++y) res[y] = (y == token) ? 1.0f : 0.0f;
+        } else {
+            float zf = (float)Z * 0x1p-62f;
+            for (int64_t y = 0; y < V; ++y) res[y] = residual_value(prow[y], qrow ? qrow[y] : 0.0f) / zf;
+        }
+    }
+    free(Rq);
+}
+
+static void orc_sd_range(void *p, int32_t lo, int32_t hi) {
+    for (int32_t s = lo; s < hi; ++s) orc_sd_stream((orc_sd_ctx *)p, s);
+}
+
+void orc_sd_verify(int32_t n_streams, int32_t V, const int32_t *draft_ids, const int32_t *off,
+                   const float *draft_probs, int64_t draft_ld, const float *target_probs, int64_t target_ld,
+                   const float *u_accept, const float *u_sample, int32_t max_m, int32_t *n_accepted,
+                   int32_t *out_token, float *residual, uint64_t *z_out, int n_threads) {
+    orc_sd_ctx c = {V, draft_ids, off, draft_probs, draft_ld, target_probs, target_ld, u_accept, u_sample,
+                    max_m, n_accepted, out_token, residual, z_out};
+    orc_parallel(n_streams, n_threads, orc_sd_range, &c);
 }
 
 /* Test hook: the exact threshold floor(u * Z). */
