@@ -186,6 +186,44 @@ int tt_verify(int32_t n_streams, int32_t v_t,
               void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * tt_verify_dense -- standard speculative sampling with dense proposals over one
+ * vocabulary (App. D Alg. 4; the homogeneous-vocabulary case, where the draft
+ * model's whole distribution over the target's tokens is the proposal).  It is
+ * tt_verify with the one-hot transferred mass q_j replaced by a full draft row.
+ *
+ * Inputs (device):
+ *   draft_ids    [sum M_b] drafted tokens x_j (CSR by off), ids in [0, v)
+ *   off          [n_streams + 1] CSR offsets, M_b = off[b+1] - off[b]
+ *   draft_probs  fp32 rows of width v, stride draft_ld >= v elements; row
+ *                off[b] + j is the distribution q_j that x_j was drawn from
+ *   target_probs fp32 rows of width v, stride target_ld >= v; stream b owns the
+ *                M_b + 1 rows starting at row off[b] + b (row j: the target's
+ *                distribution after x_1..x_j; row M_b is the bonus row)
+ *   u_accept     [sum M_b] uniforms in [0,1), u_sample [n_streams] in [0,1)
+ *   max_m        bound on M_b (0..65536); a stream outside [0, max_m] or with an
+ *                id outside [0, v) gets n_accepted = out_token = -1
+ * Outputs (device):
+ *   n_accepted[b]  gamma: x_j is kept while u_j < p_j(x_j) / q_j(x_j) (fp32,
+ *                  round-to-nearest; q_j(x_j) <= 0 keeps it), stopping at the
+ *                  first rejection
+ *   out_token[b]   with r = gamma, a sample of R(x) = max(0, p_r(x) - q_r(x))
+ *                  if r < M_b, or of p_{M_b}(x) if every draft was kept; R is
+ *                  clamped, quantised and sampled exactly as in tt_verify
+ *   residual       optional (may be NULL): [n_streams x target_ld] fp32, the
+ *                  normalised R as in tt_verify
+ * workspace: tt_verify_workspace_size(n_streams, v) bytes, no initialisation;
+ * calls that overlap in time must not share it.  Same launch shapes as
+ * tt_verify; a rejected stream reads its target row and its draft row once each.
+ */
+int tt_verify_dense(int32_t n_streams, int32_t v,
+                    const int32_t *draft_ids, const int32_t *off,
+                    const float *draft_probs, int64_t draft_ld,
+                    const float *target_probs, int64_t target_ld,
+                    const float *u_accept, const float *u_sample, int32_t max_m,
+                    int32_t *n_accepted, int32_t *out_token, float *residual,
+                    void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Workspace bytes tt_step needs: the larger of tt_align_workspace_size and
  * tt_verify_workspace_size for the same arguments (the two stages run one after
  * the other and share it).

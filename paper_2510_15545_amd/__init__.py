@@ -9,13 +9,15 @@ raised.
     align     tt_align     Dynamic Token Warping + backtrack + mapping (Sec. 4.1, Alg. 1, App. A.2)
     transfer  tt_transfer  draft probability of the aligned draft token (Alg. 2, App. A.2)
     verify    tt_verify    acceptance, residual / bonus sampling (Sec. 3, 4.2.2-4.2.3, App. D Alg. 4)
+    verify_dense  tt_verify_dense  the same with dense proposals over one vocabulary (App. D Alg. 4)
 """
 from __future__ import annotations
 
 import ctypes
 import os
 
-__all__ = ["Vocab", "align", "align_workspace", "transfer", "verify", "verify_workspace", "lib", "LIB_PATH",
+__all__ = ["Vocab", "align", "align_workspace", "transfer", "verify", "verify_dense", "verify_workspace", "lib",
+           "LIB_PATH",
            "TTError", "path_capacity"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtt.so")
@@ -61,6 +63,8 @@ def lib():
         L.tt_verify_workspace_size.restype = ctypes.c_int
         L.tt_verify.argtypes = [i32, i32, P, P, P, P, i64, P, P, i32, P, P, P, P, sz, P]
         L.tt_verify.restype = ctypes.c_int
+        L.tt_verify_dense.argtypes = [i32, i32, P, P, P, i64, P, i64, P, P, i32, P, P, P, P, sz, P]
+        L.tt_verify_dense.restype = ctypes.c_int
         L.tt_step_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz)]
         L.tt_step_workspace_size.restype = ctypes.c_int
         L.tt_step.argtypes = [VP, VP, i32, i32, i32, P, P, P, P, i32, i32, i32, P, i64, P, i64, P, P,
@@ -226,6 +230,35 @@ def verify(v_t: int, target_ids, target_off, q, target_probs, u_accept, u_sample
                          _ptr(tok, i32, "out_token"), _ptr(res, f32, "residual", allow_none=True),
                          ctypes.c_void_p(workspace.data_ptr()), int(workspace.numel()), _stream_handle(stream))
     _check(st, "tt_verify")
+    return out
+
+
+def verify_dense(v: int, draft_ids, off, draft_probs, target_probs, u_accept, u_sample, max_m: int,
+                 workspace=None, residual: bool = False, out=None, stream=None):
+    """tt_verify_dense.  Returns (n_accepted, out_token, residual or None)."""
+    torch = _torch()
+    i32, f32 = torch.int32, torch.float32
+    n = int(off.numel()) - 1
+    dev = off.device
+    for name, t in (("draft_probs", draft_probs), ("target_probs", target_probs)):
+        if t.dim() != 2 or t.stride(1) != 1 or t.dtype != f32 or not t.is_cuda:
+            raise ValueError(f"{name} must be a 2-D row-major float32 device tensor")
+    if workspace is None:
+        workspace = verify_workspace(n, v, dev)
+    if out is None:
+        out = (torch.empty(n, dtype=i32, device=dev), torch.empty(n, dtype=i32, device=dev),
+               torch.zeros((n, target_probs.stride(0)), dtype=f32, device=dev) if residual else None)
+    nacc, tok, res = out
+    ids = draft_ids if draft_ids.numel() else torch.zeros(1, dtype=i32, device=dev)
+    ua = u_accept if u_accept.numel() else torch.zeros(1, dtype=f32, device=dev)
+    st = lib().tt_verify_dense(n, int(v), _ptr(ids, i32, "draft_ids"), _ptr(off, i32, "off"),
+                               ctypes.c_void_p(draft_probs.data_ptr()), int(draft_probs.stride(0)),
+                               ctypes.c_void_p(target_probs.data_ptr()), int(target_probs.stride(0)),
+                               _ptr(ua, f32, "u_accept"), _ptr(u_sample, f32, "u_sample"), int(max_m),
+                               _ptr(nacc, i32, "n_accepted"), _ptr(tok, i32, "out_token"),
+                               _ptr(res, f32, "residual", allow_none=True),
+                               ctypes.c_void_p(workspace.data_ptr()), int(workspace.numel()), _stream_handle(stream))
+    _check(st, "tt_verify_dense")
     return out
 
 

@@ -155,7 +155,7 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     if (wave != 0) return;
     uint64_t Z;
     const int token =
-        vcore::wave_sample(row, vt, p.nc, p.vec4 != 0, [&](int c) { return sh_part[c]; }, us, rtok, rq, &Z);
+        vcore::wave_sample(row, nullptr, vt, p.nc, p.vec4 != 0, [&](int c) { return sh_part[c]; }, us, rtok, rq, &Z);
     if (tid == 0) {
         ve.n_accepted[b] = r;
         ve.out_token[b] = token;

@@ -128,6 +128,36 @@ int tt_verify(int32_t n_streams, int32_t v_t, const int32_t *target_ids, const i
     return tt::launch_verify(a, static_cast<hipStream_t>(stream));
 }
 
+int tt_verify_dense(int32_t n_streams, int32_t v, const int32_t *draft_ids, const int32_t *off,
+                    const float *draft_probs, int64_t draft_ld, const float *target_probs, int64_t target_ld,
+                    const float *u_accept, const float *u_sample, int32_t max_m, int32_t *n_accepted,
+                    int32_t *out_token, float *residual, void *workspace, size_t workspace_bytes, void *stream) {
+    if (n_streams < 0 || v < 1 || draft_ld < v || target_ld < v || max_m < 0 || max_m > kMaxVerifyLen)
+        return TT_EINVAL;
+    if (n_streams == 0) return TT_OK;
+    if (!draft_ids || !off || !draft_probs || !target_probs || !u_accept || !u_sample || !n_accepted || !out_token)
+        return TT_EINVAL;
+    tt::VerifyArgs a;
+    a.n_streams = n_streams;
+    a.v_t = v;
+    a.target_ids = draft_ids;  // the proposals verified against the target rows
+    a.target_off = off;
+    a.q = nullptr;
+    a.target_probs = target_probs;
+    a.target_ld = target_ld;
+    a.u_accept = u_accept;
+    a.u_sample = u_sample;
+    a.max_m = max_m;
+    a.n_accepted = n_accepted;
+    a.out_token = out_token;
+    a.residual = residual;
+    a.workspace = workspace;
+    a.workspace_bytes = workspace_bytes;
+    a.q_rows = draft_probs;
+    a.q_ld = draft_ld;
+    return tt::launch_verify(a, static_cast<hipStream_t>(stream));
+}
+
 int tt_step_workspace_size(int32_t n_streams, int32_t v_t, int32_t max_k, int32_t max_m, int32_t w,
                            int32_t max_token_bytes, size_t *bytes) {
     if (bytes == nullptr || v_t < 1 || max_m > kMaxVerifyLen) return TT_EINVAL;

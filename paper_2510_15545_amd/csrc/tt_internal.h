@@ -52,6 +52,10 @@ struct VerifyArgs {
     float *residual;
     void *workspace;
     size_t workspace_bytes;
+    // Dense proposals (tt_verify_dense): row target_off[b] + j of q_rows is the draft
+    // distribution of position j over the same vocabulary; null for the one-hot proposal q.
+    const float *q_rows = nullptr;
+    int64_t q_ld = 0;
 };
 
 // Workspace layout for tt_verify: Q62 mass Z and selected row r per stream, Q62 sums of
@@ -61,7 +65,7 @@ struct VerifyLayout {
     int32_t n_chunks;
 };
 VerifyLayout verify_layout(int32_t n_streams, int32_t v_t);
-int launch_verify(const VerifyArgs &a, hipStream_t stream);
+int launch_verify(const VerifyArgs &a, hipStream_t stream);  // one-hot or dense by a.q_rows
 // True when tt_verify runs one workgroup per stream (enough streams to fill the chip and
 // the row's chunk sums fit in LDS); the fused step kernel uses the same shape.
 bool verify_row_path(int32_t n_streams, int32_t v_t);

@@ -57,7 +57,9 @@ struct VParams {
 };
 
 // Acceptance scan by one wave: gamma (first rejection, else M); false if the stream is
-// invalid (M outside [0, max_m] or an id outside [0, v_t)).
+// invalid (M outside [0, max_m] or an id outside [0, v_t)).  The proposal's mass at t_j
+// is q_j (one-hot) or q_rows[t0 + j][t_j] (DENSE).
+template <bool DENSE>
 __device__ __forceinline__ bool accept_scan(const VerifyArgs &a, int b, int t0, int M, int lane, int &gamma) {
     gamma = M;
     if (M < 0 || M > a.max_m) return false;
@@ -70,7 +72,7 @@ __device__ __forceinline__ bool accept_scan(const VerifyArgs &a, int b, int t0, 
                 bad = true;
             } else {
                 const float pt = a.target_probs[(int64_t)(t0 + b + j) * a.target_ld + tok];
-                const float qj = a.q[t0 + j];
+                const float qj = DENSE ? a.q_rows[(int64_t)(t0 + j) * a.q_ld + tok] : a.q[t0 + j];
                 const float ratio = pt / qj;
                 rej = !((qj <= 0.0f) || (a.u_accept[t0 + j] < ratio));
             }
@@ -82,7 +84,37 @@ __device__ __forceinline__ bool accept_scan(const VerifyArgs &a, int b, int t0, 
     return true;
 }
 
+// The proposal taken off row r: the dense draft row (DENSE, r < M), else the one-hot
+// mass rq at token rtok (rtok = -1 after full acceptance: the bonus row is sampled as is).
+struct Proposal {
+    const float *qrow;
+    int rtok;
+    float rq;
+};
+
+template <bool DENSE>
+__device__ __forceinline__ Proposal proposal(const VerifyArgs &a, int t0, int M, int r) {
+    Proposal pr{nullptr, -1, 0.0f};
+    if (r < M) {
+        if (DENSE) pr.qrow = a.q_rows + (int64_t)(t0 + r) * a.q_ld;
+        else {
+            pr.rtok = a.target_ids[t0 + r];
+            pr.rq = a.q[t0 + r];
+        }
+    }
+    return pr;
+}
+
+// Q62 chunk sums of row's chunks [c0, c1) by the calling workgroup's waves.
+template <class Store>
+__device__ __forceinline__ void stream_row(const float *row, const Proposal &pr, int vt, bool vec, int c0, int c1,
+                                           int stride, Store store) {
+    if (pr.qrow != nullptr) stream_chunks_dense(row, pr.qrow, vt, vec, c0, c1, stride, store);
+    else stream_chunks(row, vt, vec, c0, c1, stride, pr.rtok, pr.rq, store);
+}
+
 // ------------------------------------------------------------------ row path
+template <bool DENSE>
 __global__ void __launch_bounds__(kRowThreads) verify_row(VParams p) {
     const VerifyArgs &a = p.a;
     const int b = blockIdx.x;
@@ -96,7 +128,7 @@ __global__ void __launch_bounds__(kRowThreads) verify_row(VParams p) {
     const float us = a.u_sample[b];
     if (wave == 0) {
         int gamma;
-        const bool ok = accept_scan(a, b, t0, M, lane, gamma);
+        const bool ok = accept_scan<DENSE>(a, b, t0, M, lane, gamma);
         if (lane == 0) {
             sh_gamma = gamma;
             sh_ok = ok ? 1 : 0;
@@ -114,14 +146,13 @@ __global__ void __launch_bounds__(kRowThreads) verify_row(VParams p) {
     const int r = sh_gamma;
     const int vt = a.v_t;
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
-    const int rtok = r < M ? a.target_ids[t0 + r] : -1;
-    const float rq = r < M ? a.q[t0 + r] : 0.0f;
-    stream_chunks(row, vt, p.vec4 != 0, 0, p.nc, kRowThreads / kWave, rtok, rq,
-                  [&](int c, uint64_t s) { sh_part[c] = s; });
+    const Proposal pr = proposal<DENSE>(a, t0, M, r);
+    stream_row(row, pr, vt, p.vec4 != 0, 0, p.nc, kRowThreads / kWave, [&](int c, uint64_t s) { sh_part[c] = s; });
     __syncthreads();
     if (wave != 0) return;
     uint64_t Z;
-    const int token = wave_sample(row, vt, p.nc, p.vec4 != 0, [&](int c) { return sh_part[c]; }, us, rtok, rq, &Z);
+    const int token = wave_sample(row, pr.qrow, vt, p.nc, p.vec4 != 0, [&](int c) { return sh_part[c]; }, us,
+                                  pr.rtok, pr.rq, &Z);
     if (tid == 0) {
         a.n_accepted[b] = r;
         a.out_token[b] = token;
@@ -131,6 +162,7 @@ __global__ void __launch_bounds__(kRowThreads) verify_row(VParams p) {
 }
 
 // ------------------------------------------------------------------ split path
+template <bool DENSE>
 __global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
     const VerifyArgs &a = p.a;
     const int G = gridDim.x;
@@ -146,7 +178,7 @@ __global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
     const int M = a.target_off[b + 1] - t0;
     if (wave == 0) {  // every workgroup of the stream recomputes gamma
         int gamma;
-        const bool ok = accept_scan(a, b, t0, M, lane, gamma);
+        const bool ok = accept_scan<DENSE>(a, b, t0, M, lane, gamma);
         if (lane == 0) {
             sh_gamma = gamma;
             sh_ok = ok ? 1 : 0;
@@ -164,16 +196,15 @@ __global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
     const int r = sh_gamma;
     if (s == 0 && tid == 0) p.rsel[b] = r;
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
-    const int rtok = r < M ? a.target_ids[t0 + r] : -1;
-    const float rq = r < M ? a.q[t0 + r] : 0.0f;
+    const Proposal pr = proposal<DENSE>(a, t0, M, r);
     const int c0 = s * p.cpw;
     const int c1 = (c0 + p.cpw) < p.nc ? (c0 + p.cpw) : p.nc;
     uint64_t *out = p.partials + (int64_t)b * p.nc;
-    stream_chunks(row, a.v_t, p.vec4 != 0, c0, c1, kSplitThreads / kWave, rtok, rq,
-                  [&](int c, uint64_t sum) { out[c] = sum; });
+    stream_row(row, pr, a.v_t, p.vec4 != 0, c0, c1, kSplitThreads / kWave, [&](int c, uint64_t sum) { out[c] = sum; });
 }
 
 // One wave per stream: exact threshold, crossing chunk, crossing index.
+template <bool DENSE>
 __global__ void __launch_bounds__(kWave) verify_sample(VParams p) {
     const VerifyArgs &a = p.a;
     const int b = blockIdx.x;
@@ -185,10 +216,10 @@ __global__ void __launch_bounds__(kWave) verify_sample(VParams p) {
     const float us = a.u_sample[b];
     if (r < 0) return;  // sentinel stream, outputs already written (uniform per workgroup)
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
-    const int rtok = r < M ? a.target_ids[t0 + r] : -1;
-    const float rq = r < M ? a.q[t0 + r] : 0.0f;
+    const Proposal pr = proposal<DENSE>(a, t0, M, r);
     uint64_t Z;
-    const int token = wave_sample(row, a.v_t, p.nc, p.vec4 != 0, [&](int c) { return part[c]; }, us, rtok, rq, &Z);
+    const int token =
+        wave_sample(row, pr.qrow, a.v_t, p.nc, p.vec4 != 0, [&](int c) { return part[c]; }, us, pr.rtok, pr.rq, &Z);
     if (tid == 0) {
         a.n_accepted[b] = r;
         a.out_token[b] = token;
@@ -197,6 +228,7 @@ __global__ void __launch_bounds__(kWave) verify_sample(VParams p) {
 }
 
 // Optional normalised residual row: res[x] = R(x) / fp32(Z * 2^-62), one-hot when Z = 0.
+template <bool DENSE>
 __global__ void __launch_bounds__(kSplitThreads) residual_write(VParams p, int rsplit) {
     const VerifyArgs &a = p.a;
     const int b = blockIdx.x / rsplit, sidx = blockIdx.x % rsplit;
@@ -207,8 +239,7 @@ __global__ void __launch_bounds__(kSplitThreads) residual_write(VParams p, int r
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
-    const int rtok = r < M ? a.target_ids[t0 + r] : -1;
-    const float rq = r < M ? a.q[t0 + r] : 0.0f;
+    const Proposal pr = proposal<DENSE>(a, t0, M, r);
     float *res = a.residual + (int64_t)b * a.target_ld;
     const int vt = a.v_t;
     const int per = (vt + rsplit - 1) / rsplit;
@@ -220,7 +251,7 @@ __global__ void __launch_bounds__(kSplitThreads) residual_write(VParams p, int r
     }
     const float zf = (float)Z * 0x1p-62f;
     for (int x = x0 + (int)threadIdx.x; x < x1; x += kSplitThreads)
-        res[x] = clamp01(row[x] - (x == rtok ? rq : 0.0f)) / zf;
+        res[x] = clamp01(row[x] - (pr.qrow != nullptr ? pr.qrow[x] : (x == pr.rtok ? pr.rq : 0.0f))) / zf;
 }
 
 inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
@@ -259,6 +290,7 @@ VParams make_params(const VerifyArgs &a) {
     p.partials = reinterpret_cast<uint64_t *>(ws + L.partials);
     p.nc = L.n_chunks;
     p.vec4 = ((reinterpret_cast<uintptr_t>(a.target_probs) & 15u) == 0 && (a.target_ld % 4) == 0) ? 1 : 0;
+    if (a.q_rows != nullptr && ((reinterpret_cast<uintptr_t>(a.q_rows) & 15u) != 0 || (a.q_ld % 4) != 0)) p.vec4 = 0;
     p.splits = 1;
     p.cpw = p.nc;
     p.work_items = a.n_streams;
@@ -268,22 +300,20 @@ VParams make_params(const VerifyArgs &a) {
 int launch_residual(const VParams &p, hipStream_t stream) {
     int rsplit = (p.a.v_t + 8191) / 8192;
     if (rsplit < 1) rsplit = 1;
-    hipLaunchKernelGGL(residual_write, dim3(p.a.n_streams * rsplit), dim3(kSplitThreads), 0, stream, p, rsplit);
+    if (p.a.q_rows != nullptr)
+        hipLaunchKernelGGL(residual_write<true>, dim3(p.a.n_streams * rsplit), dim3(kSplitThreads), 0, stream, p,
+                           rsplit);
+    else
+        hipLaunchKernelGGL(residual_write<false>, dim3(p.a.n_streams * rsplit), dim3(kSplitThreads), 0, stream, p,
+                           rsplit);
     return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
 }
 
-}  // namespace
-
-int launch_verify_residual(const VerifyArgs &a, hipStream_t stream) {
-    if (a.workspace == nullptr || a.workspace_bytes < verify_layout(a.n_streams, a.v_t).total) return TT_EWORKSPACE;
-    return launch_residual(make_params(a), stream);
-}
-
-int launch_verify(const VerifyArgs &a, hipStream_t stream) {
-    if (a.workspace == nullptr || a.workspace_bytes < verify_layout(a.n_streams, a.v_t).total) return TT_EWORKSPACE;
-    VParams p = make_params(a);
+template <bool DENSE>
+int launch_verify_kernels(VParams &p, hipStream_t stream) {
+    const VerifyArgs &a = p.a;
     if (verify_row_path(a.n_streams, a.v_t)) {
-        hipLaunchKernelGGL(verify_row, dim3(a.n_streams), dim3(kRowThreads), 8 * (size_t)p.nc, stream, p);
+        hipLaunchKernelGGL(verify_row<DENSE>, dim3(a.n_streams), dim3(kRowThreads), 8 * (size_t)p.nc, stream, p);
         if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
     } else {
         // splits per stream: aim for TT_VERIFY_TARGET_WG workgroups, at least one chunk per wave
@@ -296,11 +326,27 @@ int launch_verify(const VerifyArgs &a, hipStream_t stream) {
         p.splits = (p.nc + p.cpw - 1) / p.cpw;
         p.work_items = a.n_streams * p.splits;
         const int grid = ((p.work_items + kXcds - 1) / kXcds) * kXcds;
-        hipLaunchKernelGGL(verify_stream, dim3(grid), dim3(kSplitThreads), 0, stream, p);
+        hipLaunchKernelGGL(verify_stream<DENSE>, dim3(grid), dim3(kSplitThreads), 0, stream, p);
         if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
-        hipLaunchKernelGGL(verify_sample, dim3(a.n_streams), dim3(kWave), 0, stream, p);
+        hipLaunchKernelGGL(verify_sample<DENSE>, dim3(a.n_streams), dim3(kWave), 0, stream, p);
         if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
     }
+    return TT_OK;
+}
+
+}  // namespace
+
+int launch_verify_residual(const VerifyArgs &a, hipStream_t stream) {
+    if (a.workspace == nullptr || a.workspace_bytes < verify_layout(a.n_streams, a.v_t).total) return TT_EWORKSPACE;
+    return launch_residual(make_params(a), stream);
+}
+
+
+int launch_verify(const VerifyArgs &a, hipStream_t stream) {
+    if (a.workspace == nullptr || a.workspace_bytes < verify_layout(a.n_streams, a.v_t).total) return TT_EWORKSPACE;
+    VParams p = make_params(a);
+    const int st = a.q_rows != nullptr ? launch_verify_kernels<true>(p, stream) : launch_verify_kernels<false>(p, stream);
+    if (st != TT_OK) return st;
     return a.residual != nullptr ? launch_residual(p, stream) : TT_OK;
 }
 

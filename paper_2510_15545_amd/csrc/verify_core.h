@@ -183,13 +183,71 @@ __device__ __forceinline__ void stream_chunks(const float *row, int vt, bool vec
 #endif
 }
 
+// 16 consecutive floats row[x0 .. x0 + 16) (zero past vt).
+__device__ __forceinline__ void read16(const float *row, int x0, int vt, bool vec, float (&pv)[16]) {
+    if (vec && x0 + 16 <= vt) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 t = *reinterpret_cast<const float4 *>(row + x0 + 4 * q);
+            pv[4 * q] = t.x;
+            pv[4 * q + 1] = t.y;
+            pv[4 * q + 2] = t.z;
+            pv[4 * q + 3] = t.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) pv[k] = x0 + k < vt ? row[x0 + k] : 0.0f;
+    }
+}
+
+// Dense proposal (standard speculative sampling over one vocabulary): the residual is
+// max(0, p - q) elementwise over two rows.  Q62 sum of one loaded chunk of each row.
+template <class Store>
+__device__ __forceinline__ void sum_chunk_dense(const float4 (&vp)[4], const float4 (&vq)[4], int c, Store &store) {
+    uint64_t acc = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+        acc += q62(clamp01(vp[u].x - vq[u].x)) + q62(clamp01(vp[u].y - vq[u].y)) +
+               q62(clamp01(vp[u].z - vq[u].z)) + q62(clamp01(vp[u].w - vq[u].w));
+    acc = wave_inclusive_scan(acc);
+    if (threadIdx.x % kWave == kWave - 1) store(c, acc);
+}
+
+// As stream_chunks for the dense residual: chunks c0 + wave, c0 + wave + stride, ... < c1
+// of both rows, one chunk of each ahead in flight.
+template <class Store>
+__device__ __forceinline__ void stream_chunks_dense(const float *prow, const float *qrow, int vt, bool vec, int c0,
+                                                    int c1, int stride, Store store) {
+    const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    int c = c0 + wave;
+    float4 vp[4], vq[4], np_[4], nq[4];
+    if (c < c1) {
+        load_chunk(prow, c * kChunk, lane, vt, vec, vp);
+        load_chunk(qrow, c * kChunk, lane, vt, vec, vq);
+    }
+    for (; c < c1; c += stride) {
+        const int cn = c + stride;
+        if (cn < c1) {
+            load_chunk(prow, cn * kChunk, lane, vt, vec, np_);
+            load_chunk(qrow, cn * kChunk, lane, vt, vec, nq);
+        }
+        sum_chunk_dense(vp, vq, c, store);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            vp[u] = np_[u];
+            vq[u] = nq[u];
+        }
+    }
+}
+
 // Inverse-CDF sample of the row from its nc chunk sums part(c), by one wave: every lane
-// returns the token and *Zout the Q62 mass.  Chunk sums are scanned lane-blocked (lane l
+// returns the token and *Zout the Q62 mass.  The residual is max(0, row - qrow) when qrow
+// is given (dense proposal), else row less rq at the rejected proposal rtok (one-hot).  Chunk sums are scanned lane-blocked (lane l
 // holds chunks [l * per, (l + 1) * per)), the crossing chunk is re-read as 16 consecutive
 // floats per lane and scanned the same way.  Searches inside a lane are branch-free counts.
 template <class Part>
-__device__ inline int wave_sample(const float *row, int vt, int nc, bool vec, Part part, float u, int rtok,
-                                  float rq, uint64_t *Zout) {
+__device__ inline int wave_sample(const float *row, const float *qrow, int vt, int nc, bool vec, Part part, float u,
+                                  int rtok, float rq, uint64_t *Zout) {
     constexpr int kPerMax = 4;  // chunk sums kept in registers per lane (rows up to 256K floats)
     const int lane = threadIdx.x % kWave;
     const int per = (nc + kWave - 1) / kWave;
@@ -241,26 +299,19 @@ __device__ inline int wave_sample(const float *row, int vt, int nc, bool vec, Pa
     base = lane_value(base, owner);
     // the crossing chunk: lane holds elements cs*1024 + lane*16 + [0, 16)
     const int x0 = cs * kChunk + lane * 16;
-    float pv[16];
-    if (vec && x0 + 16 <= vt) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float4 t = *reinterpret_cast<const float4 *>(row + x0 + 4 * q);
-            pv[4 * q] = t.x;
-            pv[4 * q + 1] = t.y;
-            pv[4 * q + 2] = t.z;
-            pv[4 * q + 3] = t.w;
-        }
+    float pv[16], dv[16];
+    read16(row, x0, vt, vec, pv);
+    if (qrow != nullptr) {
+        read16(qrow, x0, vt, vec, dv);
     } else {
 #pragma unroll
-        for (int k = 0; k < 16; ++k) pv[k] = x0 + k < vt ? row[x0 + k] : 0.0f;
+        for (int k = 0; k < 16; ++k) dv[k] = x0 + k == rtok ? rq : 0.0f;
     }
     uint64_t qv[16];
     uint64_t sum = 0;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
-        const int x = x0 + k;
-        qv[k] = x < vt ? q62(clamp01(pv[k] - (x == rtok ? rq : 0.0f))) : 0ull;
+        qv[k] = x0 + k < vt ? q62(clamp01(pv[k] - dv[k])) : 0ull;
         sum += qv[k];
     }
     const uint64_t lincl = wave_inclusive_scan(sum) + base;

@@ -416,3 +416,75 @@ def _long_pair_prob_stage(spec, vd, vt, pairs, seed_shift, probs, w) -> Workload
         _make_probs(sub, seed_shift)
     return sub
 
+
+
+# --------------------------------------------------------------------------- dense proposals
+@dataclasses.dataclass
+class DenseWorkload:
+    """Standard speculative decoding over one vocabulary (homogeneous draft and target).
+
+    Stream b drafted M_b tokens draft_ids[off[b]:off[b+1]], token j drawn from the dense
+    draft row draft_probs[off[b] + j]; the target scored M_b + 1 prefixes, rows
+    target_probs[off[b] + b + j], j = 0..M_b."""
+    name: str
+    v: int
+    draft_ids: np.ndarray
+    off: np.ndarray
+    draft_probs: np.ndarray
+    target_probs: np.ndarray
+    u_accept: np.ndarray
+    u_sample: np.ndarray
+
+    @property
+    def n(self) -> int:
+        return len(self.off) - 1
+
+    @property
+    def max_m(self) -> int:
+        return int(np.max(np.diff(self.off))) if self.n else 0
+
+
+DENSE_INDEX = 6  # seed offset of the dense-proposal workload
+
+
+def make_dense(n_streams: int = 256, m: int = 8, v: int = 151_936, m_range: tuple | None = None,
+               noise: float = 0.5, temperature: float = 0.7, seed_shift: int = 0) -> DenseWorkload:
+    """Dense-proposal workload shaped like workload 3 on one vocabulary: target logits
+    bf16(3 N(0,1)), draft logits bf16(target + noise N(0,1)) (a draft that mostly agrees with
+    the target), fp32 softmax of logit / temperature.  Each drafted token is drawn from its
+    draft row with a seeded uniform (the drafter's own sampling, an input here).  M_b = m, or
+    uniform in m_range = (lo, hi) inclusive."""
+    c = DENSE_INDEX + seed_shift
+    rng_m = np.random.default_rng([SEED_SEQ + c, 0])
+    ms = (np.full(n_streams, m, np.int64) if m_range is None
+          else rng_m.integers(m_range[0], m_range[1] + 1, n_streams))
+    off = np.zeros(n_streams + 1, np.int32)
+    off[1:] = np.cumsum(ms)
+    total = int(off[-1])
+    inv_t = np.float32(1.0 / temperature)
+    draft_probs = np.empty((total, v), np.float32)
+    target_probs = np.empty((total + n_streams, v), np.float32)
+    draft_ids = np.empty(total, np.int32)
+
+    def logits(b, j):
+        x = _normal_row(v, 3.0, [SEED_LOGITS + c, 1, b, j])
+        return x
+
+    def target_row(r, b, j):
+        return _softmax_f32(_bf16_round(logits(b, j)) * inv_t)
+
+    def draft_row(r, b, j):
+        x = logits(b, j) + _normal_row(v, noise, [SEED_LOGITS + c, 0, b, j])
+        q = _softmax_f32(_bf16_round(x) * inv_t)
+        u = np.random.default_rng([SEED_SEQ + c, 1, b, j]).random()
+        cdf = np.cumsum(q, dtype=np.float64)
+        draft_ids[r] = min(int(np.searchsorted(cdf, u * cdf[-1], side="right")), v - 1)
+        return q
+
+    _fill_rows(target_probs, [(int(off[b]) + b + j, b, j) for b in range(n_streams) for j in range(ms[b] + 1)],
+               target_row)
+    _fill_rows(draft_probs, [(int(off[b]) + j, b, j) for b in range(n_streams) for j in range(ms[b])], draft_row)
+    u_accept = _uniform24(np.random.default_rng([SEED_UNIF + c, 0]), total)
+    u_sample = _uniform24(np.random.default_rng([SEED_UNIF + c, 1]), n_streams)
+    return DenseWorkload(f"{n_streams} streams M={m if m_range is None else m_range} V={v} dense proposals",
+                         v, draft_ids, off, draft_probs, target_probs, u_accept, u_sample)

@@ -85,6 +85,18 @@ def test_invalid_arguments_return_before_launch():
     assert L.tt_verify(1, 10, None, dummy, dummy, dummy, 10, dummy, dummy, 4, dummy, dummy, None,
                        dummy, 1 << 20, None) == tt.TT_EINVAL
 
+    def dense(n=1, v=10, ld_d=10, ld_t=10, max_m=4, ids=dummy, ws=1 << 20):
+        return L.tt_verify_dense(n, v, ids, dummy, dummy, ld_d, dummy, ld_t, dummy, dummy, max_m, dummy, dummy,
+                                 None, dummy, ws, None)
+    assert dense(ld_d=9) == tt.TT_EINVAL
+    assert dense(ld_t=9) == tt.TT_EINVAL
+    assert dense(v=0) == tt.TT_EINVAL
+    assert dense(max_m=-1) == tt.TT_EINVAL
+    assert dense(n=-1) == tt.TT_EINVAL
+    assert dense(ids=None) == tt.TT_EINVAL
+    assert dense(ws=0) == tt.TT_EWORKSPACE
+    assert dense(n=0, ids=None) == tt.TT_OK
+
     def step(vd=ctypes.byref(v), n=1, v_d=10, v_t=10, ld_d=10, ld_t=10, max_m=4, ids=dummy, ws=1 << 30):
         return L.tt_step(vd, ctypes.byref(v), n, v_d, v_t, ids, dummy, dummy, dummy, 4, max_m, 8,
                          dummy, ld_d, dummy, ld_t, dummy, dummy, dummy, dummy, dummy, dummy, dummy,
