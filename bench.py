@@ -111,6 +111,9 @@ def parse():
                     help="also run one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--only", choices=["step", "verify", "align", "transfer"], default=None,
                     help="after the timed steps, loop only this call (for profiler passes)")
+    ap.add_argument("--dense", action="store_true",
+                    help="standard speculative sampling with dense proposals over one vocabulary "
+                         "(tt_verify_dense) on 256 streams x M=8 at V=151,936 instead of the TokenTiming path")
     ap.add_argument("--traffic", type=str, default=None,
                     help="counter summary with the measured HBM bytes per launch of the dominant kernel "
                          "(default: profiles/<kernel>_counters.txt)")
@@ -124,6 +127,9 @@ def main():
         print("bench.py measures one GPU: the verification path runs per stream on a single device; "
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.dense:
+        return main_dense(args)
 
     import torch
 
@@ -379,6 +385,118 @@ def main():
         nacc_step = step_outputs[0] if step_outputs is not None else nacc
         tok_step = step_outputs[1] if step_outputs is not None else tok
         result["cpu_baseline"] = cpu_baseline(args, S, A, nacc_step, tok_step, s_out, a_out)
+    print(json.dumps(result), flush=True)
+
+
+def main_dense(args):
+    """Dense-proposal verification (App. D Alg. 4 over one vocabulary): one step is one
+    tt_verify_dense call over the batch; draft and target rows are replicated like the
+    TokenTiming path's target rows."""
+    import torch
+
+    import paper_2510_15545_amd as tt
+    from paper_2510_15545_amd import synth
+
+    tt.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    n_streams = args.streams or 256
+    t_gen = time.time()
+    D = synth.make_dense(n_streams, 8, 151_936)
+    t_gen = time.time() - t_gen
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    R = max(1, args.replicas)
+    ids, off, ua, us = t(D.draft_ids), t(D.off), t(D.u_accept), t(D.u_sample)
+    qrows = [t(D.draft_probs)]
+    prows = [t(D.target_probs)]
+    for _ in range(R - 1):
+        qrows.append(qrows[0].clone())
+        prows.append(prows[0].clone())
+    n = D.n
+    nacc = torch.empty(n, dtype=torch.int32, device=dev)
+    tok = torch.empty(n, dtype=torch.int32, device=dev)
+    ws = tt.verify_workspace(n, D.v, dev)
+
+    def step(r):
+        tt.verify_dense(D.v, ids, off, qrows[r], prows[r], ua, us, D.max_m, workspace=ws, out=(nacc, tok, None))
+
+    for i in range(args.warmup):
+        step(i % R)
+    torch.cuda.synchronize()
+    gs = 1 if args.eager else max(1, min(args.graph_steps, args.steps))
+    reps = max(1, args.steps // gs)
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if args.eager:
+        s0.record()
+        for i in range(reps):
+            step(i % R)
+        s1.record()
+    else:
+        g = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            with torch.cuda.graph(g, stream=cap):
+                for i in range(gs):
+                    step(i % R)
+        torch.cuda.current_stream().wait_stream(cap)
+        g.replay()
+        torch.cuda.synchronize()
+        s0.record()
+        for _ in range(reps):
+            g.replay()
+        s1.record()
+    torch.cuda.synchronize()
+    ms = s0.elapsed_time(s1) / (reps * gs)
+    step(0)
+    torch.cuda.synchronize()
+    if args.copy_calib_mb:
+        src = torch.empty(args.copy_calib_mb * (1 << 20) // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+    acc = nacc.cpu().numpy()
+    m = np.diff(D.off)
+    # algorithmic bytes: the target row of every stream, the draft row of every rejected
+    # stream, x_j, p_j(x_j), q_j(x_j), u_j per drafted position, u_sample, n_accepted, out_token
+    rejected = int((acc < m).sum())
+    kbytes = int(n * 4 * D.v + rejected * 4 * D.v + 16 * int(m.sum()) + 12 * n)
+    gbs = kbytes / (ms * 1e-3) / 1e9
+    wl_name = D.name
+    traffic, note = read_traffic(args.traffic or os.path.join(ROOT, "profiles", "verify_row_dense_counters.txt"),
+                                 wl_name, "verify_row")
+    result = {
+        "metric": "verified draft tokens/s, dense proposals (App. D Alg. 4) at V=151,936; verify HBM GB/s vs peak",
+        "value": round(int(m.sum()) / (ms * 1e-3), 1), "unit": "draft tokens/s",
+        "n_gpus": 1, "steps": reps * gs, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32+i64", "data": "synthetic",
+        "config": {"workload": wl_name, "streams": n, "draft_tokens_per_step": int(m.sum()), "v": D.v,
+                   "replicas": R, "path": "tt_verify_dense",
+                   "launch": "eager" if args.eager else "hip-graph of %d steps" % gs},
+        "accept": {"mean_gamma": round(float(acc.mean()), 3), "rejected_streams": rejected},
+        "roofline": {"kernel": "verify_row<dense>", "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic, "traffic_note": note,
+                     "algorithmic_bytes_per_launch": kbytes, "launch_us": round(ms * 1e3, 2)},
+        "gen_seconds": round(t_gen, 1),
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+
+        threads = len(os.sched_getaffinity(0))
+        k, t0 = 0, time.time()
+        while k == 0 or (time.time() - t0 < args.cpu_seconds and k < 50):
+            o_n, o_t, _, _ = oracle.sd_verify(D.v, D.draft_ids, D.off, D.draft_probs, D.target_probs, D.u_accept,
+                                              D.u_sample, n_threads=threads)
+            k += 1
+        dt = (time.time() - t0) / k
+        result["cpu_baseline"] = {
+            "value": round(int(m.sum()) / dt, 1), "unit": "draft tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{k} whole steps of the benchmark batch ({n} streams), {dt * 1e3:.1f} ms each",
+            "matches_gpu": bool(np.array_equal(o_n, acc) and np.array_equal(o_t, tok.cpu().numpy()))}
     print(json.dumps(result), flush=True)
 
 
