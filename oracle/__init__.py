@@ -60,6 +60,8 @@ def lib():
         L.orc_verify_dense.restype = i32
         L.orc_sd_verify.argtypes = [i32, i32, P, P, P, i64, P, i64, P, P, i32, P, P, P, P, ctypes.c_int]
         L.orc_sd_verify.restype = None
+        L.orc_delta_histogram.argtypes = [i32, P, P, P, P, i32, P]
+        L.orc_delta_histogram.restype = None
         L.orc_threshold.argtypes = [f32, u64]
         L.orc_threshold.restype = u64
         _lib = L
@@ -185,6 +187,17 @@ def sd_verify(v, draft_ids, off, draft_probs, target_probs, u_accept, u_sample, 
                         target_probs.shape[1], _p(ua), _p(u_sample), int(max_m), _p(nacc), _p(tok),
                         _p(res), _p(z), n_threads or threads_default())
     return nacc, tok, res, z
+
+
+def delta_histogram(draft_off, target_off, path_len, path, n_bins):
+    """Fig. CDF / App. K: counts of |i - j| over every optimal path cell (last bin: >= n_bins-1)."""
+    draft_off, target_off = _c(draft_off, np.int32), _c(target_off, np.int32)
+    path_len = _c(path_len, np.int32)
+    path = _c(path, np.int32) if np.size(path) else np.zeros(2, np.int32)
+    hist = np.zeros(int(n_bins), np.int64)
+    lib().orc_delta_histogram(len(draft_off) - 1, _p(draft_off), _p(target_off), _p(path_len), _p(path),
+                              int(n_bins), _p(hist))
+    return hist
 
 
 def threshold(u: float, Z: int) -> int:

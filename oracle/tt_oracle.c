@@ -23,6 +23,8 @@
  *                     (residual "modified distribution")
  *   orc_sd_verify     App. D Alg. 4 with dense proposals over one vocabulary (standard
  *                     speculative decoding, the homogeneous-vocabulary case)
+ *   orc_delta_histogram  Sec. 5 Fig. CDF / App. K: position deviation |i - j| of the
+ *                     matched pairs on the optimal paths
  *
  * Readings where the paper is silent or ambiguous (each is listed in the design
  * notes of the repository):
@@ -509,6 +511,25 @@ void orc_sd_verify(int32_t n_streams, int32_t V, const int32_t *draft_ids, const
     orc_sd_ctx c = {V, draft_ids, off, draft_probs, draft_ld, target_probs, target_ld, u_accept, u_sample,
                     max_m, n_accepted, out_token, residual, z_out};
     orc_parallel(n_streams, n_threads, orc_sd_range, &c);
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Sec. 5 "DTW Bridges the Gap" (Fig. CDF) and App. K: the position deviation of a matched
+ * draft / proxy target token pair (i, j) on an optimal warping path is |i - j|.  hist[d]
+ * counts the path cells of all pairs with |i - j| = d for d < n_bins - 1; the last bin
+ * counts every cell with |i - j| >= n_bins - 1.  Pair b's cells are path[2*(draft_off[b] +
+ * target_off[b]) ...] (path_len[b] of them, as orc_align writes them); a pair with
+ * path_len <= 0 (a sentinel pair) contributes nothing. */
+void orc_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
+                         const int32_t *path_len, const int32_t *path, int32_t n_bins, int64_t *hist) {
+    for (int32_t d = 0; d < n_bins; ++d) hist[d] = 0;
+    for (int32_t b = 0; b < n_pairs; ++b) {
+        const int32_t *cells = path + 2 * (int64_t)(draft_off[b] + target_off[b]);
+        for (int32_t c = 0; c < path_len[b]; ++c) {
+            int32_t dev = abs(cells[2 * c] - cells[2 * c + 1]);
+            hist[dev < n_bins - 1 ? dev : n_bins - 1] += 1;
+        }
+    }
 }
 
 /* Test hook: the exact threshold floor(u * Z). */

@@ -164,3 +164,45 @@ def test_step_code_order():
     p_diag = [(1, 1), (2, 2)]
     p_up = [(1, 1), (1, 2), (2, 2)]
     assert step_code(p_diag) < step_code(p_up)
+
+
+# ---- Sec. 5 Fig. CDF / App. K: position deviation of matched tokens
+def test_delta_histogram_fig2(orc):
+    """The Fig. 2 path's matched pairs deviate by 0, 1, 1, 1, 0 positions."""
+    g = load_golden("fig2_alignment.json")
+    d = [s.encode() for s in g["draft_tokens"]]
+    t = [s.encode() for s in g["target_tokens"]]
+    (cost, plen, path, mp), do, to = run(orc, d, t, [(list(range(4)), list(range(4)))], -1)
+    hist = orc.delta_histogram(do, to, plen, path, 2)
+    assert hist.tolist() == g["delta_pos_hist"]
+    # one bin only: everything lands in the overflow bin
+    assert orc.delta_histogram(do, to, plen, path, 1).tolist() == [sum(g["delta_pos_hist"])]
+
+
+def test_delta_histogram_invariants(orc):
+    """Counts sum to the path cells; a band of half-width w without widening leaves every
+    bin above w empty; identical sequences put everything at 0; sentinel pairs add nothing."""
+    from paper_2510_15545_amd import synth
+
+    wl = synth.make(2, probs=False)
+    for w in (2, 8, -1):
+        cost, plen, path, mp = orc.align(wl.vocab_d.data, wl.vocab_d.offsets, wl.vocab_d.max_len,
+                                         wl.vocab_t.data, wl.vocab_t.offsets, wl.vocab_t.max_len,
+                                         wl.draft_ids, wl.draft_off, wl.target_ids, wl.target_off, w)
+        hist = orc.delta_histogram(wl.draft_off, wl.target_off, plen, path, 64)
+        assert hist.sum() == plen.sum()
+        K, M = np.diff(wl.draft_off), np.diff(wl.target_off)
+        if w >= 0:
+            widest = int(np.max(np.maximum(w, np.abs(K - M))))
+            assert hist[widest + 1:].sum() == 0
+        # every pair's own deviations, recounted from its cells
+        for b in range(wl.n):
+            cells = unpack_path(path, plen, wl.draft_off, wl.target_off, b)
+            assert max(abs(i - j) for i, j in cells) <= (max(K[b], M[b]) if w < 0 else max(w, abs(K[b] - M[b])))
+    toks = [bytes([c]) for c in b"abcdefgh"]
+    pairs = [([0, 1, 2, 3], [0, 1, 2, 3]), ([4, 5], [4, 5])]
+    (cost, plen, path, mp), do, to = run(orc, toks, toks, pairs, 8)
+    assert orc.delta_histogram(do, to, plen, path, 4).tolist() == [6, 0, 0, 0]
+    plen2 = plen.copy()
+    plen2[1] = 0  # a sentinel pair
+    assert orc.delta_histogram(do, to, plen2, path, 4).tolist() == [4, 0, 0, 0]
