@@ -297,6 +297,10 @@ def main():
              "verify": kernel_ms(lambda i: do_verify(i % R))}
     if step_ok:
         times["step"] = kernel_ms(lambda i: do_step(i % R))
+    # side output for choosing w (Fig. CDF, App. K): deviation histogram of the aligned batch
+    hist = torch.empty(256, dtype=torch.int32, device=dev)
+    times["delta_histogram"] = kernel_ms(
+        lambda i: tt.delta_histogram(a_do, a_to, a_out[1], a_out[2], 256, out=hist))
     if args.only:
         fn = {"step": lambda i: do_step(i % R), "verify": lambda i: do_verify(i % R),
               "align": lambda i: do_align(), "transfer": lambda i: do_transfer()}[args.only]
@@ -373,7 +377,8 @@ def main():
         "three_call_ms_per_step": round(ms_calls, 5),
         "kernels_ms": {k: round(v, 5) for k, v in times.items()},
         "dtw": {"band_cells": cells, "cells_per_s": round(cells_per_s, 1),
-                "full_cells": int((Ka * Ma).sum())},
+                "full_cells": int((Ka * Ma).sum()),
+                "delta_pos_w90": tt.w_at_quantile(hist, 0.9), "path_cells": int(a_out[1].sum().item())},
         "verify": {"GBps": round(gbs_verify, 1), "frac_of_peak": round(gbs_verify / HBM_PEAK_GBS, 4),
                    "algorithmic_bytes": verify_bytes, "accept_rate": round(float(acc[acc >= 0].sum()) /
                                                                            max(1, int(m_s.sum())), 4)},

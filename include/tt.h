@@ -224,6 +224,26 @@ int tt_verify_dense(int32_t n_streams, int32_t v,
                     void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * tt_delta_histogram -- position deviation of the matched tokens of aligned pairs
+ * (Sec. 5 "DTW Bridges the Gap", Fig. CDF; App. K "Settings of w").  A cell (i, j)
+ * of an optimal warping path matches draft token i with proxy target token j; it
+ * deviates by |i - j| positions.  App. K aligns without a band (w < 0), reads the
+ * offset where the CDF of this deviation reaches 0.9 and searches w below it.
+ *
+ * Inputs (device): draft_off, target_off, path_len and path exactly as tt_align
+ * wrote them (pair b's path_len[b] cells start at int32 index
+ * 2*(draft_off[b] + target_off[b])); a pair with path_len[b] <= 0 (a sentinel) or
+ * longer than K_b + M_b contributes nothing.
+ * Output (device): hist[n_bins] int32, overwritten: hist[d] = number of cells with
+ * |i - j| = d for d < n_bins - 1, hist[n_bins - 1] = number with |i - j| >= n_bins - 1.
+ * n_bins in [1, 8192].  Two kernels on `stream` (a fill, then the count); the
+ * counts do not depend on scheduling.  TT_EINVAL on a bad size or a missing pointer.
+ */
+int tt_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
+                       const int32_t *path_len, const int32_t *path, int32_t n_bins,
+                       int32_t *hist, void *stream);
+
+/*
  * Workspace bytes tt_step needs: the larger of tt_align_workspace_size and
  * tt_verify_workspace_size for the same arguments (the two stages run one after
  * the other and share it).

@@ -10,6 +10,7 @@ raised.
     transfer  tt_transfer  draft probability of the aligned draft token (Alg. 2, App. A.2)
     verify    tt_verify    acceptance, residual / bonus sampling (Sec. 3, 4.2.2-4.2.3, App. D Alg. 4)
     verify_dense  tt_verify_dense  the same with dense proposals over one vocabulary (App. D Alg. 4)
+    delta_histogram  tt_delta_histogram  |i - j| over the optimal paths' cells (Fig. CDF, App. K)
 """
 from __future__ import annotations
 
@@ -17,7 +18,7 @@ import ctypes
 import os
 
 __all__ = ["Vocab", "align", "align_workspace", "transfer", "verify", "verify_dense", "verify_workspace", "lib",
-           "LIB_PATH",
+           "delta_histogram", "w_at_quantile", "LIB_PATH",
            "TTError", "path_capacity"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtt.so")
@@ -65,6 +66,8 @@ def lib():
         L.tt_verify.restype = ctypes.c_int
         L.tt_verify_dense.argtypes = [i32, i32, P, P, P, i64, P, i64, P, P, i32, P, P, P, P, sz, P]
         L.tt_verify_dense.restype = ctypes.c_int
+        L.tt_delta_histogram.argtypes = [i32, P, P, P, P, i32, P, P]
+        L.tt_delta_histogram.restype = ctypes.c_int
         L.tt_step_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz)]
         L.tt_step_workspace_size.restype = ctypes.c_int
         L.tt_step.argtypes = [VP, VP, i32, i32, i32, P, P, P, P, i32, i32, i32, P, i64, P, i64, P, P,
@@ -260,6 +263,33 @@ def verify_dense(v: int, draft_ids, off, draft_probs, target_probs, u_accept, u_
                                ctypes.c_void_p(workspace.data_ptr()), int(workspace.numel()), _stream_handle(stream))
     _check(st, "tt_verify_dense")
     return out
+
+
+def delta_histogram(draft_off, target_off, path_len, path, n_bins: int, out=None, stream=None):
+    """tt_delta_histogram: int32 counts of |i - j| over every aligned pair's path cells (last bin
+    collects |i - j| >= n_bins - 1)."""
+    torch = _torch()
+    i32 = torch.int32
+    n = int(draft_off.numel()) - 1
+    hist = torch.empty(int(n_bins), dtype=i32, device=draft_off.device) if out is None else out
+    st = lib().tt_delta_histogram(n, _ptr(draft_off, i32, "draft_off"), _ptr(target_off, i32, "target_off"),
+                                  _ptr(path_len, i32, "path_len"), _ptr(path, i32, "path"), int(n_bins),
+                                  _ptr(hist, i32, "hist"), _stream_handle(stream))
+    _check(st, "tt_delta_histogram")
+    return hist
+
+
+def w_at_quantile(hist, quantile: float = 0.9) -> int:
+    """App. K: the smallest deviation d whose CDF reaches `quantile` (host arithmetic on a
+    histogram returned by delta_histogram); the band half-width search stays at or below it."""
+    import numpy as np
+
+    h = np.asarray(hist.cpu() if hasattr(hist, "cpu") else hist, dtype=np.int64)
+    total = int(h.sum())
+    if total == 0:
+        return 0
+    need = quantile * total
+    return int(np.searchsorted(np.cumsum(h), need, side="left"))
 
 
 def step_workspace(n_streams: int, v_t: int, max_k: int, max_m: int, w: int, max_token_bytes: int,

@@ -1,0 +1,59 @@
+// Position deviation of matched tokens (Sec. 5 "DTW Bridges the Gap", Fig. CDF; App. K
+// "Settings of w"): a draft / proxy target pair (i, j) on an optimal warping path deviates
+// by |i - j| positions.  The histogram over a batch of aligned pairs is what App. K's
+// procedure reads to place the band half-width w (the offset where the CDF reaches 0.9,
+// collected with w = infinity).
+//
+// Two launches: a fill kernel clears the histogram (no memset node, so the call can be
+// captured in a HIP graph), then one 256-thread workgroup per group of pairs counts into an
+// LDS histogram and adds its non-zero bins to the global one with device-scope atomics.
+// The result does not depend on the order of the additions.
+#include "tt_internal.h"
+
+namespace tt {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxGroups = 1024;
+
+__global__ void __launch_bounds__(kThreads) hist_clear(int32_t *hist, int n_bins) {
+    for (int d = threadIdx.x; d < n_bins; d += kThreads) hist[d] = 0;
+}
+
+__global__ void __launch_bounds__(kThreads) delta_hist(int32_t n_pairs, const int32_t *draft_off,
+                                                       const int32_t *target_off, const int32_t *path_len,
+                                                       const int32_t *path, int n_bins, int32_t *hist) {
+    extern __shared__ int32_t sh_hist[];
+    for (int d = threadIdx.x; d < n_bins; d += kThreads) sh_hist[d] = 0;
+    __syncthreads();
+    const int last = n_bins - 1;
+    for (int b = blockIdx.x; b < n_pairs; b += gridDim.x) {
+        const int K = draft_off[b + 1] - draft_off[b], M = target_off[b + 1] - target_off[b];
+        const int n = path_len[b];
+        if (n <= 0 || n > K + M) continue;  // sentinel pair, or a length the path area cannot hold
+        const int32_t *cells = path + 2 * (int64_t)(draft_off[b] + target_off[b]);
+        for (int c = threadIdx.x; c < n; c += kThreads) {
+            const int dev = abs(cells[2 * c] - cells[2 * c + 1]);
+            atomicAdd(&sh_hist[dev < last ? dev : last], 1);
+        }
+    }
+    __syncthreads();
+    for (int d = threadIdx.x; d < n_bins; d += kThreads)
+        if (sh_hist[d] != 0) atomicAdd(&hist[d], sh_hist[d]);
+}
+
+}  // namespace
+
+int launch_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
+                           const int32_t *path_len, const int32_t *path, int32_t n_bins, int32_t *hist,
+                           hipStream_t stream) {
+    hipLaunchKernelGGL(hist_clear, dim3(1), dim3(kThreads), 0, stream, hist, n_bins);
+    if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    if (n_pairs == 0) return TT_OK;
+    const int groups = n_pairs < kMaxGroups ? n_pairs : kMaxGroups;
+    hipLaunchKernelGGL(delta_hist, dim3(groups), dim3(kThreads), sizeof(int32_t) * (size_t)n_bins, stream, n_pairs,
+                       draft_off, target_off, path_len, path, n_bins, hist);
+    return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+}
+
+}  // namespace tt

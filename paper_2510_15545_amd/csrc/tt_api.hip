@@ -11,6 +11,7 @@ namespace {
 
 constexpr int32_t kMaxAlignLen = 4096;   // bound on K_b / M_b accepted by tt_align
 constexpr int32_t kMaxVerifyLen = 65536; // bound on M_b accepted by tt_verify
+constexpr int32_t kMaxHistBins = 8192;   // bins of tt_delta_histogram (its LDS copy: 32 KB)
 
 bool vocab_ok(const tt_vocab *v) {
     return v != nullptr && v->bytes != nullptr && v->offsets != nullptr && v->n_tokens >= 1 &&
@@ -156,6 +157,14 @@ int tt_verify_dense(int32_t n_streams, int32_t v, const int32_t *draft_ids, cons
     a.q_rows = draft_probs;
     a.q_ld = draft_ld;
     return tt::launch_verify(a, static_cast<hipStream_t>(stream));
+}
+
+int tt_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
+                       const int32_t *path_len, const int32_t *path, int32_t n_bins, int32_t *hist, void *stream) {
+    if (n_pairs < 0 || n_bins < 1 || n_bins > kMaxHistBins || hist == nullptr) return TT_EINVAL;
+    if (n_pairs > 0 && (!draft_off || !target_off || !path_len || !path)) return TT_EINVAL;
+    return tt::launch_delta_histogram(n_pairs, draft_off, target_off, path_len, path, n_bins, hist,
+                                      static_cast<hipStream_t>(stream));
 }
 
 int tt_step_workspace_size(int32_t n_streams, int32_t v_t, int32_t max_k, int32_t max_m, int32_t w,

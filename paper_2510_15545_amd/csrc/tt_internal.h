@@ -72,6 +72,11 @@ bool verify_row_path(int32_t n_streams, int32_t v_t);
 // Normalised residual rows from Z and r in the workspace (written by a previous launch).
 int launch_verify_residual(const VerifyArgs &a, hipStream_t stream);
 
+// ---------------------------------------------------------------- deviation histogram (delta.hip)
+int launch_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
+                           const int32_t *path_len, const int32_t *path, int32_t n_bins, int32_t *hist,
+                           hipStream_t stream);
+
 // ---------------------------------------------------------------- fused step (step.hip)
 struct StepArgs {
     AlignArgs al;     // alignment inputs and outputs

@@ -97,6 +97,12 @@ def test_invalid_arguments_return_before_launch():
     assert dense(ws=0) == tt.TT_EWORKSPACE
     assert dense(n=0, ids=None) == tt.TT_OK
 
+    assert L.tt_delta_histogram(1, dummy, dummy, dummy, dummy, 0, dummy, None) == tt.TT_EINVAL
+    assert L.tt_delta_histogram(1, dummy, dummy, dummy, dummy, 8193, dummy, None) == tt.TT_EINVAL
+    assert L.tt_delta_histogram(1, dummy, None, dummy, dummy, 8, dummy, None) == tt.TT_EINVAL
+    assert L.tt_delta_histogram(-1, dummy, dummy, dummy, dummy, 8, dummy, None) == tt.TT_EINVAL
+    assert L.tt_delta_histogram(1, dummy, dummy, dummy, dummy, 8, None, None) == tt.TT_EINVAL
+
     def step(vd=ctypes.byref(v), n=1, v_d=10, v_t=10, ld_d=10, ld_t=10, max_m=4, ids=dummy, ws=1 << 30):
         return L.tt_step(vd, ctypes.byref(v), n, v_d, v_t, ids, dummy, dummy, dummy, 4, max_m, 8,
                          dummy, ld_d, dummy, ld_t, dummy, dummy, dummy, dummy, dummy, dummy, dummy,
@@ -116,3 +122,13 @@ def test_binding_refuses_host_tensors():
     torch = pytest.importorskip("torch")
     with pytest.raises(ValueError):
         tt._ptr(torch.zeros(3, dtype=torch.int32), torch.int32, "x")
+
+
+def test_w_at_quantile_host_rule():
+    """App. K: the offset where the CDF of the deviation first reaches the quantile."""
+    assert tt.w_at_quantile([2, 3], 0.9) == 1
+    assert tt.w_at_quantile([9, 1], 0.9) == 0  # CDF(0) = 0.9 exactly
+    assert tt.w_at_quantile([89, 10, 1], 0.9) == 1
+    assert tt.w_at_quantile([0, 0, 5], 0.5) == 2
+    assert tt.w_at_quantile([0, 0, 0], 0.9) == 0
+    assert tt.w_at_quantile([1] * 10, 1.0) == 9
