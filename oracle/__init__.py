@@ -200,6 +200,52 @@ def delta_histogram(draft_off, target_off, path_len, path, n_bins):
     return hist
 
 
+def retokenize(vd_bytes, vd_off, vt_bytes, vt_off, draft_ids, draft_off, max_m=None, max_bytes=None):
+    """Sec. 4.2.1 / Alg. 2 (S = Tokenizer_d.encode(D), T = Tokenizer_t.decode(S)) and App. A.1
+    with a greedy longest-match target tokenizer over byte strings: the draft tokens' bytes are
+    concatenated into S; from the start of S, the longest target token that is a prefix of the
+    rest is emitted (the lowest id if several tokens share those bytes), until S is consumed.
+
+    Plain Python.  A stream whose string is longer than max_bytes, that encodes to more than
+    max_m tokens, that holds a draft id outside the table, or that meets a byte no target token
+    starts with, gets no tokens (an empty CSR row).  Returns (target_ids, target_off) int32."""
+    vd_bytes = bytes(np.asarray(vd_bytes, np.uint8))
+    vt_bytes = bytes(np.asarray(vt_bytes, np.uint8))
+    vd_off = np.asarray(vd_off, np.int64)
+    vt_off = np.asarray(vt_off, np.int64)
+    table = {}
+    longest = 0
+    for t in range(len(vt_off) - 1):
+        s = vt_bytes[vt_off[t]:vt_off[t + 1]]
+        longest = max(longest, len(s))
+        if s not in table:  # ids ascend: the first holder of a string is the lowest id
+            table[s] = t
+    out, off = [], [0]
+    n_d = len(vd_off) - 1
+    for b in range(len(draft_off) - 1):
+        ids = [int(x) for x in draft_ids[draft_off[b]:draft_off[b + 1]]]
+        toks = []
+        if all(0 <= i < n_d for i in ids):
+            S = b"".join(vd_bytes[vd_off[i]:vd_off[i + 1]] for i in ids)
+            if max_bytes is None or len(S) <= max_bytes:
+                p = 0
+                while p < len(S):
+                    for ln in range(min(longest, len(S) - p), 0, -1):
+                        t = table.get(S[p:p + ln])
+                        if t is not None:
+                            toks.append(t)
+                            p += ln
+                            break
+                    else:
+                        toks = []
+                        break
+                if max_m is not None and len(toks) > max_m:
+                    toks = []
+        out.extend(toks)
+        off.append(off[-1] + len(toks))
+    return np.array(out, np.int32), np.array(off, np.int32)
+
+
 def threshold(u: float, Z: int) -> int:
     return int(lib().orc_threshold(float(np.float32(u)), int(Z)))
 
