@@ -244,6 +244,51 @@ int tt_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t 
                        int32_t *hist, void *stream);
 
 /*
+ * Token index for longest-match lookups in a vocabulary (used by tt_retokenize for
+ * the target vocabulary).  tt_token_index_size gives its bytes for n_tokens
+ * (16 bytes per hash slot, a power of two >= 4 * n_tokens slots); n_tokens in
+ * [1, 2^28].  tt_token_index_build fills `index` (device, 16-byte aligned, at
+ * least that many bytes, owned by the caller) from the table `v` in three kernels
+ * on `stream`; tokens of length 0 or above v->max_token_bytes are left out, and of
+ * several tokens with the same bytes only the lowest id can be found.  The index
+ * stays valid while the table's device arrays are unchanged.  TT_EUNSUPPORTED if
+ * v->max_token_bytes > 64, TT_EWORKSPACE if index_bytes is too small.
+ */
+int tt_token_index_size(int32_t n_tokens, size_t *bytes);
+int tt_token_index_build(const tt_vocab *v, void *index, size_t index_bytes, void *stream);
+
+/* Workspace bytes tt_retokenize needs: a count and max_m ids per stream. */
+int tt_retokenize_workspace_size(int32_t n_streams, int32_t max_m, size_t *bytes);
+
+/*
+ * tt_retokenize -- proxy target tokens from the draft tokens (Sec. 4.2.1 "Draft Token
+ * Calculation": S = Tokenizer_d.encode(D), T = Tokenizer_t.decode(S), also the
+ * first lines of Alg. 2's loop; App. A.1: T spells the same string as D).  The
+ * target tokenizer is greedy longest match over byte strings: S is the
+ * concatenation of the draft tokens' bytes, and from its start the longest target
+ * token that is a prefix of the rest of S is emitted (the lowest id among tokens
+ * with equal bytes) until S is consumed.
+ *
+ * Inputs (device unless noted): vd, vt token tables (host structs); vt_index built
+ * by tt_token_index_build for vt (index_bytes, host, its size); draft_ids /
+ * draft_off CSR as for tt_align; max_bytes (host, 1..4096) bounds |S| per stream
+ * and max_m (host, 1..4096) bounds |T|.
+ * Outputs (device): target_off[n_streams + 1] CSR offsets and target_ids packed by
+ * them (capacity n_streams * max_m ints is always enough).  A stream with a draft id
+ * outside vd, |S| > max_bytes, more than max_m target tokens, or a byte of S that no
+ * target token starts with gets zero tokens (target_off[b+1] = target_off[b]), which
+ * tt_align then treats as a sentinel pair.
+ * workspace: tt_retokenize_workspace_size bytes, no initialisation; calls that
+ * overlap in time must not share it.  Three kernels: one workgroup per stream, one
+ * for the offsets, one to pack the ids.
+ */
+int tt_retokenize(const tt_vocab *vd, const tt_vocab *vt, const void *vt_index, size_t index_bytes,
+                  int32_t n_streams, const int32_t *draft_ids, const int32_t *draft_off,
+                  int32_t max_bytes, int32_t max_m,
+                  int32_t *target_ids, int32_t *target_off,
+                  void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Workspace bytes tt_step needs: the larger of tt_align_workspace_size and
  * tt_verify_workspace_size for the same arguments (the two stages run one after
  * the other and share it).

@@ -11,6 +11,8 @@ raised.
     verify    tt_verify    acceptance, residual / bonus sampling (Sec. 3, 4.2.2-4.2.3, App. D Alg. 4)
     verify_dense  tt_verify_dense  the same with dense proposals over one vocabulary (App. D Alg. 4)
     delta_histogram  tt_delta_histogram  |i - j| over the optimal paths' cells (Fig. CDF, App. K)
+    token_index / retokenize  tt_token_index_build / tt_retokenize  draft tokens -> proxy target
+              tokens by greedy longest match (Sec. 4.2.1, Alg. 2, App. A.1)
 """
 from __future__ import annotations
 
@@ -18,7 +20,7 @@ import ctypes
 import os
 
 __all__ = ["Vocab", "align", "align_workspace", "transfer", "verify", "verify_dense", "verify_workspace", "lib",
-           "delta_histogram", "w_at_quantile", "LIB_PATH",
+           "delta_histogram", "w_at_quantile", "token_index", "retokenize", "LIB_PATH",
            "TTError", "path_capacity"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtt.so")
@@ -68,6 +70,14 @@ def lib():
         L.tt_verify_dense.restype = ctypes.c_int
         L.tt_delta_histogram.argtypes = [i32, P, P, P, P, i32, P, P]
         L.tt_delta_histogram.restype = ctypes.c_int
+        L.tt_token_index_size.argtypes = [i32, ctypes.POINTER(sz)]
+        L.tt_token_index_size.restype = ctypes.c_int
+        L.tt_token_index_build.argtypes = [VP, P, sz, P]
+        L.tt_token_index_build.restype = ctypes.c_int
+        L.tt_retokenize_workspace_size.argtypes = [i32, i32, ctypes.POINTER(sz)]
+        L.tt_retokenize_workspace_size.restype = ctypes.c_int
+        L.tt_retokenize.argtypes = [VP, VP, P, sz, i32, P, P, i32, i32, P, P, P, sz, P]
+        L.tt_retokenize.restype = ctypes.c_int
         L.tt_step_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz)]
         L.tt_step_workspace_size.restype = ctypes.c_int
         L.tt_step.argtypes = [VP, VP, i32, i32, i32, P, P, P, P, i32, i32, i32, P, i64, P, i64, P, P,
@@ -290,6 +300,42 @@ def w_at_quantile(hist, quantile: float = 0.9) -> int:
         return 0
     need = quantile * total
     return int(np.searchsorted(np.cumsum(h), need, side="left"))
+
+
+def token_index(v: Vocab, stream=None):
+    """tt_token_index_build: the longest-match index of a token table (a uint8 device tensor)."""
+    torch = _torch()
+    n = ctypes.c_size_t(0)
+    _check(lib().tt_token_index_size(v.n_tokens, ctypes.byref(n)), "tt_token_index_size")
+    idx = torch.empty(n.value, dtype=torch.uint8, device=v.offsets.device)
+    _check(lib().tt_token_index_build(ctypes.byref(v._c), ctypes.c_void_p(idx.data_ptr()), n.value,
+                                      _stream_handle(stream)), "tt_token_index_build")
+    return idx
+
+
+def retokenize(vd: Vocab, vt: Vocab, vt_index, draft_ids, draft_off, max_bytes: int, max_m: int,
+               out=None, workspace=None, stream=None):
+    """tt_retokenize.  Returns (target_ids, target_off) device tensors; target_ids has room for
+    n_streams * max_m ids (the first target_off[-1] are valid)."""
+    torch = _torch()
+    i32 = torch.int32
+    n = int(draft_off.numel()) - 1
+    dev = draft_off.device
+    if workspace is None:
+        nb = ctypes.c_size_t(0)
+        _check(lib().tt_retokenize_workspace_size(n, int(max_m), ctypes.byref(nb)), "tt_retokenize_workspace_size")
+        workspace = torch.empty(max(1, nb.value), dtype=torch.uint8, device=dev)
+    if out is None:
+        out = (torch.empty(max(1, n * int(max_m)), dtype=i32, device=dev), torch.empty(n + 1, dtype=i32, device=dev))
+    tids, toff = out
+    ids = draft_ids if draft_ids.numel() else torch.zeros(1, dtype=i32, device=dev)
+    st = lib().tt_retokenize(ctypes.byref(vd._c), ctypes.byref(vt._c), ctypes.c_void_p(vt_index.data_ptr()),
+                             int(vt_index.numel()), n, _ptr(ids, i32, "draft_ids"), _ptr(draft_off, i32, "draft_off"),
+                             int(max_bytes), int(max_m), _ptr(tids, i32, "target_ids"),
+                             _ptr(toff, i32, "target_off"), ctypes.c_void_p(workspace.data_ptr()),
+                             int(workspace.numel()), _stream_handle(stream))
+    _check(st, "tt_retokenize")
+    return out
 
 
 def step_workspace(n_streams: int, v_t: int, max_k: int, max_m: int, w: int, max_token_bytes: int,

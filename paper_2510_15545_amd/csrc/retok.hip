@@ -1,0 +1,399 @@
+// Re-tokenisation of the draft tokens into proxy target tokens (Sec. 4.2.1 "Draft Token
+// Calculation", Alg. 2 lines S = Tokenizer_d.encode(D), T = Tokenizer_t.decode(S); App. A.1
+// string consistency) with a greedy longest-match target tokenizer over byte strings: the
+// draft tokens' bytes form S, and from the start of S the longest target token that is a
+// prefix of the rest is emitted (the lowest id among tokens with the same bytes).
+//
+// Target token index (built once per vocabulary): open addressing with linear probing,
+// capacity a power of two >= 4 x the token count (load <= 1/4, so a miss probes ~1.4
+// slots).  A slot is 16 bytes {first 8 bytes of the token, length, id} and is read with
+// one 16-byte load; tokens longer than 8 bytes compare their tail against the table.  The
+// slot of a token whose bytes equal those of a lower id is marked dead by a second pass.
+// Hash: 32-bit FNV-1a over the token bytes (Fowler, Noll, Vo).
+//
+// tt_retokenize, one 256-thread workgroup per stream:
+//   1. the draft ids' lengths and a block prefix sum give each token's offset in S; the
+//      bytes of S are staged into LDS (at most 4096);
+//   2. every byte position p computes L(p), the longest target token starting at p: the
+//      FNV-1a hashes of all prefixes come from one pass over the bytes, and the first
+//      slot of eight candidate lengths is loaded together (longest first);
+//   3. one wave walks p -> p + L(p) from 0 with the L and token values of 64 positions
+//      held in its lanes (readlane per step), writing the emitted ids to LDS;
+//   4. the ids go to a padded per-stream area of the workspace with their count.
+// Then one workgroup turns the counts into CSR offsets and a copy kernel packs the ids.
+#include "tt_internal.h"
+
+namespace tt {
+namespace {
+
+constexpr uint32_t kFnvBasis = 2166136261u;
+constexpr uint32_t kFnvPrime = 16777619u;
+constexpr int kThreads = 256;
+constexpr int kWave = 64;
+constexpr int kBatch = 8;  // candidate lengths probed together
+constexpr int kScanThreads = 1024;
+
+struct Slot {
+    uint64_t key;  // first min(len, 8) bytes, little-endian, zero-padded
+    int32_t len;   // token length; -1: dead (a lower id has the same bytes)
+    int32_t id;    // -1: empty
+};
+static_assert(sizeof(Slot) == 16, "one 16-byte load per slot");
+
+__device__ __forceinline__ uint32_t fnv_step(uint32_t h, uint32_t c) { return (h ^ c) * kFnvPrime; }
+
+__device__ __forceinline__ Slot load_slot(const Slot *tab, uint32_t s) {
+    const int4 v = *reinterpret_cast<const int4 *>(tab + s);
+    Slot e;
+    e.key = (uint64_t)(uint32_t)v.x | ((uint64_t)(uint32_t)v.y << 32);
+    e.len = v.z;
+    e.id = v.w;
+    return e;
+}
+
+// bytes of token t equal bytes[0 .. len) beyond the first 8 (the key covers those)
+__device__ __forceinline__ bool tail_equal(const tt_vocab &v, int t, const uint8_t *s, int len) {
+    const uint8_t *tb = v.bytes + v.offsets[t];
+    for (int k = 8; k < len; ++k)
+        if (tb[k] != s[k]) return false;
+    return true;
+}
+
+__global__ void __launch_bounds__(kThreads) index_clear(Slot *tab, uint32_t cap) {
+    for (uint32_t s = blockIdx.x * kThreads + threadIdx.x; s < cap; s += gridDim.x * kThreads) {
+        tab[s].key = 0;
+        tab[s].len = 0;
+        tab[s].id = -1;
+    }
+}
+
+// hash, key and length of token t; false if its length is outside [1, max_token_bytes]
+__device__ __forceinline__ bool token_sig(const tt_vocab &v, int t, uint32_t &h, uint64_t &key, int &len) {
+    const int o = v.offsets[t];
+    len = v.offsets[t + 1] - o;
+    if (len < 1 || len > v.max_token_bytes) return false;
+    h = kFnvBasis;
+    key = 0;
+    for (int k = 0; k < len; ++k) {
+        const uint32_t c = v.bytes[o + k];
+        h = fnv_step(h, c);
+        if (k < 8) key |= (uint64_t)c << (8 * k);
+    }
+    return true;
+}
+
+__global__ void __launch_bounds__(kThreads) index_insert(tt_vocab v, Slot *tab, uint32_t mask) {
+    const int t = blockIdx.x * kThreads + threadIdx.x;
+    if (t >= v.n_tokens) return;
+    uint32_t h;
+    uint64_t key;
+    int len;
+    if (!token_sig(v, t, h, key, len)) return;
+    uint32_t s = h & mask;
+    for (uint32_t probe = 0; probe <= mask; ++probe) {  // at most 1/4 of the slots are taken
+        if (atomicCAS(&tab[s].id, -1, t) == -1) {
+            tab[s].key = key;
+            tab[s].len = len;
+            return;
+        }
+        s = (s + 1) & mask;
+    }
+}
+
+// A token whose bytes equal those of a lower id marks its own slot dead.  The lowest id of a
+// group is never marked and lies on every member's probe chain (linear probing leaves no
+// empty slot between a hash's home slot and any entry inserted from it), so the outcome
+// does not depend on the order in which members run.
+__global__ void __launch_bounds__(kThreads) index_dedup(tt_vocab v, Slot *tab, uint32_t mask) {
+    const int t = blockIdx.x * kThreads + threadIdx.x;
+    if (t >= v.n_tokens) return;
+    uint32_t h;
+    uint64_t key;
+    int len;
+    if (!token_sig(v, t, h, key, len)) return;
+    const uint8_t *tb = v.bytes + v.offsets[t];
+    uint32_t s = h & mask;
+    int own = -1;
+    bool dup = false;
+    for (uint32_t probe = 0; probe <= mask; ++probe) {
+        const int id = tab[s].id;
+        if (id < 0) break;
+        if (id == t) own = (int)s;
+        else if (id < t && tab[s].key == key && __hip_atomic_load(&tab[s].len, __ATOMIC_RELAXED,
+                                                                   __HIP_MEMORY_SCOPE_AGENT) == len &&
+                 tail_equal(v, id, tb, len))
+            dup = true;
+        s = (s + 1) & mask;
+    }
+    if (dup && own >= 0) __hip_atomic_store(&tab[own].len, -1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Block-wide exclusive prefix sum of one int per thread (256 threads); *total gets the sum.
+__device__ __forceinline__ int block_exclusive_scan(int v, int *sh_w, int *total) {
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    int x = v;
+    for (int d = 1; d < kWave; d <<= 1) {
+        const int y = __shfl_up(x, d);
+        if (lane >= d) x += y;
+    }
+    if (lane == kWave - 1) sh_w[wave] = x;
+    __syncthreads();
+    int before = 0, all = 0;
+    for (int w = 0; w < kThreads / kWave; ++w) {
+        before += w < wave ? sh_w[w] : 0;
+        all += sh_w[w];
+    }
+    __syncthreads();
+    *total = all;
+    return before + x - v;
+}
+
+struct RetokParams {
+    tt_vocab vd, vt;
+    const Slot *tab;
+    uint32_t mask;
+    int32_t n_streams;
+    const int32_t *draft_ids, *draft_off;
+    int32_t max_bytes, max_m;
+    int32_t *counts, *ids;  // workspace: per-stream count, padded ids [n_streams x max_m]
+    int32_t *target_ids, *target_off;
+};
+
+__global__ void __launch_bounds__(kThreads) retok_stream(RetokParams p) {
+    extern __shared__ int32_t sh[];
+    // LDS: pos/out [max_bytes] | ids [max_bytes] | tok [max_bytes] | L (u8) | S (u8)
+    int32_t *sh_pos = sh;                     // token offsets in S, later the emitted ids
+    int32_t *sh_ids = sh + p.max_bytes;       // draft ids
+    int32_t *sh_tok = sh + 2 * p.max_bytes;   // longest-match token at each position
+    uint8_t *sh_L = reinterpret_cast<uint8_t *>(sh + 3 * p.max_bytes);
+    uint8_t *sh_S = sh_L + p.max_bytes;
+    __shared__ int sh_w[kThreads / kWave];
+    __shared__ int sh_bad, sh_m;
+
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int d0 = p.draft_off[b];
+    const int K = p.draft_off[b + 1] - d0;
+    if (tid == 0) sh_bad = (K < 0 || K > p.max_bytes) ? 1 : 0;
+    __syncthreads();
+    // 1. offsets of the draft tokens in S, then the bytes of S
+    int n = 0;
+    if (!sh_bad) {
+        int carry = 0;
+        for (int base = 0; base < K; base += kThreads) {
+            const int i = base + tid;
+            int len = 0;
+            if (i < K) {
+                const int id = p.draft_ids[d0 + i];
+                if (id < 0 || id >= p.vd.n_tokens) {
+                    sh_bad = 1;
+                } else {
+                    len = p.vd.offsets[id + 1] - p.vd.offsets[id];
+                    if (len < 0) sh_bad = 1;
+                }
+                sh_ids[i] = id;
+            }
+            int tot;
+            const int ex = block_exclusive_scan(len < 0 ? 0 : len, sh_w, &tot);
+            if (i < K) sh_pos[i] = carry + ex;
+            carry += tot;
+            if (carry > p.max_bytes) break;  // uniform: every thread sees the same carry
+        }
+        n = carry;
+    }
+    __syncthreads();
+    if (n > p.max_bytes) sh_bad = 1;
+    __syncthreads();
+    if (!sh_bad) {
+        for (int x = tid; x < n; x += kThreads) {
+            int lo = 0, hi = K - 1;  // last token with pos <= x (zero-length tokens are skipped over)
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (sh_pos[mid] <= x) lo = mid;
+                else hi = mid - 1;
+            }
+            const int id = sh_ids[lo];
+            sh_S[x] = p.vd.bytes[p.vd.offsets[id] + (x - sh_pos[lo])];
+        }
+    }
+    __syncthreads();
+    // 2. longest target token starting at every position
+    if (!sh_bad) {
+        const int lmax_v = p.vt.max_token_bytes;
+        for (int x = tid; x < n; x += kThreads) {
+            const int lmax = lmax_v < n - x ? lmax_v : n - x;
+            int best_len = 0, best_tok = 0;
+            for (int hi = lmax; hi >= 1 && best_len == 0; hi -= kBatch) {
+                const int lo = hi - kBatch + 1;  // candidates lo..hi (lo may be < 1)
+                uint32_t h = kFnvBasis;
+                uint64_t key = 0;
+                const int pre = lo - 1 > 0 ? lo - 1 : 0;
+                for (int k = 0; k < pre; ++k) {
+                    const uint32_t c = sh_S[x + k];
+                    h = fnv_step(h, c);
+                    if (k < 8) key |= (uint64_t)c << (8 * k);
+                }
+                uint32_t hs[kBatch];
+                uint64_t ks[kBatch];
+#pragma unroll
+                for (int k = 0; k < kBatch; ++k) {
+                    const int l = lo + k;  // candidate length
+                    if (l >= 1) {
+                        const uint32_t c = sh_S[x + l - 1];
+                        h = fnv_step(h, c);
+                        if (l <= 8) key |= (uint64_t)c << (8 * (l - 1));
+                    }
+                    hs[k] = h;
+                    ks[k] = key;
+                }
+                Slot e[kBatch];
+#pragma unroll
+                for (int k = 0; k < kBatch; ++k) {
+                    e[k].id = -1;
+                    if (lo + k >= 1) e[k] = load_slot(p.tab, hs[k] & p.mask);
+                }
+#pragma unroll
+                for (int k = kBatch - 1; k >= 0; --k) {
+                    const int l = lo + k;
+                    if (l < 1 || best_len != 0) continue;
+                    uint32_t s = hs[k] & p.mask;
+                    Slot c = e[k];
+                    for (uint32_t probe = 0; probe <= p.mask && c.id >= 0; ++probe) {
+                        if (c.len == l && c.key == ks[k] && (l <= 8 || tail_equal(p.vt, c.id, sh_S + x, l))) {
+                            best_len = l;
+                            best_tok = c.id;
+                            break;
+                        }
+                        s = (s + 1) & p.mask;
+                        c = load_slot(p.tab, s);
+                    }
+                }
+            }
+            sh_L[x] = (uint8_t)best_len;
+            sh_tok[x] = best_tok;
+        }
+    }
+    __syncthreads();
+    // 3. the greedy walk, one wave, 64 positions per window held in lanes
+    if (wave == 0) {
+        int pos = 0, m = 0;
+        bool fail = sh_bad != 0;
+        while (!fail && pos < n) {
+            const int p0 = pos;
+            const int lv = p0 + lane < n ? (int)sh_L[p0 + lane] : 0;
+            const int tv = p0 + lane < n ? sh_tok[p0 + lane] : 0;
+            while (pos < n && pos < p0 + kWave) {
+                const int l = __builtin_amdgcn_readlane(lv, pos - p0);
+                if (l == 0 || m >= p.max_m) {
+                    fail = true;
+                    break;
+                }
+                const int t = __builtin_amdgcn_readlane(tv, pos - p0);
+                if (lane == 0) sh_pos[m] = t;  // sh_pos is free again: reuse it for the output
+                ++m;
+                pos += l;
+            }
+        }
+        if (lane == 0) sh_m = fail ? 0 : m;
+    }
+    __syncthreads();
+    // 4. padded output and count
+    const int m = sh_m;
+    for (int j = tid; j < m; j += kThreads) p.ids[(int64_t)b * p.max_m + j] = sh_pos[j];
+    if (tid == 0) p.counts[b] = m;
+}
+
+// CSR offsets from the counts (one workgroup, running total over chunks of 1024 streams).
+__global__ void __launch_bounds__(kScanThreads) retok_offsets(RetokParams p) {
+    __shared__ int sh_w[kScanThreads / kWave];
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    int carry = 0;
+    if (tid == 0) p.target_off[0] = 0;
+    for (int base = 0; base < p.n_streams; base += kScanThreads) {
+        const int b = base + tid;
+        const int v = b < p.n_streams ? p.counts[b] : 0;
+        int x = v;
+        for (int d = 1; d < kWave; d <<= 1) {
+            const int y = __shfl_up(x, d);
+            if (lane >= d) x += y;
+        }
+        if (lane == kWave - 1) sh_w[wave] = x;
+        __syncthreads();
+        int before = 0, all = 0;
+        for (int w = 0; w < kScanThreads / kWave; ++w) {
+            before += w < wave ? sh_w[w] : 0;
+            all += sh_w[w];
+        }
+        __syncthreads();
+        if (b < p.n_streams) p.target_off[b + 1] = carry + before + x;
+        carry += all;
+    }
+}
+
+__global__ void __launch_bounds__(kThreads) retok_pack(RetokParams p) {
+    const int b = blockIdx.x;
+    const int o = p.target_off[b];
+    const int m = p.target_off[b + 1] - o;
+    for (int j = threadIdx.x; j < m; j += kThreads) p.target_ids[o + j] = p.ids[(int64_t)b * p.max_m + j];
+}
+
+inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+}  // namespace
+
+uint32_t token_index_capacity(int32_t n_tokens) {
+    uint32_t cap = 64;
+    while (cap < 4u * (uint32_t)n_tokens) cap <<= 1;
+    return cap;
+}
+
+size_t token_index_bytes(int32_t n_tokens) { return sizeof(Slot) * (size_t)token_index_capacity(n_tokens); }
+
+int launch_token_index_build(const tt_vocab &v, void *index, hipStream_t stream) {
+    const uint32_t cap = token_index_capacity(v.n_tokens);
+    Slot *tab = static_cast<Slot *>(index);
+    hipLaunchKernelGGL(index_clear, dim3((cap + kThreads - 1) / kThreads < 2048 ? (cap + kThreads - 1) / kThreads : 2048),
+                       dim3(kThreads), 0, stream, tab, cap);
+    if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    const dim3 grid((v.n_tokens + kThreads - 1) / kThreads);
+    hipLaunchKernelGGL(index_insert, grid, dim3(kThreads), 0, stream, v, tab, cap - 1);
+    if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    hipLaunchKernelGGL(index_dedup, grid, dim3(kThreads), 0, stream, v, tab, cap - 1);
+    return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+}
+
+size_t retok_workspace_bytes(int32_t n_streams, int32_t max_m) {
+    return align256(4 * (size_t)n_streams) + 4 * (size_t)n_streams * (size_t)max_m;
+}
+
+size_t retok_lds_bytes(int32_t max_bytes) { return 14 * (size_t)max_bytes; }
+
+int launch_retokenize(const RetokArgs &a, hipStream_t stream) {
+    RetokParams p;
+    p.vd = a.vd;
+    p.vt = a.vt;
+    p.tab = static_cast<const Slot *>(a.index);
+    p.mask = token_index_capacity(a.vt.n_tokens) - 1;
+    p.n_streams = a.n_streams;
+    p.draft_ids = a.draft_ids;
+    p.draft_off = a.draft_off;
+    p.max_bytes = a.max_bytes;
+    p.max_m = a.max_m;
+    uint8_t *ws = static_cast<uint8_t *>(a.workspace);
+    p.counts = reinterpret_cast<int32_t *>(ws);
+    p.ids = reinterpret_cast<int32_t *>(ws + align256(4 * (size_t)a.n_streams));
+    p.target_ids = a.target_ids;
+    p.target_off = a.target_off;
+    if (a.n_streams > 0) {
+        hipLaunchKernelGGL(retok_stream, dim3(a.n_streams), dim3(kThreads), retok_lds_bytes(a.max_bytes), stream, p);
+        if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    }
+    hipLaunchKernelGGL(retok_offsets, dim3(1), dim3(kScanThreads), 0, stream, p);  // target_off[0] = 0 at least
+    if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    if (a.n_streams == 0) return TT_OK;
+    hipLaunchKernelGGL(retok_pack, dim3(a.n_streams), dim3(kThreads), 0, stream, p);
+    return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+}
+
+}  // namespace tt

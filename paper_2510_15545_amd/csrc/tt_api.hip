@@ -12,6 +12,9 @@ namespace {
 constexpr int32_t kMaxAlignLen = 4096;   // bound on K_b / M_b accepted by tt_align
 constexpr int32_t kMaxVerifyLen = 65536; // bound on M_b accepted by tt_verify
 constexpr int32_t kMaxHistBins = 8192;   // bins of tt_delta_histogram (its LDS copy: 32 KB)
+constexpr int32_t kMaxIndexTokens = 1 << 28;  // vocabulary size a token index accepts
+constexpr int32_t kMaxTokenBytes = 64;        // longest target token the index and lookups handle
+constexpr int32_t kMaxRetokBytes = 4096;      // bytes of S (and tokens of T) per stream: 14 B of LDS each
 
 bool vocab_ok(const tt_vocab *v) {
     return v != nullptr && v->bytes != nullptr && v->offsets != nullptr && v->n_tokens >= 1 &&
@@ -165,6 +168,53 @@ int tt_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t 
     if (n_pairs > 0 && (!draft_off || !target_off || !path_len || !path)) return TT_EINVAL;
     return tt::launch_delta_histogram(n_pairs, draft_off, target_off, path_len, path, n_bins, hist,
                                       static_cast<hipStream_t>(stream));
+}
+
+int tt_token_index_size(int32_t n_tokens, size_t *bytes) {
+    if (bytes == nullptr || n_tokens < 1 || n_tokens > kMaxIndexTokens) return TT_EINVAL;
+    *bytes = tt::token_index_bytes(n_tokens);
+    return TT_OK;
+}
+
+int tt_token_index_build(const tt_vocab *v, void *index, size_t index_bytes, void *stream) {
+    if (!vocab_ok(v) || v->n_tokens > kMaxIndexTokens || index == nullptr) return TT_EINVAL;
+    if (v->max_token_bytes > kMaxTokenBytes) return TT_EUNSUPPORTED;
+    if ((reinterpret_cast<uintptr_t>(index) & 15u) != 0) return TT_EINVAL;
+    if (index_bytes < tt::token_index_bytes(v->n_tokens)) return TT_EWORKSPACE;
+    return tt::launch_token_index_build(*v, index, static_cast<hipStream_t>(stream));
+}
+
+int tt_retokenize_workspace_size(int32_t n_streams, int32_t max_m, size_t *bytes) {
+    if (bytes == nullptr || n_streams < 0 || max_m < 1 || max_m > kMaxRetokBytes) return TT_EINVAL;
+    *bytes = tt::retok_workspace_bytes(n_streams, max_m);
+    return TT_OK;
+}
+
+int tt_retokenize(const tt_vocab *vd, const tt_vocab *vt, const void *vt_index, size_t index_bytes,
+                  int32_t n_streams, const int32_t *draft_ids, const int32_t *draft_off, int32_t max_bytes,
+                  int32_t max_m, int32_t *target_ids, int32_t *target_off, void *workspace,
+                  size_t workspace_bytes, void *stream) {
+    if (!vocab_ok(vd) || !vocab_ok(vt) || vt->n_tokens > kMaxIndexTokens || n_streams < 0) return TT_EINVAL;
+    if (max_bytes < 1 || max_bytes > kMaxRetokBytes || max_m < 1 || max_m > kMaxRetokBytes) return TT_EINVAL;
+    if (vt->max_token_bytes > kMaxTokenBytes) return TT_EUNSUPPORTED;
+    if (vt_index == nullptr || (reinterpret_cast<uintptr_t>(vt_index) & 15u) != 0) return TT_EINVAL;
+    if (index_bytes < tt::token_index_bytes(vt->n_tokens)) return TT_EINVAL;
+    if (!target_off) return TT_EINVAL;
+    if (n_streams > 0 && (!draft_ids || !draft_off || !target_ids)) return TT_EINVAL;
+    if (workspace == nullptr || workspace_bytes < tt::retok_workspace_bytes(n_streams, max_m)) return TT_EWORKSPACE;
+    tt::RetokArgs a;
+    a.vd = *vd;
+    a.vt = *vt;
+    a.index = vt_index;
+    a.n_streams = n_streams;
+    a.draft_ids = draft_ids;
+    a.draft_off = draft_off;
+    a.max_bytes = max_bytes;
+    a.max_m = max_m;
+    a.target_ids = target_ids;
+    a.target_off = target_off;
+    a.workspace = workspace;
+    return tt::launch_retokenize(a, static_cast<hipStream_t>(stream));
 }
 
 int tt_step_workspace_size(int32_t n_streams, int32_t v_t, int32_t max_k, int32_t max_m, int32_t w,

@@ -77,6 +77,23 @@ int launch_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int3
                            const int32_t *path_len, const int32_t *path, int32_t n_bins, int32_t *hist,
                            hipStream_t stream);
 
+// ---------------------------------------------------------------- re-tokenisation (retok.hip)
+uint32_t token_index_capacity(int32_t n_tokens);  // hash slots for a vocabulary of n_tokens
+size_t token_index_bytes(int32_t n_tokens);
+int launch_token_index_build(const tt_vocab &v, void *index, hipStream_t stream);
+struct RetokArgs {
+    tt_vocab vd, vt;
+    const void *index;  // token index of vt (launch_token_index_build)
+    int32_t n_streams;
+    const int32_t *draft_ids, *draft_off;
+    int32_t max_bytes, max_m;
+    int32_t *target_ids, *target_off;
+    void *workspace;
+};
+size_t retok_workspace_bytes(int32_t n_streams, int32_t max_m);
+size_t retok_lds_bytes(int32_t max_bytes);
+int launch_retokenize(const RetokArgs &a, hipStream_t stream);
+
 // ---------------------------------------------------------------- fused step (step.hip)
 struct StepArgs {
     AlignArgs al;     // alignment inputs and outputs

@@ -103,6 +103,29 @@ def test_invalid_arguments_return_before_launch():
     assert L.tt_delta_histogram(-1, dummy, dummy, dummy, dummy, 8, dummy, None) == tt.TT_EINVAL
     assert L.tt_delta_histogram(1, dummy, dummy, dummy, dummy, 8, None, None) == tt.TT_EINVAL
 
+    n = ctypes.c_size_t(0)
+    assert L.tt_token_index_size(0, ctypes.byref(n)) == tt.TT_EINVAL
+    assert L.tt_token_index_size(1000, ctypes.byref(n)) == 0 and n.value == 16 * 4096
+    assert L.tt_token_index_size(151936, ctypes.byref(n)) == 0 and n.value == 16 * (1 << 20)
+    assert L.tt_token_index_build(ctypes.byref(big), dummy, 1 << 30, None) == tt.TT_EUNSUPPORTED
+    assert L.tt_token_index_build(ctypes.byref(v), P(0x1004), 1 << 30, None) == tt.TT_EINVAL  # not 16-byte aligned
+    assert L.tt_token_index_build(ctypes.byref(v), dummy, 16, None) == tt.TT_EWORKSPACE
+    assert L.tt_retokenize_workspace_size(4, 0, ctypes.byref(n)) == tt.TT_EINVAL
+    assert L.tt_retokenize_workspace_size(4, 10, ctypes.byref(n)) == 0 and n.value >= 4 * 4 + 4 * 40
+
+    def retok(n=1, max_bytes=64, max_m=16, index=dummy, ib=1 << 20, ws=1 << 20, ids=dummy, vt=ctypes.byref(v)):
+        return L.tt_retokenize(ctypes.byref(v), vt, index, ib, n, ids, dummy, max_bytes, max_m, dummy, dummy, dummy,
+                               ws, None)
+    assert retok(max_bytes=0) == tt.TT_EINVAL
+    assert retok(max_bytes=4097) == tt.TT_EINVAL
+    assert retok(max_m=0) == tt.TT_EINVAL
+    assert retok(index=P(0x1008)) == tt.TT_EINVAL
+    assert retok(ib=16) == tt.TT_EINVAL
+    assert retok(ws=4) == tt.TT_EWORKSPACE
+    assert retok(ids=None) == tt.TT_EINVAL
+    assert retok(n=-1) == tt.TT_EINVAL
+    assert retok(vt=ctypes.byref(big)) == tt.TT_EUNSUPPORTED
+
     def step(vd=ctypes.byref(v), n=1, v_d=10, v_t=10, ld_d=10, ld_t=10, max_m=4, ids=dummy, ws=1 << 30):
         return L.tt_step(vd, ctypes.byref(v), n, v_d, v_t, ids, dummy, dummy, dummy, 4, max_m, 8,
                          dummy, ld_d, dummy, ld_t, dummy, dummy, dummy, dummy, dummy, dummy, dummy,
