@@ -279,8 +279,9 @@ int tt_retokenize_workspace_size(int32_t n_streams, int32_t max_m, size_t *bytes
  * target token starts with gets zero tokens (target_off[b+1] = target_off[b]), which
  * tt_align then treats as a sentinel pair.
  * workspace: tt_retokenize_workspace_size bytes, no initialisation; calls that
- * overlap in time must not share it.  Three kernels: one workgroup per stream, one
- * for the offsets, one to pack the ids.
+ * overlap in time must not share it.  Two kernels up to 2,048 streams (one workgroup
+ * per stream, then one that places and packs the ids), three beyond (the offsets get
+ * a kernel of their own).
  */
 int tt_retokenize(const tt_vocab *vd, const tt_vocab *vt, const void *vt_index, size_t index_bytes,
                   int32_t n_streams, const int32_t *draft_ids, const int32_t *draft_off,

@@ -5,8 +5,9 @@
 // collected with w = infinity).
 //
 // Two launches: a fill kernel clears the histogram (no memset node, so the call can be
-// captured in a HIP graph), then one 256-thread workgroup per group of pairs counts into an
-// LDS histogram and adds its non-zero bins to the global one with device-scope atomics.
+// captured in a HIP graph), then up to 256 workgroups of 256 threads count their pairs into
+// LDS histograms (one atomic per run of equal deviation in a thread's eight consecutive
+// cells) and add their non-zero bins to the global one with device-scope atomics.
 // The result does not depend on the order of the additions.
 #include "tt_internal.h"
 
@@ -14,7 +15,8 @@ namespace tt {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxGroups = 1024;
+constexpr int kMaxGroups = 256;  // one per compute unit: fewer global atomics on the shared bins
+constexpr int kRun = 8;           // consecutive path cells per thread
 
 __global__ void __launch_bounds__(kThreads) hist_clear(int32_t *hist, int n_bins) {
     for (int d = threadIdx.x; d < n_bins; d += kThreads) hist[d] = 0;
@@ -32,9 +34,22 @@ __global__ void __launch_bounds__(kThreads) delta_hist(int32_t n_pairs, const in
         const int n = path_len[b];
         if (n <= 0 || n > K + M) continue;  // sentinel pair, or a length the path area cannot hold
         const int32_t *cells = path + 2 * (int64_t)(draft_off[b] + target_off[b]);
-        for (int c = threadIdx.x; c < n; c += kThreads) {
-            const int dev = abs(cells[2 * c] - cells[2 * c + 1]);
-            atomicAdd(&sh_hist[dev < last ? dev : last], 1);
+        // kRun consecutive cells per thread: along a path i - j changes by at most one per
+        // step, so a thread's cells form few runs of equal deviation and it adds once per run
+        for (int c0 = threadIdx.x * kRun; c0 < n; c0 += kThreads * kRun) {
+            const int c1 = c0 + kRun < n ? c0 + kRun : n;
+            int cur = -1, cnt = 0;
+            for (int c = c0; c < c1; ++c) {
+                int dev = abs(cells[2 * c] - cells[2 * c + 1]);
+                dev = dev < last ? dev : last;
+                if (dev != cur) {
+                    if (cnt) atomicAdd(&sh_hist[cur], cnt);
+                    cur = dev;
+                    cnt = 0;
+                }
+                ++cnt;
+            }
+            if (cnt) atomicAdd(&sh_hist[cur], cnt);
         }
     }
     __syncthreads();

@@ -20,7 +20,9 @@
 //   3. one wave walks p -> p + L(p) from 0 with the L and token values of 64 positions
 //      held in its lanes (readlane per step), writing the emitted ids to LDS;
 //   4. the ids go to a padded per-stream area of the workspace with their count.
-// Then one workgroup turns the counts into CSR offsets and a copy kernel packs the ids.
+// Then the ids are packed into CSR order: up to 2,048 streams one kernel in which every
+// workgroup sums the counts before its stream; beyond, one workgroup scans the counts and a
+// copy kernel packs.
 #include "tt_internal.h"
 
 namespace tt {
@@ -32,6 +34,7 @@ constexpr int kThreads = 256;
 constexpr int kWave = 64;
 constexpr int kBatch = 8;  // candidate lengths probed together
 constexpr int kScanThreads = 1024;
+constexpr int kFoldStreams = 2048;  // up to this many streams the offsets are summed inside the pack kernel
 
 struct Slot {
     uint64_t key;  // first min(len, 8) bytes, little-endian, zero-padded
@@ -161,9 +164,9 @@ struct RetokParams {
 
 __global__ void __launch_bounds__(kThreads) retok_stream(RetokParams p) {
     extern __shared__ int32_t sh[];
-    // LDS: pos/out [max_bytes] | ids [max_bytes] | tok [max_bytes] | L (u8) | S (u8)
+    // LDS: pos/out [max_bytes] | src [max_bytes] | tok [max_bytes] | L (u8) | S (u8)
     int32_t *sh_pos = sh;                     // token offsets in S, later the emitted ids
-    int32_t *sh_ids = sh + p.max_bytes;       // draft ids
+    int32_t *sh_src = sh + p.max_bytes;       // byte offset of each draft token in vd.bytes
     int32_t *sh_tok = sh + 2 * p.max_bytes;   // longest-match token at each position
     uint8_t *sh_L = reinterpret_cast<uint8_t *>(sh + 3 * p.max_bytes);
     uint8_t *sh_S = sh_L + p.max_bytes;
@@ -189,10 +192,11 @@ __global__ void __launch_bounds__(kThreads) retok_stream(RetokParams p) {
                 if (id < 0 || id >= p.vd.n_tokens) {
                     sh_bad = 1;
                 } else {
-                    len = p.vd.offsets[id + 1] - p.vd.offsets[id];
+                    const int o = p.vd.offsets[id];
+                    len = p.vd.offsets[id + 1] - o;
                     if (len < 0) sh_bad = 1;
+                    sh_src[i] = o;
                 }
-                sh_ids[i] = id;
             }
             int tot;
             const int ex = block_exclusive_scan(len < 0 ? 0 : len, sh_w, &tot);
@@ -213,8 +217,7 @@ __global__ void __launch_bounds__(kThreads) retok_stream(RetokParams p) {
                 if (sh_pos[mid] <= x) lo = mid;
                 else hi = mid - 1;
             }
-            const int id = sh_ids[lo];
-            sh_S[x] = p.vd.bytes[p.vd.offsets[id] + (x - sh_pos[lo])];
+            sh_S[x] = p.vd.bytes[sh_src[lo] + (x - sh_pos[lo])];
         }
     }
     __syncthreads();
@@ -338,6 +341,28 @@ __global__ void __launch_bounds__(kThreads) retok_pack(RetokParams p) {
     for (int j = threadIdx.x; j < m; j += kThreads) p.target_ids[o + j] = p.ids[(int64_t)b * p.max_m + j];
 }
 
+// For batches up to kFoldStreams: stream b sums the counts before it itself (at most
+// kFoldStreams loads per workgroup), writes target_off[b] (and the total) and packs its ids,
+// so no separate offsets kernel runs.
+__global__ void __launch_bounds__(kThreads) retok_pack_fold(RetokParams p) {
+    __shared__ int sh_w[kThreads / kWave];
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    int part = 0;
+    for (int c = tid; c < b; c += kThreads) part += p.counts[c];
+    for (int d = kWave / 2; d > 0; d >>= 1) part += __shfl_xor(part, d);
+    if (lane == 0) sh_w[wave] = part;
+    __syncthreads();
+    int o = 0;
+    for (int w = 0; w < kThreads / kWave; ++w) o += sh_w[w];
+    const int m = p.counts[b];
+    if (tid == 0) {
+        p.target_off[b] = o;
+        if (b == p.n_streams - 1) p.target_off[b + 1] = o + m;
+    }
+    for (int j = tid; j < m; j += kThreads) p.target_ids[o + j] = p.ids[(int64_t)b * p.max_m + j];
+}
+
 inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
 }  // namespace
@@ -388,6 +413,10 @@ int launch_retokenize(const RetokArgs &a, hipStream_t stream) {
     if (a.n_streams > 0) {
         hipLaunchKernelGGL(retok_stream, dim3(a.n_streams), dim3(kThreads), retok_lds_bytes(a.max_bytes), stream, p);
         if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    }
+    if (a.n_streams > 0 && a.n_streams <= kFoldStreams) {
+        hipLaunchKernelGGL(retok_pack_fold, dim3(a.n_streams), dim3(kThreads), 0, stream, p);
+        return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
     }
     hipLaunchKernelGGL(retok_offsets, dim3(1), dim3(kScanThreads), 0, stream, p);  // target_off[0] = 0 at least
     if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;

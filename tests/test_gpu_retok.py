@@ -33,7 +33,7 @@ def run(vd, vt, idx, draft_ids, draft_off, max_bytes, max_m):
     return ids.cpu().numpy()[:off[-1]], off
 
 
-@pytest.mark.parametrize("index,n", [(1, None), (2, None), (3, None), (5, 128), (4, 96)])
+@pytest.mark.parametrize("index,n", [(1, None), (2, None), (3, None), (5, 128), (4, 96), (2, 2300)])
 def test_workload_batches(index, n):
     import paper_2510_15545_amd as tt
 
