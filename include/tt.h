@@ -72,7 +72,9 @@ typedef struct {
  * max_m <= 64 (each pair's working set stays in LDS), otherwise room for the
  * 2-bit predecessor codes of every pair's band (n_pairs * max_k *
  * (ceil(min(max_m, 2 L + 1) / 16) + 1) * 4 bytes, L the largest band half-width
- * the bounds allow).  Returns TT_EUNSUPPORTED when the bounds need more LDS than
+ * the bounds allow), rounded up to 256 bytes and followed, for 2 to 2,048 pairs, by
+ * one int per pair: the order in which the pairs are dispatched (descending band
+ * work, so the longest pairs start first).  Returns TT_EUNSUPPORTED when the bounds need more LDS than
  * one MI355X workgroup can hold (token bytes (max_k + max_m) * slot, the slot
  * being max_token_bytes rounded up to 8, 16, 32 or 64, plus
  * 9 * (max_k + max_m) + about 11 KB).

@@ -68,6 +68,10 @@ constexpr int band_threads() {
     return TB <= 16 ? 512 : 256;
 }
 constexpr int kChunk = 64;                       // sweep steps per cost chunk
+constexpr int kOrderThreads = 256;               // dispatch-order ranks: threads per workgroup
+constexpr int kOrderSplit = 4;                   // lanes counting one pair's rank
+constexpr int kOrderPairsPerGroup = kOrderThreads / kOrderSplit;
+constexpr int kOrderMax = 2048;                  // pairs it orders (11-bit index in the key); more keep their order
 constexpr int kGroups = kChunk / 4;              // cost dwords per lane and chunk
 constexpr int kCostStride = kGroups + 1;         // dwords per lane in a chunk buffer (odd: no bank conflicts)
 constexpr int kRowFront = 64;                    // row buffers hold columns -64 .. max_m + 135
@@ -284,11 +288,11 @@ __device__ __forceinline__ void sweep_chunk(Sweep &sw, const uint32_t *buf, cons
 template <int TB>
 __global__ void __launch_bounds__(band_threads<TB>()) __attribute__((amdgpu_waves_per_eu(band_threads<TB>() / 64)))
 dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
-                                                     int rw) {
+                                                     int rw, const int32_t *order) {
     constexpr int kThreads = band_threads<TB>();
     constexpr int kHelpers = kThreads - kWave;
     extern __shared__ __align__(16) uint8_t lds[];
-    const int b = blockIdx.x;
+    const int b = order != nullptr ? order[blockIdx.x] : (int)blockIdx.x;  // pairs in descending work
     const int tid = threadIdx.x, lane = tid % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: wave-level branches stay scalar
     const int d0 = a.draft_off[b], K = a.draft_off[b + 1] - d0;
@@ -516,20 +520,81 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
     }
 }
 
+// Dispatch order for the strip kernel: pairs by descending band work K * W (in units of 16
+// cells), ties by index.  Workgroups are handed to compute units in launch order, so the
+// longest pairs start first and the short ones fill in around them (on the 1,024 long pairs:
+// 393 us in generator order, about 254 us sorted).  Every 256-thread workgroup builds all n
+// 32-bit keys (work class, index) in LDS and ranks its own 64 pairs: a pair's slot is the number
+// of keys below its own, counted by four lanes over a quarter of the keys each with broadcast
+// LDS reads.
+__device__ __forceinline__ uint32_t order_key(const AlignArgs &a, int i) {
+    const int K = a.draft_off[i + 1] - a.draft_off[i], M = a.target_off[i + 1] - a.target_off[i];
+    uint32_t work = 0;
+    if (K >= 1 && K <= a.max_k && M >= 1 && M <= a.max_m) {
+        const int mx = K > M ? K : M;
+        int L = a.w < 0 ? mx : (a.w > abs(K - M) ? a.w : abs(K - M));
+        L = L < mx ? L : mx;
+        const int W = 2 * L + 1 < M ? 2 * L + 1 : M;
+        work = ((uint32_t)K * (uint32_t)W) >> 4;  // <= 4096 * 4096 / 16 = 2^20
+    }
+    work = work < 0xFFFFFu ? work : 0xFFFFFu;
+    return ((0xFFFFFu - work) << 11) | (uint32_t)i;  // 20 + 11 bits: unique for i < 2048
+}
+
+__global__ void __launch_bounds__(kOrderThreads) order_pairs(AlignArgs a, int32_t *order) {
+    __shared__ __align__(16) uint32_t keys[kOrderMax];
+    const int n = a.n_pairs;
+    const int n16 = (n + 15) & ~15;
+    for (int i = threadIdx.x; i < n16; i += kOrderThreads) keys[i] = i < n ? order_key(a, i) : ~0u;  // pad: never below a key
+    __syncthreads();
+    const uint4 *k4 = reinterpret_cast<const uint4 *>(keys);
+    // four lanes per pair, each counting a quarter of the keys; partial counts meet by shuffles
+    const int i = blockIdx.x * kOrderPairsPerGroup + (int)threadIdx.x / kOrderSplit;
+    const int part = threadIdx.x % kOrderSplit;
+    const uint32_t mine = i < n ? keys[i] : 0u;
+    const int quads = n16 >> 2;  // a multiple of 4
+    const int per = ((quads / kOrderSplit) + 3) & ~3;
+    const int q0 = part * per;
+    const int q1 = q0 + per < quads ? q0 + per : quads;
+    int r = 0;
+    for (int q = q0; q < q1; q += 4) {  // every lane of a quarter reads the same 16 keys
+        uint4 k[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) k[u] = q + u < q1 ? k4[q + u] : make_uint4(~0u, ~0u, ~0u, ~0u);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) r += (k[u].x < mine) + (k[u].y < mine) + (k[u].z < mine) + (k[u].w < mine);
+    }
+    r += __shfl_xor(r, 1);
+    r += __shfl_xor(r, 2);
+    if (i < n && part == 0) order[r] = i;
+}
+
+inline size_t order_offset(size_t code_words) { return (4 * code_words + 255) & ~size_t(255); }
+
 template <int TB>
 int launch_tb(const AlignArgs &a, void *workspace, size_t workspace_bytes, hipStream_t stream) {
     const LdsPlan lp = plan_lds(a.max_k, a.max_m, a.w, TB);
     if (lp.total > kLdsLimit) return TT_EUNSUPPORTED;
     const int rw = row_words_bound(a.max_k, a.max_m, a.w);
     const size_t stride = (size_t)a.max_k * (size_t)rw;  // code words per pair
-    if (workspace == nullptr || workspace_bytes < 4 * stride * (size_t)a.n_pairs) return TT_EWORKSPACE;
+    const bool sorted = a.n_pairs >= 2 && a.n_pairs <= kOrderMax;
+    const size_t need = sorted ? order_offset(stride * (size_t)a.n_pairs) + 4 * (size_t)a.n_pairs
+                               : 4 * stride * (size_t)a.n_pairs;
+    if (workspace == nullptr || workspace_bytes < need) return TT_EWORKSPACE;
+    int32_t *order = nullptr;
+    if (sorted) {
+        order = reinterpret_cast<int32_t *>(static_cast<uint8_t *>(workspace) + order_offset(stride * (size_t)a.n_pairs));
+        hipLaunchKernelGGL(order_pairs, dim3((a.n_pairs + kOrderPairsPerGroup - 1) / kOrderPairsPerGroup),
+                           dim3(kOrderThreads), 0, stream, a, order);
+        if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    }
     if (lp.total > 64 * 1024) {
         if (hipFuncSetAttribute(reinterpret_cast<const void *>(&dtw_band<TB>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lp.total) != hipSuccess)
             return TT_ELAUNCH;
     }
     hipLaunchKernelGGL(dtw_band<TB>, dim3(a.n_pairs), dim3(band_threads<TB>()), lp.total, stream, a, lp,
-                       static_cast<uint32_t *>(workspace), stride, rw);
+                       static_cast<uint32_t *>(workspace), stride, rw, order);
     return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
 }
 
@@ -551,7 +616,9 @@ size_t align_lds_bytes(int32_t max_k, int32_t max_m, int32_t w, int tb) {
 
 size_t align_workspace_bytes(int32_t n_pairs, int32_t max_k, int32_t max_m, int32_t w) {
     if (TT_ALIGN_ROWS && align_rows_fits(max_k, max_m)) return 0;
-    return 4 * (size_t)n_pairs * (size_t)max_k * (size_t)row_words_bound(max_k, max_m, w);
+    const size_t words = (size_t)n_pairs * (size_t)max_k * (size_t)row_words_bound(max_k, max_m, w);
+    if (n_pairs >= 2 && n_pairs <= kOrderMax) return order_offset(words) + 4 * (size_t)n_pairs;
+    return 4 * words;
 }
 
 int launch_align(const AlignArgs &a, void *workspace, size_t workspace_bytes, hipStream_t stream) {

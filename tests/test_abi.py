@@ -40,12 +40,19 @@ def test_workspace_sizes_are_host_computed():
     assert n.value >= 256 * (8 + 4) + 256 * 149 * 8
     assert L.tt_verify_workspace_size(-1, 10, ctypes.byref(n)) == tt.TT_EINVAL
     assert L.tt_align_workspace_size(256, 8, 64, 8, 8, ctypes.byref(n)) == 0 and n.value == 0
+    def strip_ws(pairs, words_per_pair):  # 2-bit codes, then the dispatch order (one int per pair)
+        return ((4 * pairs * words_per_pair + 255) // 256) * 256 + 4 * pairs
+
     assert L.tt_align_workspace_size(1024, 512, 512, 8, 8, ctypes.byref(n)) == 0
-    assert n.value == 1024 * 512 * 33 * 4  # 2-bit codes for a 512-wide band row starting mid-word
+    assert n.value == strip_ws(1024, 512 * 33)  # 2-bit codes for a 512-wide band row starting mid-word
     assert L.tt_align_workspace_size(8, 4096, 4096, -1, 8, ctypes.byref(n)) == 0
-    assert n.value == 8 * 4096 * 257 * 4
+    assert n.value == strip_ws(8, 4096 * 257)
     # short pairs in a batch with one long target still take the strip kernel's workspace
-    assert L.tt_align_workspace_size(4, 8, 100, 8, 8, ctypes.byref(n)) == 0 and n.value == 4 * 8 * 8 * 4
+    assert L.tt_align_workspace_size(4, 8, 100, 8, 8, ctypes.byref(n)) == 0 and n.value == strip_ws(4, 8 * 8)
+    # one pair needs no dispatch order; above 2,048 pairs the order is not sorted
+    assert L.tt_align_workspace_size(1, 8, 100, 8, 8, ctypes.byref(n)) == 0 and n.value == 8 * 8 * 4
+    assert L.tt_align_workspace_size(2049, 8, 100, 8, 8, ctypes.byref(n)) == 0 and n.value == 2049 * 8 * 8 * 4
+    assert L.tt_align_workspace_size(2048, 8, 100, 8, 8, ctypes.byref(n)) == 0 and n.value == strip_ws(2048, 64)
     assert L.tt_align_workspace_size(8, 4096, 4096, -1, 16, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
     assert L.tt_align_workspace_size(8, 16, 16, 8, 65, ctypes.byref(n)) == tt.TT_EUNSUPPORTED
     # tt_step shares one workspace between its stages: the larger of the two
