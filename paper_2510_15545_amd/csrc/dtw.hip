@@ -407,32 +407,32 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
         int r = rtop;
         for (; r >= i0; --r) {
             const int rr = r - i0;
-            const int kr0 = (g.jlo(r) - jf + rr) >> 4;
-            const int te = e - jf + rr;  // sweep step of the entry cell
+            const int kr0 = (g.jlo(r) - jf + rr) >> 4;  // the row's first code word, in strip steps / 16
+            const int te = e - jf + rr;                 // sweep step of the entry cell
             int k = (te >> 4) - kr0;
-            if (k < 0 || k >= rw) {  // never: the entry column lies inside the row's band
-                more = false;
-                break;
-            }
+            // the checks below never fire on codes the sweep wrote (the entry column lies inside
+            // the row's band, and the band's first cell is not a left move); they are folded into
+            // one flag so the walk's dependent chain has a single branch per row
+            int bad = (uint32_t)k >= (uint32_t)rw ? 1 : 0;
+            k = bad ? 0 : k;
             uint32_t w = __builtin_amdgcn_readfirstlane(word(rr, k));
             // cells whose move is not (i, j-1), at steps <= te
             uint32_t m = ~w & 0x55555555u & (0xFFFFFFFFu << (30 - 2 * (te & 15)));
-            while (m == 0u && k > 0) {  // the run continues into the word below
-                --k;
-                w = __builtin_amdgcn_readfirstlane(word(rr, k));
-                m = ~w & 0x55555555u;
+            if (m == 0u) {
+                while (m == 0u && k > 0) {  // the run continues into the word below
+                    --k;
+                    w = __builtin_amdgcn_readfirstlane(word(rr, k));
+                    m = ~w & 0x55555555u;
+                }
+                bad |= m == 0u ? 1 : 0;
             }
-            if (m == 0u) {  // never: the band's first cell is not a left move
-                more = false;
-                break;
-            }
-            const int pos = __builtin_ctz(m);
+            const int pos = m != 0u ? __builtin_ctz(m) : 0;
             const int x = jf + 16 * (kr0 + k) + ((30 - pos) >> 1) - rr;
             rec = lane == rr ? (((uint32_t)x << 16) | (uint32_t)e) : rec;
-            e = ((w >> (pos + 1)) & 1u) ? x : x - 1;
-            if (e < 1 || r == 1) {
+            e = x - (int)((~w >> (pos + 1)) & 1u);  // x after an (i-1, j) move, x - 1 after a diagonal
+            if ((bad | (e < 1 ? 1 : 0) | (r == 1 ? 1 : 0)) != 0) {
                 more = false;
-                --r;
+                r -= bad ? 0 : 1;  // a bad row is not on the path; otherwise this row was the last
                 break;
             }
         }
