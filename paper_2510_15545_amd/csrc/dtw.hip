@@ -394,6 +394,7 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
     // the highest column x <= e whose move is not (i, j-1); it enters row i-1 at x - 1
     // after a diagonal move and at x after an (i-1, j) move
     __builtin_amdgcn_s_waitcnt(0);  // wave 0's code-word stores are complete before they are read back
+    const int cost_km = wave == 0 ? rowIn[M] : 0;  // C(K, M), read before the row buffers are reused
     int e = M;      // entry column of the row being walked (uniform over wave 0)
     int first = 1;  // first row on the path
     // Wave 0 walks rows rtop down to i0 of one strip with uniform (scalar) state; word(rr, k)
@@ -441,7 +442,150 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
         if (!more) first = r + 1;
         return more;
     };
-    if (rw <= kWave) {
+    // One row of the walk for any row r (the code words' step numbering is that of the 64-row
+    // strip holding r): entry column e, the row's code words at rowwords; returns the entry
+    // column of row r - 1 and the row's run record, and raises bad on codes the sweep cannot
+    // have written (see walk_strip).
+    auto row_step = [&](int r, int ein, const uint32_t *rowwords, uint32_t &rec_out, int &bad) -> int {
+        const int i0s = 1 + ((r - 1) & ~(kWave - 1));
+        const int rr = r - i0s;
+        const int jf = g.jlo(i0s);
+        const int kr0 = (g.jlo(r) - jf + rr) >> 4;
+        const int te = ein - jf + rr;
+        int k = (te >> 4) - kr0;
+        bad = (uint32_t)k >= (uint32_t)rw ? 1 : 0;
+        k = bad ? 0 : k;
+        uint32_t w = __builtin_amdgcn_readfirstlane(rowwords[k]);
+        uint32_t m = ~w & 0x55555555u & (0xFFFFFFFFu << (30 - 2 * (te & 15)));
+        if (m == 0u) {
+            while (m == 0u && k > 0) {
+                --k;
+                w = __builtin_amdgcn_readfirstlane(rowwords[k]);
+                m = ~w & 0x55555555u;
+            }
+            bad |= m == 0u ? 1 : 0;
+        }
+        const int pos = m != 0u ? __builtin_ctz(m) : 0;
+        const int x = jf + 16 * (kr0 + k) + ((30 - pos) >> 1) - rr;
+        rec_out = ((uint32_t)x << 16) | (uint32_t)ein;
+        return x - (int)((~w >> (pos + 1)) & 1u);
+    };
+    // Segment-parallel walk (code words of up to 64 rows per segment staged in LDS): the rows
+    // are cut into segments of kSeg; a group of segments is staged into the LDS the sweep no
+    // longer needs (token tables, row buffers, distance buffers), and every wave walks one
+    // segment at the same time, the topmost from its known entry column and the others from a
+    // guess on the line from (1, 1) to (K, M), recording each row's entry column (in poff) and
+    // run (in seg).  Wave 0 then corrects the segments top-down: entering a segment at its true
+    // column it re-walks rows only until its entry column meets the recorded one; from there the
+    // recorded walk is the true walk, because a row's exit depends only on its entry column.
+    // Optimal paths from nearby columns merge within a few rows, so the correction is short.
+    constexpr int kSeg = 32;
+    constexpr int kWaves = kThreads / kWave;
+    uint32_t *scr = reinterpret_cast<uint32_t *>(lds + lp.tslot);
+    const int scr_words = (int)((lp.path - lp.tslot) / 4);
+    int par = scr_words / (kSeg * rw);
+    par = par < kWaves ? par : kWaves;
+    __shared__ int s_exit[kWaves], s_more, s_first, s_etrue;
+    if (rw <= kWave && par >= 2 && K > kSeg) {
+        const int nseg = (K + kSeg - 1) / kSeg;
+        if (tid == 0) {
+            s_more = 1;
+            s_first = 1;
+            s_etrue = M;
+        }
+        for (int top = nseg - 1; top >= 0; top -= par) {
+            __syncthreads();  // s_more / s_etrue published; the previous group's buffers are free
+            if (!s_more) break;  // uniform
+            const int nsg = top + 1 < par ? top + 1 : par;
+            const int sg = top - wave;  // this wave's segment
+            const int lo = sg * kSeg + 1;
+            const int hi = (lo + kSeg - 1) < K ? (lo + kSeg - 1) : K;
+            uint32_t *buf = scr + wave * kSeg * rw;
+            if (wave < nsg) {
+                const uint32_t *src = parked + (size_t)(lo - 1) * rw;
+                for (int q = lane; q < (hi - lo + 1) * rw; q += kWave) buf[q] = src[q];
+            }
+            __syncthreads();
+            if (wave < nsg) {  // speculative walk of the segment, uniform state per wave
+                int ew;
+                if (wave == 0) {
+                    ew = s_etrue;
+                } else {  // the line from (1, 1) to (K, M), clamped into row hi's band
+                    ew = 1 + (int)(((long long)(hi - 1) * (M - 1)) / (K - 1));
+                    ew = ew < g.jlo(hi) ? g.jlo(hi) : (ew > g.jhi(hi) ? g.jhi(hi) : ew);
+                }
+                uint32_t rec = 0, ent = 0;
+                int badw = 0;
+                for (int r = hi; r >= lo; --r) {
+                    uint32_t rc;
+                    int bad;
+                    const int en = row_step(r, ew, buf + (r - lo) * rw, rc, bad);
+                    ent = lane == r - lo ? (uint32_t)ew : ent;
+                    rec = lane == r - lo ? rc : rec;
+                    if (bad) {
+                        badw = 1;
+                        break;
+                    }
+                    ew = en;
+                    if (r == 1) break;
+                }
+                if (lane < hi - lo + 1) {
+                    seg[lo - 1 + lane] = rec;
+                    poff[lo - 1 + lane] = badw ? 0xFFFFFFFFu : ent;  // never an entry column: forces a re-walk
+                }
+                if (lane == 0) s_exit[wave] = ew;
+            }
+            __syncthreads();
+            if (wave == 0) {  // corrections, top-down
+                int et = s_etrue;
+                bool more = true;
+                int fst = 1;
+                for (int w = 0; w < nsg && more; ++w) {
+                    const int lo2 = (top - w) * kSeg + 1;
+                    const int hi2 = (lo2 + kSeg - 1) < K ? (lo2 + kSeg - 1) : K;
+                    const uint32_t *b2 = scr + w * kSeg * rw;
+                    bool met = false;
+                    for (int r = hi2; r >= lo2; --r) {
+                        if ((uint32_t)et == poff[r - 1]) {  // the recorded walk is the true walk from here
+                            met = true;
+                            break;
+                        }
+                        uint32_t rc;
+                        int bad;
+                        const int en = row_step(r, et, b2 + (r - lo2) * rw, rc, bad);
+                        if (bad) {  // as in walk_strip: row r is not on the path
+                            more = false;
+                            fst = r + 1;
+                            break;
+                        }
+                        if (lane == 0) {
+                            seg[r - 1] = rc;
+                            poff[r - 1] = (uint32_t)et;
+                        }
+                        et = en;
+                        if (et < 1 || r == 1) {
+                            more = false;
+                            fst = r;
+                            break;
+                        }
+                    }
+                    if (met) {
+                        et = s_exit[w];
+                        if (lo2 == 1) more = false;  // the recorded walk reached row 1
+                    } else if (more && lo2 == 1) {
+                        more = false;
+                    }
+                }
+                if (lane == 0) {
+                    s_etrue = et;
+                    s_more = more ? 1 : 0;
+                    if (!more) s_first = fst;
+                }
+            }
+        }
+        __syncthreads();
+        first = s_first;
+    } else if (rw <= kWave) {
         // each strip's code words are staged into the freed cost buffers by the other waves
         // while wave 0 walks the strip below it in the other half
         uint32_t *stg = costbuf;
@@ -476,7 +620,7 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
         }
     }
     if (wave == 0) {
-        if (lane == 0) a.cost[b] = rowIn[M];  // C(K, M), from the last strip's last row
+        if (lane == 0) a.cost[b] = cost_km;  // C(K, M), from the last strip's last row
         // rows first..K are on the path: path offsets
         int carry = 0;
         for (int r0 = first - 1; r0 < K; r0 += kWave) {
