@@ -224,3 +224,26 @@ def test_empty_batch_and_argument_errors():
     assert nacc.numel() == 0 and tok.numel() == 0
     with pytest.raises(tt.TTError):
         tt.verify(8, e, torch.zeros(2, dtype=torch.int32, device="cuda"), f, P, f, f, -1)
+
+
+@pytest.mark.parametrize("w", [-1, 0, 3, 8])
+def test_strip_walk_segment_and_group_boundaries(w):
+    """Pairs whose row counts sit on and around the 32-row segments and 64-row strips of the
+    strip kernel's backtrack (segments walked in parallel from guessed columns, then corrected),
+    with several band widths, some pairs far off the diagonal: bit-exact against the oracle."""
+    print(f"[case] strip walk boundaries w={w}", flush=True)
+    rng = np.random.default_rng(100 + w)
+    toks = random_tokens(rng, 120, 1, 6, alphabet=b"abcdefgh")
+    v = vocab_of(toks)
+    ks = [31, 32, 33, 63, 64, 65, 95, 96, 97, 128, 200, 257, 300]
+    pairs = []
+    for k in ks:
+        for m in (max(1, k // 3), k, k + 37, 2 * k):
+            d = list(rng.integers(0, len(toks), k))
+            # targets that share long stretches with the drafts (paths near the diagonal) or not
+            t = (d[:m] + list(rng.integers(0, len(toks), max(0, m - k)))) if rng.random() < 0.5 else \
+                list(rng.integers(0, len(toks), m))
+            pairs.append((d, t))
+    wl = workload(v, v, pairs, len(toks), len(toks), w=w, probs=False)
+    g = gpu_run(wl, w=w)
+    compare_align(wl, g, oracle_run(wl, w=w))
