@@ -307,8 +307,9 @@ int tt_step_workspace_size(int32_t n_streams, int32_t v_t, int32_t max_k, int32_
  * both stages).  Sec. 4.1 / Alg. 1 / App. H (alignment), Alg. 2 / App. A.2
  * (transfer), Sec. 3, Sec. 4.2.2-4.2.3, App. D Alg. 4 (verification).
  *
- * When max_k <= 64, max_m <= 64, n_streams >= 256 and the verify rows have at
- * most 8M floats, the path runs as ONE kernel with a workgroup per stream: the
+ * When max_k <= 64, max_m <= 64, and either n_streams >= 256 with verify rows of
+ * at most 8M floats or v_t <= 16384 (short rows, any batch size), the path runs as
+ * ONE kernel with a workgroup per stream: the
  * pair is aligned in LDS, map and q never leave the chip before they are used,
  * and the selected target row is read once.  Otherwise it issues the three
  * calls' kernels in order.  Every output array (cost, path_len, path, map, q,
