@@ -247,3 +247,42 @@ def test_strip_walk_segment_and_group_boundaries(w):
     wl = workload(v, v, pairs, len(toks), len(toks), w=w, probs=False)
     g = gpu_run(wl, w=w)
     compare_align(wl, g, oracle_run(wl, w=w))
+
+
+@pytest.mark.parametrize("n,V,dense", [(256, 300_000, False), (3, 9_000_000, False), (256, 300_000, True)])
+def test_large_vocabularies(n, V, dense):
+    """Rows past 256 chunks (the sampler's chunk sums no longer fit four per lane) on the
+    one-workgroup-per-stream path, and rows past 8M floats (over the row path's LDS) on the
+    split path; one-hot and dense proposals, bit-exact against the oracle."""
+    import torch
+
+    import oracle
+    import paper_2510_15545_amd as tt
+
+    print(f"[case] large vocabulary n={n} V={V} dense={dense}", flush=True)
+    rng = np.random.default_rng(V + n)
+    Ms = rng.integers(0, 3, n)
+    off = np.zeros(n + 1, np.int32)
+    off[1:] = np.cumsum(Ms)
+    nt = int(off[-1])
+    ids = rng.integers(0, V, nt).astype(np.int32)
+    rows = rng.random((nt + n, V), dtype=np.float32)
+    rows /= rows.sum(axis=1, keepdims=True, dtype=np.float32)
+    ids[::3] = np.argmax(rows[(off[:-1] + np.arange(n))[np.repeat(np.arange(n), Ms)][::3]], axis=1)  # likely accepts
+    ua = (rng.integers(0, 1 << 24, nt) * 2.0**-24).astype(np.float32)
+    us = (rng.integers(0, 1 << 24, n) * 2.0**-24).astype(np.float32)
+    us[0] = np.float32(1 - 2**-24)
+    P = to_dev(rows)
+    if dense:
+        qrows = rng.random((max(1, nt), V), dtype=np.float32)
+        qrows /= qrows.sum(axis=1, keepdims=True, dtype=np.float32)
+        o_nacc, o_tok, _, _ = oracle.sd_verify(V, ids, off, qrows[:nt], rows, ua, us)
+        nacc, tok, _ = tt.verify_dense(V, to_dev(ids), to_dev(off), to_dev(qrows), P, to_dev(ua), to_dev(us), 2)
+    else:
+        q = rng.random(nt).astype(np.float32) * np.float32(1e-5)
+        o_nacc, o_tok, _, _ = oracle.verify(V, ids, off, q, rows, ua, us)
+        nacc, tok, _ = tt.verify(V, to_dev(ids), to_dev(off), to_dev(q), P, to_dev(ua), to_dev(us), 2)
+    torch.cuda.synchronize()
+    assert np.array_equal(nacc.cpu().numpy(), o_nacc)
+    assert np.array_equal(tok.cpu().numpy(), o_tok)
+    assert 0 < (o_nacc < Ms).sum() or n < 8
