@@ -311,8 +311,10 @@ int tt_step_workspace_size(int32_t n_streams, int32_t v_t, int32_t max_k, int32_
  * at most 8M floats or v_t <= 16384 (short rows, any batch size), the path runs as
  * ONE kernel with a workgroup per stream: the
  * pair is aligned in LDS, map and q never leave the chip before they are used,
- * and the selected target row is read once.  Otherwise it issues the three
- * calls' kernels in order.  Every output array (cost, path_len, path, map, q,
+ * and the selected target row is read once.  Other batches of pairs with
+ * K, M <= 64 run that kernel up to the acceptance scan (alignment, transfer, gamma)
+ * followed by the split verification kernels of tt_verify; larger pairs issue the
+ * three calls' kernels in order.  Every output array (cost, path_len, path, map, q,
  * n_accepted, out_token, residual) is written exactly as by the three calls.
  * workspace: tt_step_workspace_size bytes, no initialisation needed.
  */

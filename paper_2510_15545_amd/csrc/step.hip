@@ -36,7 +36,9 @@ struct SParams {
     int32_t nc, vec4;
 };
 
-template <int TB>
+// STREAM = false: the kernel stops once gamma is known and leaves it in rsel for the split
+// verification kernels (batches of long rows too small to fill the chip one stream per CU).
+template <int TB, bool STREAM>
 __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     const AlignArgs &al = p.s.al;
     const TransferArgs &tr = p.s.tr;
@@ -144,6 +146,11 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
         return;
     }
 
+    if (!STREAM) {
+        if (tid == 0) p.rsel[b] = sh_gamma;
+        return;
+    }
+
     // ---- 4. stream the selected row once, then sample
     const int r = sh_gamma, rtok = sh_rtok;
     const float rq = sh_rq;
@@ -164,10 +171,31 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     }
 }
 
-template <int TB>
+template <int TB, bool STREAM>
 int launch_tb(const SParams &p, size_t lds, hipStream_t stream) {
-    hipLaunchKernelGGL(step_fused<TB>, dim3(p.s.ve.n_streams), dim3(kThreads), lds, stream, p);
+    hipLaunchKernelGGL((step_fused<TB, STREAM>), dim3(p.s.ve.n_streams), dim3(kThreads), lds, stream, p);
     return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+}
+
+template <bool STREAM>
+int launch_any_tb(const SParams &p, int tb, size_t lds, hipStream_t stream) {
+    switch (tb) {
+        case 8: return launch_tb<8, STREAM>(p, lds, stream);
+        case 16: return launch_tb<16, STREAM>(p, lds, stream);
+        case 32: return launch_tb<32, STREAM>(p, lds, stream);
+        default: return launch_tb<64, STREAM>(p, lds, stream);
+    }
+}
+
+SParams make_sparams(const StepArgs &s, const VerifyLayout &L) {
+    uint8_t *ws = static_cast<uint8_t *>(s.ve.workspace);
+    SParams p;
+    p.s = s;
+    p.zsum = reinterpret_cast<uint64_t *>(ws + L.zsum);
+    p.rsel = reinterpret_cast<int32_t *>(ws + L.rsel);
+    p.nc = L.n_chunks;
+    p.vec4 = ((reinterpret_cast<uintptr_t>(s.ve.target_probs) & 15u) == 0 && (s.ve.target_ld % 4) == 0) ? 1 : 0;
+    return p;
 }
 
 }  // namespace
@@ -189,23 +217,25 @@ int launch_step_fused(const StepArgs &s, int tb, hipStream_t stream) {
     if (!step_fused_fits(s, tb)) return TT_EUNSUPPORTED;
     const VerifyLayout L = verify_layout(s.ve.n_streams, s.ve.v_t);
     if (s.ve.workspace == nullptr || s.ve.workspace_bytes < L.total) return TT_EWORKSPACE;
-    uint8_t *ws = static_cast<uint8_t *>(s.ve.workspace);
-    SParams p;
-    p.s = s;
-    p.zsum = reinterpret_cast<uint64_t *>(ws + L.zsum);
-    p.rsel = reinterpret_cast<int32_t *>(ws + L.rsel);
-    p.nc = L.n_chunks;
-    p.vec4 = ((reinterpret_cast<uintptr_t>(s.ve.target_probs) & 15u) == 0 && (s.ve.target_ld % 4) == 0) ? 1 : 0;
-    const size_t lds = 8 * (size_t)p.nc;
-    int st;
-    switch (tb) {
-        case 8: st = launch_tb<8>(p, lds, stream); break;
-        case 16: st = launch_tb<16>(p, lds, stream); break;
-        case 32: st = launch_tb<32>(p, lds, stream); break;
-        default: st = launch_tb<64>(p, lds, stream); break;
-    }
+    const SParams p = make_sparams(s, L);
+    const int st = launch_any_tb<true>(p, tb, 8 * (size_t)p.nc, stream);
     if (st != TT_OK) return st;
     return s.ve.residual != nullptr ? launch_verify_residual(s.ve, stream) : TT_OK;
+}
+
+bool step_front_fits(const StepArgs &s, int tb) {
+    return (tb == 8 || tb == 16 || tb == 32 || tb == 64) && align_rows_fits(s.al.max_k, s.al.max_m) &&
+           s.ve.max_m <= rows::kMaxSide;
+}
+
+int launch_step_front(const StepArgs &s, int tb, hipStream_t stream) {
+    if (!step_front_fits(s, tb)) return TT_EUNSUPPORTED;
+    const VerifyLayout L = verify_layout(s.ve.n_streams, s.ve.v_t);
+    if (s.ve.workspace == nullptr || s.ve.workspace_bytes < L.total) return TT_EWORKSPACE;
+    const SParams p = make_sparams(s, L);
+    const int st = launch_any_tb<false>(p, tb, 0, stream);
+    if (st != TT_OK) return st;
+    return launch_verify_after_gamma(s.ve, stream);
 }
 
 }  // namespace tt

@@ -291,6 +291,7 @@ int tt_step(const tt_vocab *vd, const tt_vocab *vt, int32_t n_streams, int32_t v
     s.ve.workspace_bytes = workspace_bytes;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (TT_STEP_FUSED && tt::step_fused_fits(s, tb)) return tt::launch_step_fused(s, tb, st);
+    if (TT_STEP_FUSED && tt::step_front_fits(s, tb)) return tt::launch_step_front(s, tb, st);
     int rc = tt::launch_align(s.al, workspace, workspace_bytes, st);
     if (rc == TT_OK) rc = tt::launch_transfer(s.tr, st);
     if (rc == TT_OK) rc = tt::launch_verify(s.ve, st);

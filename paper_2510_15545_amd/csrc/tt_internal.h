@@ -71,6 +71,9 @@ int launch_verify(const VerifyArgs &a, hipStream_t stream);  // one-hot or dense
 bool verify_row_path(int32_t n_streams, int32_t v_t);
 // Normalised residual rows from Z and r in the workspace (written by a previous launch).
 int launch_verify_residual(const VerifyArgs &a, hipStream_t stream);
+// The split path's streaming and sampling for the one-hot proposal with gamma already in the
+// workspace (rsel, -1 for sentinel streams whose outputs are written), then the residual rows.
+int launch_verify_after_gamma(const VerifyArgs &a, hipStream_t stream);
 
 // ---------------------------------------------------------------- deviation histogram (delta.hip)
 int launch_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
@@ -104,5 +107,9 @@ struct StepArgs {
 // and the one-workgroup-per-stream verification; TT_EUNSUPPORTED otherwise.
 bool step_fused_fits(const StepArgs &s, int tb);
 int launch_step_fused(const StepArgs &s, int tb, hipStream_t stream);
+// Otherwise, when the pairs fit the row-scan alignment: the same kernel up to gamma (alignment,
+// transfer, acceptance) and the split verification path after it.
+bool step_front_fits(const StepArgs &s, int tb);
+int launch_step_front(const StepArgs &s, int tb, hipStream_t stream);
 
 }  // namespace tt

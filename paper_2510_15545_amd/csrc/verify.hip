@@ -162,7 +162,9 @@ __global__ void __launch_bounds__(kRowThreads) verify_row(VParams p) {
 }
 
 // ------------------------------------------------------------------ split path
-template <bool DENSE>
+// GIVEN: gamma was found by an earlier kernel of the same call (the fused step's front) and
+// is read from rsel (-1: a sentinel stream whose outputs are already written).
+template <bool DENSE, bool GIVEN>
 __global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
     const VerifyArgs &a = p.a;
     const int G = gridDim.x;
@@ -176,7 +178,13 @@ __global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
 
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
-    if (wave == 0) {  // every workgroup of the stream recomputes gamma
+    if (GIVEN) {
+        const int r = p.rsel[b];
+        if (tid == 0) {
+            sh_gamma = r;
+            sh_ok = r >= 0 ? 1 : 0;
+        }
+    } else if (wave == 0) {  // every workgroup of the stream recomputes gamma
         int gamma;
         const bool ok = accept_scan<DENSE>(a, b, t0, M, lane, gamma);
         if (lane == 0) {
@@ -186,7 +194,7 @@ __global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
     }
     __syncthreads();
     if (!sh_ok) {
-        if (s == 0 && tid == 0) {
+        if (!GIVEN && s == 0 && tid == 0) {
             a.n_accepted[b] = -1;
             a.out_token[b] = -1;
             p.rsel[b] = -1;
@@ -194,7 +202,7 @@ __global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
         return;
     }
     const int r = sh_gamma;
-    if (s == 0 && tid == 0) p.rsel[b] = r;
+    if (!GIVEN && s == 0 && tid == 0) p.rsel[b] = r;
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
     const Proposal pr = proposal<DENSE>(a, t0, M, r);
     const int c0 = s * p.cpw;
@@ -309,29 +317,34 @@ int launch_residual(const VParams &p, hipStream_t stream) {
     return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
 }
 
+// Split path: the streaming kernel over B x S workgroups, then one sampling wave per stream.
+template <bool DENSE, bool GIVEN>
+int launch_split(VParams &p, hipStream_t stream) {
+    const VerifyArgs &a = p.a;
+    // splits per stream: aim for TT_VERIFY_TARGET_WG workgroups, at least one chunk per wave
+    constexpr int kWaves = kSplitThreads / kWave;
+    int max_splits = (p.nc + kWaves - 1) / kWaves;
+    int splits = (TT_VERIFY_TARGET_WG + a.n_streams - 1) / a.n_streams;
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    p.cpw = (p.nc + splits - 1) / splits;
+    p.splits = (p.nc + p.cpw - 1) / p.cpw;
+    p.work_items = a.n_streams * p.splits;
+    const int grid = ((p.work_items + kXcds - 1) / kXcds) * kXcds;
+    hipLaunchKernelGGL((verify_stream<DENSE, GIVEN>), dim3(grid), dim3(kSplitThreads), 0, stream, p);
+    if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    hipLaunchKernelGGL(verify_sample<DENSE>, dim3(a.n_streams), dim3(kWave), 0, stream, p);
+    return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+}
+
 template <bool DENSE>
 int launch_verify_kernels(VParams &p, hipStream_t stream) {
     const VerifyArgs &a = p.a;
     if (verify_row_path(a.n_streams, a.v_t)) {
         hipLaunchKernelGGL(verify_row<DENSE>, dim3(a.n_streams), dim3(kRowThreads), 8 * (size_t)p.nc, stream, p);
-        if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
-    } else {
-        // splits per stream: aim for TT_VERIFY_TARGET_WG workgroups, at least one chunk per wave
-        constexpr int kWaves = kSplitThreads / kWave;
-        int max_splits = (p.nc + kWaves - 1) / kWaves;
-        int splits = (TT_VERIFY_TARGET_WG + a.n_streams - 1) / a.n_streams;
-        if (splits > max_splits) splits = max_splits;
-        if (splits < 1) splits = 1;
-        p.cpw = (p.nc + splits - 1) / splits;
-        p.splits = (p.nc + p.cpw - 1) / p.cpw;
-        p.work_items = a.n_streams * p.splits;
-        const int grid = ((p.work_items + kXcds - 1) / kXcds) * kXcds;
-        hipLaunchKernelGGL(verify_stream<DENSE>, dim3(grid), dim3(kSplitThreads), 0, stream, p);
-        if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
-        hipLaunchKernelGGL(verify_sample<DENSE>, dim3(a.n_streams), dim3(kWave), 0, stream, p);
-        if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+        return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
     }
-    return TT_OK;
+    return launch_split<DENSE, false>(p, stream);
 }
 
 }  // namespace
@@ -341,6 +354,14 @@ int launch_verify_residual(const VerifyArgs &a, hipStream_t stream) {
     return launch_residual(make_params(a), stream);
 }
 
+
+int launch_verify_after_gamma(const VerifyArgs &a, hipStream_t stream) {
+    if (a.workspace == nullptr || a.workspace_bytes < verify_layout(a.n_streams, a.v_t).total) return TT_EWORKSPACE;
+    VParams p = make_params(a);
+    const int st = launch_split<false, true>(p, stream);
+    if (st != TT_OK) return st;
+    return a.residual != nullptr ? launch_residual(p, stream) : TT_OK;
+}
 
 int launch_verify(const VerifyArgs &a, hipStream_t stream) {
     if (a.workspace == nullptr || a.workspace_bytes < verify_layout(a.n_streams, a.v_t).total) return TT_EWORKSPACE;

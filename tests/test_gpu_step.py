@@ -67,8 +67,10 @@ def test_step_matches_three_calls_and_oracle(c, n):
         same_as_three_calls(wl, step_run(wl, d, w=w), gpu_run(wl, w=w, d=d))
 
 
-def test_step_sentinels_in_a_fused_batch():
-    """Invalid pairs and streams inside a batch large enough for the fused kernel."""
+@pytest.mark.parametrize("n,v_t", [(280, None), (40, 20_000)])
+def test_step_sentinels_in_a_fused_batch(n, v_t):
+    """Invalid pairs and streams inside a batch large enough for the fused kernel, and inside a
+    small batch of long rows (the fused front up to gamma, then the split verification)."""
     rng = np.random.default_rng(21)
     toks = random_tokens(rng, 300, 1, 6)
     v = vocab_of(toks)
@@ -82,10 +84,11 @@ def test_step_sentinels_in_a_fused_batch():
     pairs[12] = ([5, 6], [])                # M = 0: align sentinel, verify samples the bonus row
     pairs[13] = (list(range(1, 12)), [9])   # K above the bound below
     pairs[14] = ([1], list(range(1, 22)))   # M above the bound below
-    wl = workload(v, v, pairs, len(toks), len(toks), seed=3)
+    pairs = pairs[:n]
+    wl = workload(v, v, pairs, len(toks), v_t or len(toks), seed=3)
     d = upload(wl)
     for bounds in ((10, 20), (64, 64)):
-        print(f"[case] tt_step sentinels bounds={bounds}", flush=True)
+        print(f"[case] tt_step sentinels n={n} v_t={v_t} bounds={bounds}", flush=True)
         s = step_run(wl, d, bounds=bounds, residual=True)
         import copy
         wl2 = copy.copy(wl)
