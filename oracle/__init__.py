@@ -246,6 +246,78 @@ def retokenize(vd_bytes, vd_off, vt_bytes, vt_off, draft_ids, draft_off, max_m=N
     return np.array(out, np.int32), np.array(off, np.int32)
 
 
+def vocab_intersection(vd_bytes, vd_off, vt_bytes, vt_off, vd_max_bytes=None, vt_max_bytes=None):
+    """App. D Alg. 3 (TLI): the intersection of the draft and target vocabularies, each taken as
+    a set of byte strings.  Where several ids of one vocabulary share a string, the lowest id
+    stands for it and the others are outside the intersection; tokens of length 0 or longer
+    than the table's declared maximum are outside too.
+
+    Plain Python.  Returns (d2t int32[V_d], t2d int32[V_t]): d2t[x] is the target id of draft
+    id x's string when both sides have it, else -1; t2d is the converse."""
+    def table(data, off, max_bytes):
+        data = bytes(np.asarray(data, np.uint8))
+        off = np.asarray(off, np.int64)
+        first, strings = {}, []
+        for t in range(len(off) - 1):
+            s = data[off[t]:off[t + 1]]
+            ok = 0 < len(s) and (max_bytes is None or len(s) <= max_bytes)
+            strings.append(s if ok else None)
+            if ok and s not in first:  # ids ascend: the first holder is the lowest id
+                first[s] = t
+        return first, strings
+
+    fd, sd = table(vd_bytes, vd_off, vd_max_bytes)
+    ft, st = table(vt_bytes, vt_off, vt_max_bytes)
+    d2t = np.full(len(sd), -1, np.int32)
+    t2d = np.full(len(st), -1, np.int32)
+    for x, s in enumerate(sd):
+        if s is not None and fd[s] == x and s in ft:
+            d2t[x] = ft[s]
+            t2d[ft[s]] = x
+    return d2t, t2d
+
+
+def round_to_f32(num: int, scale_bits: int) -> np.float32:
+    """num * 2^-scale_bits (num >= 0 an exact integer) rounded once to the nearest fp32, ties
+    to even (normal results only, which is all tli_proposal produces)."""
+    if num == 0:
+        return np.float32(0.0)
+    shift = num.bit_length() - 24
+    if shift <= 0:
+        return np.float32(np.ldexp(float(num), -scale_bits))
+    mant, rem = num >> shift, num & ((1 << shift) - 1)
+    half = 1 << (shift - 1)
+    if rem > half or (rem == half and (mant & 1)):
+        mant += 1
+    return np.float32(np.ldexp(float(mant), shift - scale_bits))
+
+
+def tli_proposal(d2t, t2d, draft_probs):
+    """App. D Alg. 3 (TLI): q' over the target vocabulary from draft rows q over V_d,
+    q'(y) = q(x) / S for y = d2t[x] in the intersection and 0 elsewhere, S the mass q puts on
+    the intersection.  Readings: q is clamped to [0, 1] (NaN -> 0); S is the sum of the
+    intersected masses, each truncated to a multiple of 2^-62 and summed exactly, then rounded
+    once to the nearest fp32; q'(y) is the fp32 quotient; a row with S = 0 gives a zero row.
+
+    Rows of draft_probs are [n, V_d] float32; returns [n, V_t] float32."""
+    q = np.asarray(draft_probs, np.float32)
+    d2t = np.asarray(d2t, np.int64)
+    t2d = np.asarray(t2d, np.int64)
+    n = q.shape[0]
+    out = np.zeros((n, len(t2d)), np.float32)
+    inter = np.nonzero(d2t >= 0)[0]
+    for r in range(n):
+        qc = np.nan_to_num(q[r], nan=0.0)
+        qc = np.minimum(np.maximum(qc, np.float32(0.0)), np.float32(1.0)).astype(np.float32)
+        # floor(q * 2^62) is an exact integer below 2^63 (q has a 24-bit significand)
+        fixed = np.floor(qc[inter].astype(np.float64) * 2.0 ** 62)
+        S = round_to_f32(sum(int(v) for v in fixed), 62)
+        if S == 0:
+            continue
+        out[r, d2t[inter]] = qc[inter] / S  # fp32 quotients
+    return out
+
+
 def threshold(u: float, Z: int) -> int:
     return int(lib().orc_threshold(float(np.float32(u)), int(Z)))
 
