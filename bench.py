@@ -316,6 +316,18 @@ def main():
     hist = torch.empty(256, dtype=torch.int32, device=dev)
     times["delta_histogram"] = kernel_ms(
         lambda i: tt.delta_histogram(a_do, a_to, a_out[1], a_out[2], 256, out=hist))
+    # Token-Level Intersection proposal (App. D Alg. 3): q' over V_t for every draft row of the
+    # batch (one per drafted position); the intersection of the two vocabularies is built once
+    tli = None
+    if draft_probs.shape[1] == vd.n_tokens:
+        d2t, t2d = tt.vocab_intersection(vd, tt.token_index(vd), vt, vt_index)
+        tli_out = torch.empty((draft_probs.shape[0], vt.n_tokens), dtype=torch.float32, device=dev)
+        times["tli_proposal"] = kernel_ms(lambda i: tt.tli_proposal(d2t, t2d, draft_probs, out=tli_out), reps=3)
+        tli_bytes = 4 * draft_probs.shape[0] * (vd.n_tokens + vt.n_tokens)
+        tli = {"us": round(times["tli_proposal"] * 1e3, 1), "rows": int(draft_probs.shape[0]),
+               "intersection_tokens": int((d2t >= 0).sum().item()),
+               "GBps": round(tli_bytes / (times["tli_proposal"] * 1e-3) / 1e9, 1)}
+        del tli_out
     if args.only:
         fn = {"step": lambda i: do_step(i % R), "verify": lambda i: do_verify(i % R),
               "align": lambda i: do_align(), "transfer": lambda i: do_transfer()}[args.only]
@@ -397,6 +409,7 @@ def main():
         "retokenize": {"us": round(times["retokenize"] * 1e3, 2) if "retokenize" in times else None,
                        "string_bytes": rt_bytes,
                        "target_tokens": int(A.target_off[-1])},
+        "tli_proposal": tli,
         "verify": {"GBps": round(gbs_verify, 1), "frac_of_peak": round(gbs_verify / HBM_PEAK_GBS, 4),
                    "algorithmic_bytes": verify_bytes, "accept_rate": round(float(acc[acc >= 0].sum()) /
                                                                            max(1, int(m_s.sum())), 4)},

@@ -292,6 +292,46 @@ int tt_retokenize(const tt_vocab *vd, const tt_vocab *vt, const void *vt_index, 
                   void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * tt_vocab_intersection -- the vocabulary intersection of the Token-Level
+ * Intersection proposal (App. D Alg. 3, the set T ∩ D), each vocabulary taken as a
+ * set of byte strings.
+ *
+ * Inputs: vd, vt token tables (host structs over device arrays) and their token
+ * indexes vd_index, vt_index (device, built by tt_token_index_build from the same
+ * tables; *_index_bytes their sizes, host).
+ * Outputs (device, owned by the caller): d2t[vd->n_tokens] holds, for draft id x, the
+ * id of the target token with the same bytes (the lowest such id), or -1 when vt has
+ * no such token, x is not the lowest draft id holding its bytes, or x's length is 0
+ * or above vd->max_token_bytes; t2d[vt->n_tokens] is the converse (d2t[x] = y exactly
+ * when t2d[y] = x).
+ * Two kernels on `stream`, no workspace.  TT_EINVAL for a missing or misaligned
+ * pointer or an index smaller than tt_token_index_size gives, TT_EUNSUPPORTED if a
+ * table's max_token_bytes is above 64.
+ */
+int tt_vocab_intersection(const tt_vocab *vd, const void *vd_index, size_t vd_index_bytes,
+                          const tt_vocab *vt, const void *vt_index, size_t vt_index_bytes,
+                          int32_t *d2t, int32_t *t2d, void *stream);
+
+/*
+ * tt_tli_proposal -- q' of App. D Alg. 3 for n_rows draft distributions: q'(y) =
+ * q(x) / S where y = d2t[x] (x in the intersection), 0 at every other target id, and
+ * S the mass q puts on the intersection.  Standard speculative sampling then runs
+ * with q' as the dense proposal (tt_verify_dense).
+ *
+ * Inputs (device): d2t[v_d] and t2d[v_t] from tt_vocab_intersection (an entry of
+ * t2d outside [0, v_d) counts as -1); draft_probs,
+ * n_rows rows of v_d floats at a stride of draft_ld floats.  Output (device): q_out,
+ * n_rows rows of v_t floats at a stride of q_ld floats, every element written.
+ * q is clamped to [0, 1] (NaN -> 0); S is the sum of the intersected q(x), each
+ * truncated to a multiple of 2^-62, formed exactly and rounded once to the nearest
+ * fp32 (ties to even); q'(y) is the fp32 quotient.  A row with S = 0 is written as
+ * zeros.  One kernel on `stream` (a workgroup per row), no workspace.  TT_EINVAL for
+ * n_rows < 0, v_d or v_t < 1, a stride below its row length or a missing pointer.
+ */
+int tt_tli_proposal(int32_t n_rows, int32_t v_d, int32_t v_t, const int32_t *d2t, const int32_t *t2d,
+                    const float *draft_probs, int64_t draft_ld, float *q_out, int64_t q_ld, void *stream);
+
+/*
  * Workspace bytes tt_step needs: the larger of tt_align_workspace_size and
  * tt_verify_workspace_size for the same arguments (the two stages run one after
  * the other and share it).

@@ -78,6 +78,10 @@ def lib():
         L.tt_retokenize_workspace_size.restype = ctypes.c_int
         L.tt_retokenize.argtypes = [VP, VP, P, sz, i32, P, P, i32, i32, P, P, P, sz, P]
         L.tt_retokenize.restype = ctypes.c_int
+        L.tt_vocab_intersection.argtypes = [VP, P, sz, VP, P, sz, P, P, P]
+        L.tt_vocab_intersection.restype = ctypes.c_int
+        L.tt_tli_proposal.argtypes = [i32, i32, i32, P, P, P, i64, P, i64, P]
+        L.tt_tli_proposal.restype = ctypes.c_int
         L.tt_step_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz)]
         L.tt_step_workspace_size.restype = ctypes.c_int
         L.tt_step.argtypes = [VP, VP, i32, i32, i32, P, P, P, P, i32, i32, i32, P, i64, P, i64, P, P,
@@ -335,6 +339,43 @@ def retokenize(vd: Vocab, vt: Vocab, vt_index, draft_ids, draft_off, max_bytes: 
                              _ptr(toff, i32, "target_off"), ctypes.c_void_p(workspace.data_ptr()),
                              int(workspace.numel()), _stream_handle(stream))
     _check(st, "tt_retokenize")
+    return out
+
+
+def vocab_intersection(vd: Vocab, vd_index, vt: Vocab, vt_index, out=None, stream=None):
+    """tt_vocab_intersection (App. D Alg. 3's T ∩ D by byte strings).  Returns (d2t, t2d) int32
+    device tensors of vd.n_tokens and vt.n_tokens entries (-1 outside the intersection)."""
+    torch = _torch()
+    i32 = torch.int32
+    dev = vd.offsets.device
+    if out is None:
+        out = (torch.empty(vd.n_tokens, dtype=i32, device=dev), torch.empty(vt.n_tokens, dtype=i32, device=dev))
+    d2t, t2d = out
+    st = lib().tt_vocab_intersection(ctypes.byref(vd._c), ctypes.c_void_p(vd_index.data_ptr()), int(vd_index.numel()),
+                                     ctypes.byref(vt._c), ctypes.c_void_p(vt_index.data_ptr()), int(vt_index.numel()),
+                                     _ptr(d2t, i32, "d2t"), _ptr(t2d, i32, "t2d"), _stream_handle(stream))
+    _check(st, "tt_vocab_intersection")
+    return out
+
+
+def tli_proposal(d2t, t2d, draft_probs, v_d: int | None = None, out=None, stream=None):
+    """tt_tli_proposal: q' rows over the target vocabulary (App. D Alg. 3) from draft rows
+    [n, >= V_d] float32.  Returns out [n, V_t] (or the given tensor, any row stride >= V_t)."""
+    torch = _torch()
+    i32, f32 = torch.int32, torch.float32
+    v_d = int(d2t.numel()) if v_d is None else int(v_d)
+    v_t = int(t2d.numel())
+    if draft_probs.dim() != 2 or draft_probs.stride(1) != 1 or draft_probs.dtype != f32 or not draft_probs.is_cuda:
+        raise ValueError("draft_probs must be a 2-D row-major float32 device tensor")
+    n = int(draft_probs.shape[0])
+    if out is None:
+        out = torch.empty((n, v_t), dtype=f32, device=draft_probs.device)
+    if out.dim() != 2 or out.stride(1) != 1 or out.dtype != f32 or not out.is_cuda:
+        raise ValueError("out must be a 2-D row-major float32 device tensor")
+    st = lib().tt_tli_proposal(n, v_d, v_t, _ptr(d2t, i32, "d2t"), _ptr(t2d, i32, "t2d"),
+                               ctypes.c_void_p(draft_probs.data_ptr()), int(draft_probs.stride(0)),
+                               ctypes.c_void_p(out.data_ptr()), int(out.stride(0)), _stream_handle(stream))
+    _check(st, "tt_tli_proposal")
     return out
 
 

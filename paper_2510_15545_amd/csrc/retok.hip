@@ -20,6 +20,9 @@
 //   3. one wave walks p -> p + L(p) from 0 with the L and token values of 64 positions
 //      held in its lanes (readlane per step), writing the emitted ids to LDS;
 //   4. the ids go to a padded per-stream area of the workspace with their count.
+// The same index serves the vocabulary intersection of the Token-Level Intersection proposal
+// (App. D Alg. 3): a token is in it when it is the lowest id holding its bytes and the other
+// vocabulary's index finds those bytes.
 // Then the ids are packed into CSR order: up to 2,048 streams one kernel in which every
 // workgroup sums the counts before its stream; beyond, one workgroup scans the counts and a
 // copy kernel packs.
@@ -365,6 +368,36 @@ __global__ void __launch_bounds__(kThreads) retok_pack_fold(RetokParams p) {
 
 inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
+// Id in the index's table of the token with these bytes (the lowest id of several), or -1.
+__device__ __forceinline__ int find_token(const Slot *tab, uint32_t mask, const tt_vocab &v, uint32_t h, uint64_t key,
+                                          int len, const uint8_t *bytes) {
+    uint32_t s = h & mask;
+    for (uint32_t probe = 0; probe <= mask; ++probe) {
+        const Slot c = load_slot(tab, s);
+        if (c.id < 0) return -1;  // dead slots keep their id, so a chain never ends early
+        if (c.len == len && c.key == key && (len <= 8 || tail_equal(v, c.id, bytes, len))) return c.id;
+        s = (s + 1) & mask;
+    }
+    return -1;
+}
+
+// Vocabulary intersection (App. D Alg. 3), one thread per token t of vocabulary A: out[t] is
+// the id in B of t's bytes when t is the lowest id in A holding them, else -1.
+__global__ void __launch_bounds__(kThreads) vocab_isect(tt_vocab va, const Slot *ta, uint32_t ma, tt_vocab vb,
+                                                        const Slot *tb, uint32_t mb, int32_t *out) {
+    const int t = blockIdx.x * kThreads + threadIdx.x;
+    if (t >= va.n_tokens) return;
+    uint32_t h;
+    uint64_t key;
+    int len;
+    int res = -1;
+    if (token_sig(va, t, h, key, len)) {
+        const uint8_t *bytes = va.bytes + va.offsets[t];
+        if (find_token(ta, ma, va, h, key, len, bytes) == t) res = find_token(tb, mb, vb, h, key, len, bytes);
+    }
+    out[t] = res;
+}
+
 }  // namespace
 
 uint32_t token_index_capacity(int32_t n_tokens) {
@@ -385,6 +418,19 @@ int launch_token_index_build(const tt_vocab &v, void *index, hipStream_t stream)
     hipLaunchKernelGGL(index_insert, grid, dim3(kThreads), 0, stream, v, tab, cap - 1);
     if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
     hipLaunchKernelGGL(index_dedup, grid, dim3(kThreads), 0, stream, v, tab, cap - 1);
+    return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+}
+
+int launch_vocab_intersection(const tt_vocab &vd, const void *vd_index, const tt_vocab &vt, const void *vt_index,
+                              int32_t *d2t, int32_t *t2d, hipStream_t stream) {
+    const Slot *td = static_cast<const Slot *>(vd_index);
+    const Slot *tt_ = static_cast<const Slot *>(vt_index);
+    const uint32_t md = token_index_capacity(vd.n_tokens) - 1, mt = token_index_capacity(vt.n_tokens) - 1;
+    hipLaunchKernelGGL(vocab_isect, dim3((vd.n_tokens + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, vd, td,
+                       md, vt, tt_, mt, d2t);
+    if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
+    hipLaunchKernelGGL(vocab_isect, dim3((vt.n_tokens + kThreads - 1) / kThreads), dim3(kThreads), 0, stream, vt, tt_,
+                       mt, vd, td, md, t2d);
     return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
 }
 

@@ -184,6 +184,38 @@ int tt_token_index_build(const tt_vocab *v, void *index, size_t index_bytes, voi
     return tt::launch_token_index_build(*v, index, static_cast<hipStream_t>(stream));
 }
 
+int tt_vocab_intersection(const tt_vocab *vd, const void *vd_index, size_t vd_index_bytes, const tt_vocab *vt,
+                          const void *vt_index, size_t vt_index_bytes, int32_t *d2t, int32_t *t2d, void *stream) {
+    if (!vocab_ok(vd) || !vocab_ok(vt) || vd->n_tokens > kMaxIndexTokens || vt->n_tokens > kMaxIndexTokens)
+        return TT_EINVAL;
+    if (vd->max_token_bytes > kMaxTokenBytes || vt->max_token_bytes > kMaxTokenBytes) return TT_EUNSUPPORTED;
+    if (vd_index == nullptr || vt_index == nullptr || (reinterpret_cast<uintptr_t>(vd_index) & 15u) != 0 ||
+        (reinterpret_cast<uintptr_t>(vt_index) & 15u) != 0)
+        return TT_EINVAL;
+    if (vd_index_bytes < tt::token_index_bytes(vd->n_tokens) || vt_index_bytes < tt::token_index_bytes(vt->n_tokens))
+        return TT_EINVAL;
+    if (d2t == nullptr || t2d == nullptr) return TT_EINVAL;
+    return tt::launch_vocab_intersection(*vd, vd_index, *vt, vt_index, d2t, t2d, static_cast<hipStream_t>(stream));
+}
+
+int tt_tli_proposal(int32_t n_rows, int32_t v_d, int32_t v_t, const int32_t *d2t, const int32_t *t2d,
+                    const float *draft_probs, int64_t draft_ld, float *q_out, int64_t q_ld, void *stream) {
+    if (n_rows < 0 || v_d < 1 || v_t < 1 || draft_ld < v_d || q_ld < v_t) return TT_EINVAL;
+    if (n_rows == 0) return TT_OK;
+    if (!d2t || !t2d || !draft_probs || !q_out) return TT_EINVAL;
+    tt::TliArgs a;
+    a.n_rows = n_rows;
+    a.v_d = v_d;
+    a.v_t = v_t;
+    a.d2t = d2t;
+    a.t2d = t2d;
+    a.draft_probs = draft_probs;
+    a.draft_ld = draft_ld;
+    a.q_out = q_out;
+    a.q_ld = q_ld;
+    return tt::launch_tli_proposal(a, static_cast<hipStream_t>(stream));
+}
+
 int tt_retokenize_workspace_size(int32_t n_streams, int32_t max_m, size_t *bytes) {
     if (bytes == nullptr || n_streams < 0 || max_m < 1 || max_m > kMaxRetokBytes) return TT_EINVAL;
     *bytes = tt::retok_workspace_bytes(n_streams, max_m);

@@ -94,6 +94,20 @@ struct RetokArgs {
     void *workspace;
 };
 size_t retok_workspace_bytes(int32_t n_streams, int32_t max_m);
+// d2t / t2d of the vocabulary intersection from the two tables' token indexes.
+int launch_vocab_intersection(const tt_vocab &vd, const void *vd_index, const tt_vocab &vt, const void *vt_index,
+                              int32_t *d2t, int32_t *t2d, hipStream_t stream);
+
+// ---------------------------------------------------------------- TLI proposal rows (tli.hip)
+struct TliArgs {
+    int32_t n_rows, v_d, v_t;
+    const int32_t *d2t, *t2d;
+    const float *draft_probs;
+    int64_t draft_ld;
+    float *q_out;
+    int64_t q_ld;
+};
+int launch_tli_proposal(const TliArgs &a, hipStream_t stream);
 size_t retok_lds_bytes(int32_t max_bytes);
 int launch_retokenize(const RetokArgs &a, hipStream_t stream);
 

@@ -147,6 +147,27 @@ def test_invalid_arguments_return_before_launch():
     assert step(vd=ctypes.byref(big)) == tt.TT_EUNSUPPORTED
     assert step(n=0) == tt.TT_OK
 
+    def isect(vd=ctypes.byref(v), ia=dummy, ib_d=1 << 20, it=dummy, ib_t=1 << 20, d2t=dummy, t2d=dummy):
+        return L.tt_vocab_intersection(vd, ia, ib_d, ctypes.byref(v), it, ib_t, d2t, t2d, None)
+    assert isect(vd=None) == tt.TT_EINVAL
+    assert isect(ia=None) == tt.TT_EINVAL
+    assert isect(it=P(0x1008)) == tt.TT_EINVAL  # not 16-byte aligned
+    assert isect(ib_d=16) == tt.TT_EINVAL
+    assert isect(ib_t=16) == tt.TT_EINVAL
+    assert isect(t2d=None) == tt.TT_EINVAL
+    assert isect(vd=ctypes.byref(big)) == tt.TT_EUNSUPPORTED
+
+    def tli(n=2, v_d=10, v_t=12, ld_d=10, ld_q=12, d2t=dummy, q=dummy):
+        return L.tt_tli_proposal(n, v_d, v_t, d2t, dummy, dummy, ld_d, q, ld_q, None)
+    assert tli(n=-1) == tt.TT_EINVAL
+    assert tli(v_d=0) == tt.TT_EINVAL
+    assert tli(v_t=0) == tt.TT_EINVAL
+    assert tli(ld_d=9) == tt.TT_EINVAL
+    assert tli(ld_q=11) == tt.TT_EINVAL
+    assert tli(d2t=None) == tt.TT_EINVAL
+    assert tli(q=None) == tt.TT_EINVAL
+    assert tli(n=0, q=None) == tt.TT_OK
+
 
 def test_binding_refuses_host_tensors():
     torch = pytest.importorskip("torch")
