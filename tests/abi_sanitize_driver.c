@@ -53,6 +53,10 @@ int main(void) {
     EXPECT(tt_token_index_build(&v, (void *)0x1004, 1 << 30, NULL) == TT_EINVAL);
     EXPECT(tt_retokenize(&v, &v, W, 1 << 20, 1, D, D, 0, 16, D, D, W, 1 << 20, NULL) == TT_EINVAL);
     EXPECT(tt_retokenize(&v, &v, W, 1 << 20, 1, D, D, 64, 16, D, D, W, 4, NULL) == TT_EWORKSPACE);
+    EXPECT(tt_vocab_intersection(&v, W, 1 << 20, &v, W, 16, D, D, NULL) == TT_EINVAL);
+    EXPECT(tt_vocab_intersection(&big, W, 1 << 20, &v, W, 1 << 20, D, D, NULL) == TT_EUNSUPPORTED);
+    EXPECT(tt_tli_proposal(1, 10, 10, D, D, F, 9, F, 10, NULL) == TT_EINVAL);
+    EXPECT(tt_tli_proposal(0, 10, 10, NULL, NULL, NULL, 10, NULL, 10, NULL) == TT_OK);
     printf("done\n");
     return 0;
 }
