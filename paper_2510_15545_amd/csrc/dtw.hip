@@ -18,10 +18,13 @@
 //     chunk c, waves 1-3 evaluate the distances of chunk c + 1 into the other half of a
 //     double buffer ([lane][step / 4] dwords, one byte per step, bit 7 set for cells
 //     outside the band so the sweep needs no band arithmetic).  One barrier per chunk.
-//   * Token distance: the bit-parallel edit-distance recurrence (Myers 1999, in Hyyro's
-//     2001 global-distance form) with the longer token as the pattern (one bit per byte,
-//     at most 64) and the shorter one as the text; per-byte match masks come from SWAR
-//     byte comparison of the packed pattern.
+//   * Token distance: per-byte match masks of a packed token come from SWAR byte
+//     comparison.  When every draft token of a wave's cells has at most two bytes (nearly
+//     always for natural-language tokens), a closed form over the target token's match
+//     masks for those bytes gives the distance; otherwise the bit-parallel edit-distance
+//     recurrence (Myers 1999, in Hyyro's 2001 global-distance form) runs with the longer
+//     token as the pattern (one bit per byte, at most 64) and the shorter one as the text.
+//     Each thread loads the target tokens of its four cells together before computing.
 //   * Each cell's predecessor choice is two bits (up: C(i-1, j) < C(i-1, j-1); left:
 //     C(i, j-1) below both), shifted into a per-lane register, 16 steps per dword, and
 //     stored straight from registers into the caller's workspace, row-major by draft row.
@@ -150,22 +153,40 @@ __device__ __forceinline__ Strip strip_at(const Band &g, int s) {
     return st;
 }
 
-// Edit distance between two tokens of at most 32 bytes: Myers' recurrence with the longer
-// token as the pattern (32-bit masks) and D(0, j) = j, read at the end from the vertical
-// deltas (as in the shared distance).  The loop over the shorter token's bytes leaves once
-// no lane of the wave has bytes left; lanes already done keep their state.
+// Bits 0 .. n-1 set (n <= 32).
+__device__ __forceinline__ uint32_t low_mask(int n) { return n >= 32 ? 0xFFFFFFFFu : ((1u << n) - 1u); }
+
+// Edit distance between a draft token of at most two bytes (the text, xm bytes: c1 = byte 0
+// broadcast in bc1, c2 = byte 1 in bc2) and a target token (the pattern, yn bytes in yw, lim
+// its bit mask), in closed form over the pattern positions E1, E2 that equal c1, c2:
+//   xm = 0 or yn = 0   d = xm + yn
+//   xm = 1             d = yn - [E1 != 0]
+//   xm = 2, yn = 1     d = 2 - [E1 | E2 != 0]
+//   xm = 2, yn >= 2    d = yn - 2 + (0 if some a < b has E1[a] and E2[b];
+//                                    1 else if E1 has a bit below yn - 1 or E2 a bit above 0;
+//                                    2 else)
+// (for yn >= 2 the two text bytes go to two increasing pattern positions, the other yn - 2
+// bytes are deleted, and each costs 1 unless it matches; an alignment that inserts a text
+// byte costs at least yn).
 template <int TB>
-__device__ __forceinline__ uint32_t short_distance(const uint32_t (&aw)[TB / 4], int m, const uint32_t *y, int n) {
-    uint32_t bw[TB / 4], pw[TB / 4], tw[TB / 4];
-    read_slot<TB>(y, bw);
-    const bool swap = n > m;
-#pragma unroll
-    for (int q = 0; q < TB / 4; ++q) {
-        pw[q] = swap ? bw[q] : aw[q];
-        tw[q] = swap ? aw[q] : bw[q];
-    }
-    const int pm = swap ? n : m, tn = swap ? m : n;
-    const uint32_t lim = pm >= 32 ? 0xFFFFFFFFu : ((1u << pm) - 1u);
+__device__ __forceinline__ uint32_t closed_distance(const uint32_t (&yw)[TB / 4], int yn, uint32_t lim, uint32_t bc1,
+                                                    uint32_t bc2, int xm) {
+    const uint32_t e1 = dtw::match_mask<TB>(yw, bc1) & lim;
+    const uint32_t e2 = dtw::match_mask<TB>(yw, bc2) & lim;
+    const uint32_t low1 = e1 & (0u - e1);                   // lowest position matching c1
+    const bool in_order = (e2 & ~((low1 << 1) - 1u)) != 0;  // c2 matches further on
+    const bool one = (e1 & (lim >> 1)) != 0 || (e2 & ~1u) != 0;
+    const uint32_t two = yn - 2 + (in_order ? 0u : (one ? 1u : 2u));
+    const uint32_t d2 = yn == 1 ? 2u - ((e1 | e2) != 0 ? 1u : 0u) : two;
+    const uint32_t d1 = (uint32_t)yn - (e1 != 0 ? 1u : 0u);
+    return (xm == 0 || yn == 0) ? (uint32_t)(xm + yn) : (xm == 1 ? d1 : d2);
+}
+
+// The same distance by Myers' recurrence with D(0, j) = j over the text's bytes, read at the
+// end from the vertical deltas; the loop leaves once no lane of the wave has bytes left.
+template <int TB>
+__device__ __forceinline__ uint32_t myers_distance(const uint32_t (&pw)[TB / 4], const uint32_t (&tw)[TB / 4], int tn,
+                                                   uint32_t lim) {
     uint32_t vp = 0xFFFFFFFFu, vn = 0;
 #pragma unroll
     for (int k = 0; k < TB; ++k) {
@@ -189,7 +210,10 @@ __device__ __forceinline__ uint32_t short_distance(const uint32_t (&aw)[TB / 4],
 // t in [T0, T0 + 64) goes to byte t & 3 of dword buf[r][(t - T0) / 4]; out-of-band
 // cells get 0x80.  Threads h, h + nh, ... each take four consecutive steps of one row, and
 // consecutive threads consecutive steps: a wave's lanes then leave the band together
-// (rows in consecutive lanes would diverge at every band edge).
+// (rows in consecutive lanes would diverge at every band edge).  The four cells of a thread
+// load their target tokens together (columns clamped into [1, M], results masked) and take
+// the closed form with the draft token as the text unless some lane of the wave has a draft
+// token of more than two bytes.
 template <int TB>
 __device__ __forceinline__ void chunk_costs(const Band &g, const Strip &st, int T0, uint32_t *buf,
                                             const uint32_t *tslot, const uint8_t *tlen, const uint32_t *dslot,
@@ -204,19 +228,55 @@ __device__ __forceinline__ void chunk_costs(const Band &g, const Strip &st, int 
             uint32_t xw[TB / 4];
             read_slot<TB>(dslot + (i - 1) * (TB / 4), xw);
             const int xm = dlen[i - 1];
+            if constexpr (TB <= 32) {
+                const bool closed = !__any(xm > 2);  // uniform: the wave's draft tokens have at most two bytes
+                const uint32_t bc1 = __builtin_amdgcn_perm(0u, xw[0], 0u);
+                const uint32_t bc2 = __builtin_amdgcn_perm(0u, xw[0], 0x01010101u);
+                constexpr int kBatch = TB <= 8 ? 4 : 1;  // target slots loaded together (within 64 VGPRs)
+                uint32_t d[4];
+#pragma unroll
+                for (int u0 = 0; u0 < 4; u0 += kBatch) {
+                    uint32_t yw[kBatch][TB / 4];
+                    int yn[kBatch];
+#pragma unroll
+                    for (int v = 0; v < kBatch; ++v) {
+                        int j = jb + u0 + v;
+                        j = j < 1 ? 1 : (j > g.M ? g.M : j);
+                        read_slot<TB>(tslot + (j - 1) * (TB / 4), yw[v]);
+                        yn[v] = tlen[j - 1];
+                    }
+#pragma unroll
+                    for (int v = 0; v < kBatch; ++v) {
+                        if (closed) {
+                            d[u0 + v] = closed_distance<TB>(yw[v], yn[v], low_mask(yn[v]), bc1, bc2, xm);
+                        } else {
+                            const bool swap = yn[v] > xm;
+                            uint32_t pw[TB / 4], tw[TB / 4];
+#pragma unroll
+                            for (int q = 0; q < TB / 4; ++q) {
+                                pw[q] = swap ? yw[v][q] : xw[q];
+                                tw[q] = swap ? xw[q] : yw[v][q];
+                            }
+                            d[u0 + v] = myers_distance<TB>(pw, tw, swap ? xm : yn[v], low_mask(swap ? yn[v] : xm));
+                        }
+                    }
+                }
+                packed = 0;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int j = jb + u;
+                    packed |= ((j >= jl && j <= jh) ? d[u] : 0x80u) << (8 * u);
+                }
+            } else {
 #pragma unroll 1
-            for (int u = 0; u < 4; ++u) {
-                const int j = jb + u;
-                if (j >= jl && j <= jh) {
-                    uint32_t d;
-                    if constexpr (TB <= 32) {
-                        d = short_distance<TB>(xw, xm, tslot + (j - 1) * (TB / 4), tlen[j - 1]);
-                    } else {
+                for (int u = 0; u < 4; ++u) {
+                    const int j = jb + u;
+                    if (j >= jl && j <= jh) {
                         uint32_t yw[TB / 4];
                         read_slot<TB>(tslot + (j - 1) * (TB / 4), yw);
-                        d = (uint32_t)token_distance<TB>(xw, xm, yw, tlen[j - 1]);
+                        const uint32_t d = (uint32_t)token_distance<TB>(xw, xm, yw, tlen[j - 1]);
+                        packed = (packed & ~(0xFFu << (8 * u))) | (d << (8 * u));
                     }
-                    packed = (packed & ~(0xFFu << (8 * u))) | (d << (8 * u));
                 }
             }
         }
