@@ -524,7 +524,7 @@ def main_dense(args):
 
         threads = len(os.sched_getaffinity(0))
         k, t0 = 0, time.time()
-        while k == 0 or (time.time() - t0 < args.cpu_seconds and k < 50):
+        while k == 0 or time.time() - t0 < args.cpu_seconds:
             o_n, o_t, _, _ = oracle.sd_verify(D.v, D.draft_ids, D.off, D.draft_probs, D.target_probs, D.u_accept,
                                               D.u_sample, n_threads=threads)
             k += 1
@@ -549,7 +549,7 @@ def cpu_baseline(args, S, A, nacc, tok, s_out, a_out):
     threads = len(os.sched_getaffinity(0))
     reps, t0 = 0, time.time()
     out = None
-    while reps == 0 or (time.time() - t0 < args.cpu_seconds and reps < 50):
+    while reps == 0 or time.time() - t0 < args.cpu_seconds:
         if S is not A:
             oracle.align(A.vocab_d.data, A.vocab_d.offsets, A.vocab_d.max_len, A.vocab_t.data,
                          A.vocab_t.offsets, A.vocab_t.max_len, A.draft_ids, A.draft_off, A.target_ids,
