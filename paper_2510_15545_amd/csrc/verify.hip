@@ -16,9 +16,10 @@
 // 30.6 us against ordinary loads.
 //
 // Two launch shapes:
-//   row path    (at least one stream per CU): one 1024-thread workgroup per stream
-//               runs the acceptance scan once, streams its whole row with 16 waves,
-//               keeps the chunk sums in LDS and one wave samples.  One kernel.
+//   row path    (at least one stream per CU): one workgroup per stream runs the
+//               acceptance scan once, streams its whole row (about eight chunks per
+//               wave: 64 to 1024 threads), keeps the chunk sums in LDS and one wave
+//               samples.  One kernel.
 //   split path  (fewer streams): verify_stream over B x S workgroups (every workgroup
 //               of a stream recomputes gamma, streams its share of the row and stores
 //               chunk sums), then verify_sample with one wave per stream.  The kernel
@@ -114,8 +115,8 @@ __device__ __forceinline__ void stream_row(const float *row, const Proposal &pr,
 }
 
 // ------------------------------------------------------------------ row path
-template <bool DENSE>
-__global__ void __launch_bounds__(kRowThreads) verify_row(VParams p) {
+template <bool DENSE, int THREADS>
+__global__ void __launch_bounds__(THREADS) verify_row(VParams p) {
     const VerifyArgs &a = p.a;
     const int b = blockIdx.x;
     const int tid = threadIdx.x, lane = tid % kWave;
@@ -147,7 +148,7 @@ __global__ void __launch_bounds__(kRowThreads) verify_row(VParams p) {
     const int vt = a.v_t;
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
     const Proposal pr = proposal<DENSE>(a, t0, M, r);
-    stream_row(row, pr, vt, p.vec4 != 0, 0, p.nc, kRowThreads / kWave, [&](int c, uint64_t s) { sh_part[c] = s; });
+    stream_row(row, pr, vt, p.vec4 != 0, 0, p.nc, THREADS / kWave, [&](int c, uint64_t s) { sh_part[c] = s; });
     __syncthreads();
     if (wave != 0) return;
     uint64_t Z;
@@ -341,7 +342,16 @@ template <bool DENSE>
 int launch_verify_kernels(VParams &p, hipStream_t stream) {
     const VerifyArgs &a = p.a;
     if (verify_row_path(a.n_streams, a.v_t)) {
-        hipLaunchKernelGGL(verify_row<DENSE>, dim3(a.n_streams), dim3(kRowThreads), 8 * (size_t)p.nc, stream, p);
+        // about eight chunks per wave: short rows take small workgroups, so that several
+        // streams share a compute unit and their acceptance scans and samples overlap
+        const size_t lds = 8 * (size_t)p.nc;
+        const int waves = (p.nc + 7) / 8;
+        const dim3 g(a.n_streams);
+        if (waves <= 1) hipLaunchKernelGGL((verify_row<DENSE, 64>), g, dim3(64), lds, stream, p);
+        else if (waves <= 2) hipLaunchKernelGGL((verify_row<DENSE, 128>), g, dim3(128), lds, stream, p);
+        else if (waves <= 4) hipLaunchKernelGGL((verify_row<DENSE, 256>), g, dim3(256), lds, stream, p);
+        else if (waves <= 8) hipLaunchKernelGGL((verify_row<DENSE, 512>), g, dim3(512), lds, stream, p);
+        else hipLaunchKernelGGL((verify_row<DENSE, kRowThreads>), g, dim3(kRowThreads), lds, stream, p);
         return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
     }
     return launch_split<DENSE, false>(p, stream);
