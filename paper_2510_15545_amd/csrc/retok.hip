@@ -18,7 +18,8 @@
 //      FNV-1a hashes of all prefixes come from one pass over the bytes, and the first
 //      slot of eight candidate lengths is loaded together (longest first);
 //   3. one wave walks p -> p + L(p) from 0 with the L and token values of 64 positions
-//      held in its lanes (readlane per step), writing the emitted ids to LDS;
+//      held in its lanes (a readlane per step, the emitted positions kept in a scalar
+//      mask), then writes the window's emitted ids to LDS;
 //   4. the ids go to a padded per-stream area of the workspace with their count.
 // The same index serves the vocabulary intersection of the Token-Level Intersection proposal
 // (App. D Alg. 3): a token is in it when it is the lowest id holding its bytes and the other
@@ -281,25 +282,32 @@ __global__ void __launch_bounds__(kThreads) retok_stream(RetokParams p) {
         }
     }
     __syncthreads();
-    // 3. the greedy walk, one wave, 64 positions per window held in lanes
+    // 3. the greedy walk, one wave, 64 positions per window held in lanes.  Inside a window the
+    // dependent loop is a bound check, a readlane and a mask update: a position where no target
+    // token starts sends the walk past the window (a ballot then reports the failure), the
+    // emitted positions go to a scalar mask, and their count and ids are formed after it
     if (wave == 0) {
         int pos = 0, m = 0;
         bool fail = sh_bad != 0;
         while (!fail && pos < n) {
-            const int p0 = pos;
-            const int lv = p0 + lane < n ? (int)sh_L[p0 + lane] : 0;
-            const int tv = p0 + lane < n ? sh_tok[p0 + lane] : 0;
-            while (pos < n && pos < p0 + kWave) {
-                const int l = __builtin_amdgcn_readlane(lv, pos - p0);
-                if (l == 0 || m >= p.max_m) {
-                    fail = true;
-                    break;
-                }
-                const int t = __builtin_amdgcn_readlane(tv, pos - p0);
-                if (lane == 0) sh_pos[m] = t;  // sh_pos is free again: reuse it for the output
-                ++m;
-                pos += l;
+            const int p0 = pos, m0 = m;
+            const int lim = (n - p0 < kWave ? n - p0 : kWave);  // window length
+            const bool inside = lane < lim;
+            const int lv = inside ? (int)sh_L[p0 + lane] : 0;
+            const int tv = inside ? sh_tok[p0 + lane] : 0;
+            const uint64_t dead = __ballot(inside && lv == 0);  // no target token starts here
+            const int step = lv == 0 ? kWave : lv;
+            uint64_t emitted = 0;  // bit k: a token starts at p0 + k
+            int rel = 0;
+            while (rel < lim) {
+                emitted |= 1ull << rel;
+                rel += __builtin_amdgcn_readlane(step, rel);
             }
+            m = m0 + __popcll(emitted);
+            fail = (emitted & dead) != 0 || m > p.max_m;
+            pos = p0 + rel;
+            // sh_pos is free again: it takes the output, the k-th emitted position giving id m0 + k
+            if ((emitted >> lane) & 1ull) sh_pos[m0 + __popcll(emitted & ((1ull << lane) - 1ull))] = tv;
         }
         if (lane == 0) sh_m = fail ? 0 : m;
     }
