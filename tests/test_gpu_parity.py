@@ -99,10 +99,11 @@ def test_one_workgroup_per_stream_path():
     compare_verify(g, o, residual=True)
 
 
-@pytest.mark.parametrize("c", [2, 3])
+@pytest.mark.parametrize("c", [2, 3, 5])
 def test_full_size_workload(c):
-    """The benchmark's shapes, every stream checked (workload 3 takes the row path)."""
-    wl = _case(c, {2: None, 3: None})
+    """The benchmark's shapes, every stream checked (workloads 3 and 5 take the row path;
+    workload 5 is 512 streams over rows of 262,144)."""
+    wl = _case(c, {2: None, 3: None, 5: None})
     g = gpu_run(wl)
     o = oracle_run(wl)
     compare_align(wl, g, o)

@@ -50,7 +50,7 @@ def same_as_three_calls(wl, s, g):
         assert np.array_equal(s["residual"].view(np.uint32), g["residual"].view(np.uint32))
 
 
-@pytest.mark.parametrize("c,n", [(1, 300), (2, 256), (3, None), (2, 32), (5, 256), (1, None), (1, 7)])
+@pytest.mark.parametrize("c,n", [(1, 300), (2, 256), (3, None), (2, 32), (5, 256), (5, None), (1, None), (1, 7)])
 def test_step_matches_three_calls_and_oracle(c, n):
     print(f"[case] tt_step workload {c} streams={n}", flush=True)
     wl = synth.make(c, n_streams=n)
