@@ -405,10 +405,15 @@ def main():
         "kernels_ms": {k: round(v, 5) for k, v in times.items()},
         "dtw": {"band_cells": cells, "cells_per_s": round(cells_per_s, 1),
                 "full_cells": int((Ka * Ma).sum()),
+                "full_cells_per_s": round(int((Ka * Ma).sum()) / (times["align"] * 1e-3), 1),
                 "delta_pos_w90": tt.w_at_quantile(hist, 0.9), "path_cells": int(a_out[1].sum().item())},
         "retokenize": {"us": round(times["retokenize"] * 1e3, 2) if "retokenize" in times else None,
                        "string_bytes": rt_bytes,
                        "target_tokens": int(A.target_off[-1])},
+        "throughput": {"target_positions_per_s": round(int(m_s.sum()) / (ms_step * 1e-3), 1),
+                       "accepted_drafts_per_s": round(int(acc[acc >= 0].sum()) / (ms_step * 1e-3), 1),
+                       "transfer_share_of_three_calls": round(times["transfer"] / (times["align"] + times["transfer"] +
+                                                                                   times["verify"]), 4)},
         "tli_proposal": tli,
         "verify": {"GBps": round(gbs_verify, 1), "frac_of_peak": round(gbs_verify / HBM_PEAK_GBS, 4),
                    "algorithmic_bytes": verify_bytes, "accept_rate": round(float(acc[acc >= 0].sum()) /
@@ -532,6 +537,7 @@ def main_dense(args):
         result["cpu_baseline"] = {
             "value": round(int(m.sum()) / dt, 1), "unit": "draft tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{k} whole steps of the benchmark batch ({n} streams), {dt * 1e3:.1f} ms each",
+            "cpu_model": cpu_model(),
             "matches_gpu": bool(np.array_equal(o_n, acc) and np.array_equal(o_t, tok.cpu().numpy()))}
     print(json.dumps(result), flush=True)
 
@@ -557,6 +563,16 @@ def cpu_baseline(args, S, A, nacc, tok, s_out, a_out):
         out = oracle.run_workload(S, n_threads=threads)
         reps += 1
     dt = (time.time() - t0) / reps
+    # the same on one thread, for a third of the time
+    reps1, t1 = 0, time.time()
+    while reps1 == 0 or time.time() - t1 < args.cpu_seconds / 3:
+        if S is not A:
+            oracle.align(A.vocab_d.data, A.vocab_d.offsets, A.vocab_d.max_len, A.vocab_t.data,
+                         A.vocab_t.offsets, A.vocab_t.max_len, A.draft_ids, A.draft_off, A.target_ids,
+                         A.target_off, args.w, n_threads=1)
+        oracle.run_workload(S, n_threads=1)
+        reps1 += 1
+    dt1 = (time.time() - t1) / reps1
     draft_tokens = int(S.draft_off[-1])
     match = bool(np.array_equal(out["n_accepted"], nacc.cpu().numpy()) and
                  np.array_equal(out["out_token"], tok.cpu().numpy()) and
@@ -564,7 +580,21 @@ def cpu_baseline(args, S, A, nacc, tok, s_out, a_out):
     return {"value": round(draft_tokens / dt, 1), "unit": "draft tokens/s", "cores": threads,
             "kind": "oracle", "sample": f"{reps} whole steps of the benchmark batch "
                                         f"({S.n} streams), {dt * 1e3:.1f} ms each",
-            "matches_gpu": match}
+            "value_1_thread": round(draft_tokens / dt1, 1),
+            "sample_1_thread": f"{reps1} whole steps, {dt1 * 1e3:.1f} ms each",
+            "cpu_model": cpu_model(), "matches_gpu": match}
+
+
+def cpu_model():
+    """The host CPU's model name (/proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 if __name__ == "__main__":
