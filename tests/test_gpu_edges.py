@@ -254,12 +254,27 @@ def test_large_vocabularies(n, V, dense):
     """Rows past 256 chunks (the sampler's chunk sums no longer fit four per lane) on the
     one-workgroup-per-stream path, and rows past 8M floats (over the row path's LDS) on the
     split path; one-hot and dense proposals, bit-exact against the oracle."""
+    print(f"[case] large vocabulary n={n} V={V} dense={dense}", flush=True)
+    verify_case(n, V, dense)
+
+
+@pytest.mark.parametrize("V", [640, 12_000, 30_000, 50_000, 100_000])
+@pytest.mark.parametrize("dense", [False, True])
+def test_row_path_workgroup_sizes(V, dense):
+    """The one-workgroup-per-stream path sizes its workgroup from the row (about eight 1024-float
+    chunks per wave): 64, 128, 256, 512 and 1024 threads for these widths."""
+    print(f"[case] row path n=256 V={V} dense={dense}", flush=True)
+    verify_case(256, V, dense)
+
+
+def verify_case(n, V, dense):
+    """Random rows of width V for n streams with 0-2 proposals each; GPU outputs against the
+    oracle, bit for bit (one-hot proposals through tt_verify, dense through tt_verify_dense)."""
     import torch
 
     import oracle
     import paper_2510_15545_amd as tt
 
-    print(f"[case] large vocabulary n={n} V={V} dense={dense}", flush=True)
     rng = np.random.default_rng(V + n)
     Ms = rng.integers(0, 3, n)
     off = np.zeros(n + 1, np.int32)
