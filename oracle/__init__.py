@@ -5,7 +5,8 @@ this package.  The GPU library never calls it and shares no code with it.
 
 `tt_oracle.c` holds the arithmetic (plain C, fp32 where the inputs are fp32,
 exact integers elsewhere); this module builds it with gcc and wraps it with
-ctypes over numpy arrays.  See the header of `tt_oracle.c` for the paper
+ctypes over numpy arrays.  The re-tokenisation, the vocabulary intersection and
+the Token-Level Intersection proposal are written here in plain Python / numpy.  See the header of `tt_oracle.c` for the paper
 passages each function follows and the readings taken where the paper is silent.
 
 Parity status: every function here is pinned by tests under `tests/`
