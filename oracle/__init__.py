@@ -63,6 +63,10 @@ def lib():
         L.orc_sd_verify.restype = None
         L.orc_delta_histogram.argtypes = [i32, P, P, P, P, i32, P]
         L.orc_delta_histogram.restype = None
+        L.orc_sexp.argtypes = [f32]
+        L.orc_sexp.restype = f32
+        L.orc_verify_logits.argtypes = [i32, i32, P, P, P, P, i64, P, P, P, i32, P, P, P, ctypes.c_int]
+        L.orc_verify_logits.restype = None
         L.orc_threshold.argtypes = [f32, u64]
         L.orc_threshold.restype = u64
         _lib = L
@@ -188,6 +192,35 @@ def sd_verify(v, draft_ids, off, draft_probs, target_probs, u_accept, u_sample, 
                         target_probs.shape[1], _p(ua), _p(u_sample), int(max_m), _p(nacc), _p(tok),
                         _p(res), _p(z), n_threads or threads_default())
     return nacc, tok, res, z
+
+
+def sexp(x: float) -> np.float32:
+    """The software exponential of the logits path (x <= 0)."""
+    return np.float32(lib().orc_sexp(float(np.float32(x))))
+
+
+def verify_logits(v, target_ids, target_off, q, logits_bf16, inv_temp, u_accept, u_sample, max_m=None,
+                  n_threads=None):
+    """Verification from bf16 target logits (uint16 bit patterns, rows off[b]+b+j) and a per-stream
+    inverse temperature: the target softmax formed with the specified exponential, then the
+    one-hot acceptance and the residual sample.  Returns (n_accepted, out_token, Z)."""
+    target_ids, target_off = _c(target_ids, np.int32), _c(target_off, np.int32)
+    q, inv_temp = _c(q, np.float32), _c(inv_temp, np.float32)
+    u_accept, u_sample = _c(u_accept, np.float32), _c(u_sample, np.float32)
+    logits_bf16 = _c(logits_bf16, np.uint16)
+    n = len(target_off) - 1
+    if max_m is None:
+        max_m = int(np.diff(target_off).max()) if n else 0
+    nacc = np.full(n, -7, np.int32)
+    tok = np.full(n, -7, np.int32)
+    z = np.zeros(n, np.uint64)
+    ti = target_ids if target_ids.size else np.zeros(1, np.int32)
+    q_ = q if q.size else np.zeros(1, np.float32)
+    ua = u_accept if u_accept.size else np.zeros(1, np.float32)
+    lib().orc_verify_logits(n, int(v), _p(ti), _p(target_off), _p(q_), _p(logits_bf16), logits_bf16.shape[1],
+                            _p(inv_temp), _p(ua), _p(u_sample), int(max_m), _p(nacc), _p(tok), _p(z),
+                            n_threads or threads_default())
+    return nacc, tok, z
 
 
 def delta_histogram(draft_off, target_off, path_len, path, n_bins):

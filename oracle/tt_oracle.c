@@ -25,6 +25,8 @@
  *                     speculative decoding, the homogeneous-vocabulary case)
  *   orc_delta_histogram  Sec. 5 Fig. CDF / App. K: position deviation |i - j| of the
  *                     matched pairs on the optimal paths
+ *   orc_verify_logits the verification from bf16 logits and a temperature (App. F), the
+ *                     target softmax formed with a specified software exponential
  *
  * Readings where the paper is silent or ambiguous (each is listed in the design
  * notes of the repository):
@@ -530,6 +532,150 @@ void orc_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_
             hist[dev < n_bins - 1 ? dev : n_bins - 1] += 1;
         }
     }
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Verification from bf16 target logits with a temperature (the step before Sec. 3's target
+ * distribution, App. F sampling temperatures): P_t = softmax(logit * inv_temp) formed inside
+ * the verification.  Readings (the paper fixes none of this arithmetic):
+ *   x        = fp32(bf16 logit) * inv_temp (fp32); NaN logits count as minus infinity;
+ *   m        = the largest x of the row;
+ *   e(x)     = orc_sexp(x - m), a specified software exponential (below);
+ *   e39(x)   = floor(e(x) * 2^39) (exact: e <= 1 has 24 significant bits);
+ *   S        = (sum of e39) * 2^-39 rounded once to the nearest fp32, ties to even;
+ *   P_t(t_j) = e(t_j) / S (fp32), and the acceptance test of the one-hot path;
+ *   residual on rejection at r: the row's e39 with the entry at t_r replaced by
+ *            floor(clamp(e(t_r) - q_r * S, 0, 1) * 2^39) -- proportional to
+ *            max(0, P_t - q_r e_{t_r}); after full acceptance the bonus row's e39;
+ *   sample   T = floor(u * Z) and the first index whose prefix exceeds T, as for the
+ *            probability rows; if Z = 0 the first index of the largest x (0 if none).
+ * Rows of at most 2^23 entries keep every sum below 2^63. */
+
+/* exp(x) for x <= 0: Cody-Waite reduction x = k ln2 + r (k = x log2(e) rounded to the
+ * nearest integer, ties to even; r by two fused multiply-adds with ln2 split into its fp32
+ * value and the fp32 value of the remainder), the degree-6 Taylor polynomial of exp(r) by
+ * Horner's rule with fused multiply-adds, then scaling by 2^k.  0 below -87 and for NaN. */
+float orc_sexp(float x) {
+    if (!(x >= -87.0f)) return 0.0f;
+    const float kf = rintf(x * 0x1.715476p+0f);
+    float r = fmaf(-kf, 0x1.62e430p-1f, x);
+    r = fmaf(-kf, -0x1.05c610p-29f, r);
+    float p = 0x1.6c16c2p-10f;     /* 1/6! */
+    p = fmaf(p, r, 0x1.111112p-7f); /* 1/5! */
+    p = fmaf(p, r, 0x1.555556p-5f); /* 1/4! */
+    p = fmaf(p, r, 0x1.555556p-3f); /* 1/3! */
+    p = fmaf(p, r, 0.5f);
+    p = fmaf(p, r, 1.0f);
+    p = fmaf(p, r, 1.0f);
+    return ldexpf(p, (int)kf);
+}
+
+static uint64_t q39(float e) { /* floor(e * 2^39) for e in [0, 1] */
+    const float s = e * 128.0f;
+    const uint32_t hi = (uint32_t)s;
+    const uint32_t lo = (uint32_t)((s - (float)hi) * 4294967296.0f);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+static float q39_to_f32(uint64_t n) { /* n * 2^-39 rounded to the nearest fp32, ties to even */
+    if (n == 0) return 0.0f;
+    int bl = 64;
+    while (!((n >> (bl - 1)) & 1u)) --bl;
+    if (bl <= 24) return ldexpf((float)n, -39);
+    const int sh = bl - 24;
+    uint64_t mant = n >> sh;
+    const uint64_t rem = n & ((1ull << sh) - 1), half = 1ull << (sh - 1);
+    if (rem > half || (rem == half && (mant & 1u))) ++mant;
+    return ldexpf((float)mant, sh - 39);
+}
+
+static float bf16_to_f32(uint16_t h) {
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+
+typedef struct {
+    int32_t v;
+    const int32_t *ids, *off;
+    const float *q;
+    const uint16_t *logits;
+    int64_t ld;
+    const float *inv_temp, *ua, *us;
+    int32_t max_m;
+    int32_t *nacc, *tok;
+    uint64_t *z;
+} orc_logits_ctx;
+
+static void orc_logits_stream(orc_logits_ctx *c, int32_t b) {
+    const int32_t t0 = c->off[b], M = c->off[b + 1] - t0;
+    int ok = M >= 0 && M <= c->max_m && c->inv_temp[b] > 0.0f;
+    for (int32_t j = 0; ok && j < M; ++j) ok = c->ids[t0 + j] >= 0 && c->ids[t0 + j] < c->v;
+    if (!ok) {
+        c->nacc[b] = -1;
+        c->tok[b] = -1;
+        c->z[b] = 0;
+        return;
+    }
+    float *x = (float *)malloc(sizeof(float) * (size_t)c->v);
+    uint64_t *e39 = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)c->v);
+    const float it = c->inv_temp[b];
+    for (int32_t j = 0; j <= M; ++j) {
+        const uint16_t *row = c->logits + (int64_t)(t0 + b + j) * c->ld;
+        float m = -INFINITY;
+        for (int32_t i = 0; i < c->v; ++i) {
+            x[i] = bf16_to_f32(row[i]) * it;
+            if (isnan(x[i])) x[i] = -INFINITY;
+            if (x[i] > m) m = x[i];
+        }
+        uint64_t Sq = 0;
+        for (int32_t i = 0; i < c->v; ++i) Sq += (e39[i] = q39(orc_sexp(x[i] - m)));
+        const float S = q39_to_f32(Sq);
+        uint64_t Z = Sq;
+        if (j < M) {
+            const int32_t t = c->ids[t0 + j];
+            const float qj = c->q[t0 + j];
+            const float et = orc_sexp(x[t] - m);
+            const float P = et / S;
+            if (qj <= 0.0f || c->ua[t0 + j] < P / qj) continue; /* accepted: next position */
+            float rt = et - qj * S;
+            rt = fminf(fmaxf(rt, 0.0f), 1.0f); /* NaN -> 0 */
+            const uint64_t before = e39[t];
+            e39[t] = q39(rt);
+            Z = Sq - before + e39[t];
+        }
+        int32_t token = 0;
+        if (Z == 0) {
+            float best = -INFINITY;
+            for (int32_t i = 0; i < c->v; ++i)
+                if (x[i] > best) {
+                    best = x[i];
+                    token = i;
+                }
+        } else {
+            token = sample_quantised(e39, c->v, Z, c->us[b]);
+        }
+        c->nacc[b] = j;
+        c->tok[b] = token;
+        c->z[b] = Z;
+        break;
+    }
+    free(x);
+    free(e39);
+}
+
+static void orc_logits_range(void *p, int32_t lo, int32_t hi) {
+    for (int32_t s = lo; s < hi; ++s) orc_logits_stream((orc_logits_ctx *)p, s);
+}
+
+void orc_verify_logits(int32_t n_streams, int32_t v, const int32_t *target_ids, const int32_t *target_off,
+                       const float *q, const uint16_t *logits, int64_t ld, const float *inv_temp,
+                       const float *u_accept, const float *u_sample, int32_t max_m, int32_t *n_accepted,
+                       int32_t *out_token, uint64_t *z_out, int n_threads) {
+    orc_logits_ctx c = {v, target_ids, target_off, q, logits, ld, inv_temp, u_accept, u_sample, max_m,
+                        n_accepted, out_token, z_out};
+    orc_parallel(n_streams, n_threads, orc_logits_range, &c);
 }
 
 /* Test hook: the exact threshold floor(u * Z). */

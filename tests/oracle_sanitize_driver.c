@@ -33,6 +33,11 @@ void orc_sd_verify(int32_t n_streams, int32_t V, const int32_t *draft_ids, const
 void orc_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
                          const int32_t *path_len, const int32_t *path, int32_t n_bins, int64_t *hist);
 uint64_t orc_threshold(float u, uint64_t Z);
+float orc_sexp(float x);
+void orc_verify_logits(int32_t n_streams, int32_t v, const int32_t *target_ids, const int32_t *target_off,
+                       const float *q, const uint16_t *logits, int64_t ld, const float *inv_temp,
+                       const float *u_accept, const float *u_sample, int32_t max_m, int32_t *n_accepted,
+                       int32_t *out_token, uint64_t *z_out, int n_threads);
 
 static uint32_t rng_state = 12345u;
 static uint32_t next_u32(void) { /* xorshift32 */
@@ -141,6 +146,19 @@ int main(void) {
            acc);
     printf("threshold %llu %llu\n", (unsigned long long)orc_threshold(0.5f, 1000u),
            (unsigned long long)orc_threshold(1.0f - 0x1p-24f, ~0ull));
+
+    /* logits: bf16 rows (random bit patterns of finite values, one NaN row), stream 1 invalid */
+    uint16_t *lg = (uint16_t *)malloc(sizeof(uint16_t) * 8 * VT);
+    for (int k = 0; k < 8 * VT; ++k) lg[k] = (uint16_t)(0x3c00u + (next_u32() % 0x0800u));
+    for (int x = 0; x < VT; ++x) lg[2 * VT + x] = 0x7FC0u;
+    int32_t loff[4] = {0, 2, 3, 5}, lids[5] = {1, 3, 70, 0, 49};
+    float lq[5] = {0.5f, 0.9f, 0.1f, 0.2f, 0.3f}, lit[3] = {1.0f, 1.4f, 2.0f}, lus[3] = {0.25f, 0.75f, 0.5f};
+    int32_t lnacc[3], ltok[3];
+    uint64_t lz[3];
+    orc_verify_logits(3, VT, lids, loff, lq, lg, VT, lit, sua, lus, 4, lnacc, ltok, lz, 2);
+    printf("logits %d/%d %d/%d %d/%d sexp %.7g\n", lnacc[0], ltok[0], lnacc[1], ltok[1], lnacc[2], ltok[2],
+           (double)orc_sexp(-1.0f));
+    free(lg);
 
     free(vdb); free(vtb); free(vdo); free(vto); free(dids); free(tids); free(path); free(map);
     free(dprobs); free(q); free(tprobs); free(ua); free(res); free(sq); free(sp); free(sres);

@@ -1,0 +1,125 @@
+"""Pins for the oracle's verification from bf16 logits (the target softmax formed inside the
+verification, with the sampling temperatures of App. F).
+
+The software exponential is checked against the C library's exp of the same fp32 argument
+(an ulp bound over a dense grid, exact special values); the verification is checked against
+laws computed independently in float64: with a one-hot proposal of mass 1 the emitted token
+follows softmax(logit / T), and after a rejection it follows the closed form of the
+transferred-proposal law (min(1, p/q) at the proposal, the rest in proportion); an exactly
+representable softmax fixes the acceptance boundary; invalid streams give sentinels.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from test_oracle_verify import ALPHA, chi2_pvalue, u24
+
+
+def bf16_bits(x):
+    """Round fp32 values to bf16 (ties to even), returned as uint16 bit patterns."""
+    b = np.asarray(x, np.float32).view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return b.astype(np.uint16)
+
+
+def bf16_value(bits):
+    return (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def softmax64(x):
+    x = np.asarray(x, np.float64)
+    e = np.exp(x - x.max())
+    return e / e.sum()
+
+
+def ulps(a: np.float32, b: float) -> float:
+    """|a - b| in units of the fp32 spacing at b."""
+    return abs(float(a) - b) / float(np.spacing(np.float32(b)))
+
+
+def test_sexp_ulp_bound_and_special_values(orc):
+    xs = np.concatenate([-np.geomspace(1e-7, 86.99, 4000), np.linspace(-86.99, 0.0, 4001)]).astype(np.float32)
+    worst = max(ulps(orc.sexp(x), math.exp(float(x))) for x in xs)
+    assert worst <= 3.0, worst  # the reduction error grows with |k|: 2.6 ulp at x = -81
+    assert orc.sexp(0.0) == np.float32(1.0)
+    assert orc.sexp(-87.01) == 0 and orc.sexp(-1e30) == 0 and orc.sexp(float("nan")) == 0
+    assert orc.sexp(float("-inf")) == 0
+    ys = np.sort(xs)
+    vals = np.array([orc.sexp(y) for y in ys])
+    assert np.all(np.diff(vals) >= 0)  # non-decreasing in x
+
+
+def one_position_batch(rng, logits_rows, q, N, t=None):
+    """N streams with M = 1 over the same two rows (position 0 and the bonus row)."""
+    V = logits_rows.shape[1]
+    ids = np.full(N, t if t is not None else 0, np.int32)
+    off = np.arange(N + 1, dtype=np.int32)
+    rows = np.tile(logits_rows, (N, 1))
+    return V, ids, off, np.full(N, q, np.float32), rows
+
+
+@pytest.mark.parametrize("temp", [1.0, 0.7])
+def test_emitted_token_follows_the_tempered_softmax(orc, temp):
+    """q = 1 at the proposal: accept with probability p(t), else the residual (p without t,
+    renormalised), so the emitted token's law is p = softmax(logit / T)."""
+    rng = np.random.default_rng(80)
+    V, N, t = 6, 200_000, 2
+    bits = bf16_bits(rng.normal(0, 1.5, (2, V)).astype(np.float32))
+    it = np.float32(1.0 / temp)
+    V, ids, off, q, rows = one_position_batch(rng, bits, 1.0, N, t)
+    nacc, tok, _ = orc.verify_logits(V, ids, off, q, rows, np.full(N, it, np.float32), u24(rng, N), u24(rng, N))
+    first = np.where(nacc > 0, t, tok)
+    p = softmax64(bf16_value(bits[0]) * it)
+    assert chi2_pvalue(np.bincount(first, minlength=V), p) > ALPHA
+    assert abs(np.mean(nacc) - p[t]) < 5 * math.sqrt(p[t] * (1 - p[t]) / N)
+
+
+def test_rejection_law_closed_form(orc):
+    """One-hot proposal of mass a at t: P(out = t) = min(1, p(t)/a), any other x in proportion
+    to p(x) -- the transferred-proposal law, here with p = softmax(logit)."""
+    rng = np.random.default_rng(81)
+    V, N, t, a = 5, 200_000, 1, 0.6
+    bits = bf16_bits(np.array([[0.2, 0.9, -0.4, 0.0, 0.5], [0.0] * 5], np.float32))
+    V, ids, off, q, rows = one_position_batch(rng, bits, a, N, t)
+    nacc, tok, _ = orc.verify_logits(V, ids, off, q, rows, np.ones(N, np.float32), u24(rng, N), u24(rng, N))
+    out = np.where(nacc > 0, t, tok)
+    p = softmax64(bf16_value(bits[0]))
+    keep = min(1.0, p[t] / a)
+    law = np.array([(1 - keep) * p[x] / (1 - p[t]) for x in range(V)])
+    law[t] = keep
+    assert chi2_pvalue(np.bincount(out, minlength=V), law) > ALPHA
+
+
+def test_exact_softmax_fixes_the_accept_boundary(orc):
+    """Eight equal logits: every e = 1, S = 8 exactly, p(t) = 1/8; with q = 1/4 the ratio is 1/2,
+    so u = 1/2 - 2^-24 accepts and u = 1/2 rejects."""
+    V = 8
+    bits = bf16_bits(np.full((2, V), 3.0, np.float32))
+    for u, want in ((0.5 - 2.0 ** -24, 1), (0.5, 0)):
+        nacc, tok, z = orc.verify_logits(V, np.array([3], np.int32), np.array([0, 1], np.int32),
+                                         np.array([0.25], np.float32), bits, np.ones(1, np.float32),
+                                         np.array([u], np.float32), np.array([0.0], np.float32))
+        assert nacc[0] == want
+        if want == 0:  # residual: p(t) - q < 0, so t has no mass; Z = 7 * 2^39; u_sample = 0 -> first token
+            assert int(z[0]) == 7 * 2 ** 39 and tok[0] == 0
+
+
+def test_sentinels_nan_and_empty_rows(orc):
+    V = 4
+    bits = bf16_bits(np.zeros((7, V), np.float32))
+    bits[5] = 0x7FC0                      # NaN logits: no mass
+    bits[5, 2] = bf16_bits(np.float32(1.0))
+    bits[6] = 0xFF80                      # -inf everywhere: Z = 0, token 0
+    ids = np.array([1, 9, 0, 0], np.int32)  # stream 1 has an id outside [0, V)
+    off = np.array([0, 1, 2, 3, 3], np.int32)
+    # stream b's rows start at off[b] + b: stream 0 rows 0-1, stream 1 rows 2-3, stream 2 rows 4-5, stream 3 row 6
+    q = np.ones(3, np.float32)
+    it = np.array([1, 1, 1, 1], np.float32)
+    ua = np.array([0.99, 0.99, 0.0], np.float32)  # stream 2 accepts its proposal
+    nacc, tok, z = orc.verify_logits(V, ids, off, q, bits, it, ua, np.array([0.3, 0.3, 0.3, 0.7], np.float32))
+    assert nacc[1] == -1 and tok[1] == -1
+    assert nacc[2] == 1 and tok[2] == 2     # the bonus row's only finite logit (the rest are NaN)
+    assert nacc[3] == 0 and tok[3] == 0 and int(z[3]) == 0
+    bad_t = orc.verify_logits(V, ids[:1], off[:2], q[:1], bits, np.array([0.0], np.float32), ua[:1], ua[:1])
+    assert bad_t[0][0] == -1
