@@ -226,6 +226,33 @@ int tt_verify_dense(int32_t n_streams, int32_t v,
                     void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * tt_verify_logits -- tt_verify with the target distributions given as bf16 logits and a
+ * per-stream sampling temperature (App. F) instead of fp32 probability rows: the softmax
+ * of Sec. 3's acceptance rule and of the residual (App. D Alg. 4) is formed inside.
+ *
+ * Inputs (device): target_ids, target_off, q, u_accept, u_sample as for tt_verify;
+ * target_logits: bf16 bit patterns, row target_off[b] + b + j (j in [0, M_b]) at a stride
+ * of target_ld elements; inv_temperature[n_streams] fp32 (1 / T, > 0).  max_m as for
+ * tt_verify.  Outputs (device): n_accepted, out_token as for tt_verify (no residual rows).
+ * Arithmetic, all of it order-independent: x = logit * inv_temperature (NaN counts as
+ * minus infinity), m = the row's largest x, e = exp(x - m) by a specified software
+ * exponential (Cody-Waite reduction, degree-6 Taylor polynomial with fused multiply-adds,
+ * 0 below -87), e39 = floor(e * 2^39) summed exactly, S = that sum * 2^-39 rounded once
+ * to fp32, P_t(t_j) = e(t_j) / S in fp32; accept while q_j <= 0 or u_j < P_t(t_j) / q_j;
+ * after a rejection at r the residual is the row's e39 with the entry at t_r replaced by
+ * floor(clamp(e(t_r) - q_r * S, 0, 1) * 2^39), after full acceptance the bonus row's e39;
+ * the token is the first index whose prefix exceeds floor(u_sample * Z) (the first
+ * largest x when Z = 0).  A stream with M_b outside [0, max_m], an id outside [0, v_t)
+ * or inv_temperature <= 0 gets n_accepted = out_token = -1.
+ * One kernel on `stream`, a workgroup per stream reading rows 0 .. gamma; no workspace.
+ * TT_EINVAL on a bad size or a missing pointer, TT_EUNSUPPORTED for v_t > 2^23.
+ */
+int tt_verify_logits(int32_t n_streams, int32_t v_t, const int32_t *target_ids, const int32_t *target_off,
+                     const float *q, const uint16_t *target_logits, int64_t target_ld,
+                     const float *inv_temperature, const float *u_accept, const float *u_sample,
+                     int32_t max_m, int32_t *n_accepted, int32_t *out_token, void *stream);
+
+/*
  * tt_delta_histogram -- position deviation of the matched tokens of aligned pairs
  * (Sec. 5 "DTW Bridges the Gap", Fig. CDF; App. K "Settings of w").  A cell (i, j)
  * of an optimal warping path matches draft token i with proxy target token j; it

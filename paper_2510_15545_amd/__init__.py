@@ -68,6 +68,8 @@ def lib():
         L.tt_verify.restype = ctypes.c_int
         L.tt_verify_dense.argtypes = [i32, i32, P, P, P, i64, P, i64, P, P, i32, P, P, P, P, sz, P]
         L.tt_verify_dense.restype = ctypes.c_int
+        L.tt_verify_logits.argtypes = [i32, i32, P, P, P, P, i64, P, P, P, i32, P, P, P]
+        L.tt_verify_logits.restype = ctypes.c_int
         L.tt_delta_histogram.argtypes = [i32, P, P, P, P, i32, P, P]
         L.tt_delta_histogram.restype = ctypes.c_int
         L.tt_token_index_size.argtypes = [i32, ctypes.POINTER(sz)]
@@ -276,6 +278,32 @@ def verify_dense(v: int, draft_ids, off, draft_probs, target_probs, u_accept, u_
                                _ptr(res, f32, "residual", allow_none=True),
                                ctypes.c_void_p(workspace.data_ptr()), int(workspace.numel()), _stream_handle(stream))
     _check(st, "tt_verify_dense")
+    return out
+
+
+def verify_logits(v_t: int, target_ids, target_off, q, target_logits, inv_temperature, u_accept, u_sample,
+                  max_m: int, out=None, stream=None):
+    """tt_verify_logits: target_logits is a 2-D row-major device tensor of bf16 (or its int16 / uint16
+    bit patterns); inv_temperature float32 [n_streams].  Returns (n_accepted, out_token)."""
+    torch = _torch()
+    i32, f32 = torch.int32, torch.float32
+    n = int(target_off.numel()) - 1
+    dev = target_off.device
+    if target_logits.dim() != 2 or target_logits.stride(1) != 1 or not target_logits.is_cuda or \
+            target_logits.element_size() != 2:
+        raise ValueError("target_logits must be a 2-D row-major 16-bit device tensor")
+    if out is None:
+        out = (torch.empty(n, dtype=i32, device=dev), torch.empty(n, dtype=i32, device=dev))
+    nacc, tok = out
+    ids = target_ids if target_ids.numel() else torch.zeros(1, dtype=i32, device=dev)
+    qq = q if q.numel() else torch.zeros(1, dtype=f32, device=dev)
+    ua = u_accept if u_accept.numel() else torch.zeros(1, dtype=f32, device=dev)
+    st = lib().tt_verify_logits(n, int(v_t), _ptr(ids, i32, "target_ids"), _ptr(target_off, i32, "target_off"),
+                                _ptr(qq, f32, "q"), ctypes.c_void_p(target_logits.data_ptr()),
+                                int(target_logits.stride(0)), _ptr(inv_temperature, f32, "inv_temperature"),
+                                _ptr(ua, f32, "u_accept"), _ptr(u_sample, f32, "u_sample"), int(max_m),
+                                _ptr(nacc, i32, "n_accepted"), _ptr(tok, i32, "out_token"), _stream_handle(stream))
+    _check(st, "tt_verify_logits")
     return out
 
 

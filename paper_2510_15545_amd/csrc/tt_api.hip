@@ -14,6 +14,7 @@ constexpr int32_t kMaxVerifyLen = 65536; // bound on M_b accepted by tt_verify
 constexpr int32_t kMaxHistBins = 8192;   // bins of tt_delta_histogram (its LDS copy: 32 KB)
 constexpr int32_t kMaxIndexTokens = 1 << 28;  // vocabulary size a token index accepts
 constexpr int32_t kMaxTokenBytes = 64;        // longest target token the index and lookups handle
+constexpr int32_t kMaxLogitsRow = 1 << 23;     // logits per row tt_verify_logits accepts (64-bit exact sums)
 constexpr int32_t kMaxRetokBytes = 4096;      // bytes of S (and tokens of T) per stream: 14 B of LDS each
 
 bool vocab_ok(const tt_vocab *v) {
@@ -160,6 +161,33 @@ int tt_verify_dense(int32_t n_streams, int32_t v, const int32_t *draft_ids, cons
     a.q_rows = draft_probs;
     a.q_ld = draft_ld;
     return tt::launch_verify(a, static_cast<hipStream_t>(stream));
+}
+
+int tt_verify_logits(int32_t n_streams, int32_t v_t, const int32_t *target_ids, const int32_t *target_off,
+                     const float *q, const uint16_t *target_logits, int64_t target_ld, const float *inv_temperature,
+                     const float *u_accept, const float *u_sample, int32_t max_m, int32_t *n_accepted,
+                     int32_t *out_token, void *stream) {
+    if (n_streams < 0 || v_t < 1 || target_ld < v_t || max_m < 0 || max_m > kMaxVerifyLen) return TT_EINVAL;
+    if (v_t > kMaxLogitsRow) return TT_EUNSUPPORTED;
+    if (n_streams == 0) return TT_OK;
+    if (!target_ids || !target_off || !q || !target_logits || !inv_temperature || !u_accept || !u_sample ||
+        !n_accepted || !out_token)
+        return TT_EINVAL;
+    tt::LogitsArgs a;
+    a.n_streams = n_streams;
+    a.v_t = v_t;
+    a.target_ids = target_ids;
+    a.target_off = target_off;
+    a.q = q;
+    a.logits = target_logits;
+    a.ld = target_ld;
+    a.inv_temp = inv_temperature;
+    a.u_accept = u_accept;
+    a.u_sample = u_sample;
+    a.max_m = max_m;
+    a.n_accepted = n_accepted;
+    a.out_token = out_token;
+    return tt::launch_verify_logits(a, static_cast<hipStream_t>(stream));
 }
 
 int tt_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,

@@ -98,6 +98,19 @@ size_t retok_workspace_bytes(int32_t n_streams, int32_t max_m);
 int launch_vocab_intersection(const tt_vocab &vd, const void *vd_index, const tt_vocab &vt, const void *vt_index,
                               int32_t *d2t, int32_t *t2d, hipStream_t stream);
 
+// ---------------------------------------------------------------- verification from logits (logits.hip)
+struct LogitsArgs {
+    int32_t n_streams, v_t;
+    const int32_t *target_ids, *target_off;
+    const float *q;
+    const uint16_t *logits;  // bf16 bit patterns
+    int64_t ld;
+    const float *inv_temp, *u_accept, *u_sample;
+    int32_t max_m;
+    int32_t *n_accepted, *out_token;
+};
+int launch_verify_logits(const LogitsArgs &a, hipStream_t stream);
+
 // ---------------------------------------------------------------- TLI proposal rows (tli.hip)
 struct TliArgs {
     int32_t n_rows, v_d, v_t;

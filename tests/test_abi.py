@@ -157,6 +157,17 @@ def test_invalid_arguments_return_before_launch():
     assert isect(t2d=None) == tt.TT_EINVAL
     assert isect(vd=ctypes.byref(big)) == tt.TT_EUNSUPPORTED
 
+    def logits(n=1, v=10, ld=10, max_m=4, it=dummy, lg=dummy):
+        return L.tt_verify_logits(n, v, dummy, dummy, dummy, lg, ld, it, dummy, dummy, max_m, dummy, dummy, None)
+    assert logits(n=-1) == tt.TT_EINVAL
+    assert logits(v=0) == tt.TT_EINVAL
+    assert logits(ld=9) == tt.TT_EINVAL
+    assert logits(max_m=-1) == tt.TT_EINVAL
+    assert logits(it=None) == tt.TT_EINVAL
+    assert logits(lg=None) == tt.TT_EINVAL
+    assert logits(v=(1 << 23) + 1, ld=(1 << 23) + 1) == tt.TT_EUNSUPPORTED
+    assert logits(n=0, lg=None) == tt.TT_OK
+
     def tli(n=2, v_d=10, v_t=12, ld_d=10, ld_q=12, d2t=dummy, q=dummy):
         return L.tt_tli_proposal(n, v_d, v_t, d2t, dummy, dummy, ld_d, q, ld_q, None)
     assert tli(n=-1) == tt.TT_EINVAL
