@@ -114,6 +114,11 @@ def parse():
     ap.add_argument("--dense", action="store_true",
                     help="standard speculative sampling with dense proposals over one vocabulary "
                          "(tt_verify_dense) on 256 streams x M=8 at V=151,936 instead of the TokenTiming path")
+    ap.add_argument("--lse", action="store_true",
+                    help="with --logits: pass per-row log-sum-exp values (computed on the GPU beforehand)")
+    ap.add_argument("--logits", action="store_true",
+                    help="verification from bf16 target logits and a temperature (tt_verify_logits) on the "
+                         "benchmark's 256 streams at V_t=151,936 instead of fp32 probability rows")
     ap.add_argument("--traffic", type=str, default=None,
                     help="counter summary with the measured HBM bytes per launch of the dominant kernel "
                          "(default: profiles/<kernel>_counters.txt)")
@@ -130,6 +135,8 @@ def main():
 
     if args.dense:
         return main_dense(args)
+    if args.logits:
+        return main_logits(args)
 
     import torch
 
@@ -539,6 +546,126 @@ def main_dense(args):
             "sample": f"{k} whole steps of the benchmark batch ({n} streams), {dt * 1e3:.1f} ms each",
             "cpu_model": cpu_model(),
             "matches_gpu": bool(np.array_equal(o_n, acc) and np.array_equal(o_t, tok.cpu().numpy()))}
+    print(json.dumps(result), flush=True)
+
+
+def main_logits(args):
+    """Verification from bf16 logits (tt_verify_logits) on the benchmark's streams: the same
+    target ids, offsets and uniforms, target logits bf16(3 N(0,1)) with the logit of each
+    proposal raised to the row's maximum + 1 at 30% of the positions, temperature 0.7, proposal
+    masses uniform in [0.05, 0.55).  Logits are generated on the GPU (seeded) and replicated
+    like the probability rows."""
+    import torch
+
+    import paper_2510_15545_amd as tt
+    from paper_2510_15545_amd import synth
+
+    tt.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_gen = time.time()
+    S = synth.make(3, n_streams=args.streams, probs=False)
+    n, V = S.n, S.v_t
+    m = np.diff(S.target_off)
+    rows = int(S.target_off[-1]) + n
+    g = torch.Generator(device=dev)
+    g.manual_seed(3003)
+    x = torch.randn((rows, V), generator=g, device=dev, dtype=torch.float32).mul_(3.0)
+    row_of = torch.from_numpy((S.target_off[:-1] + np.arange(n))[np.repeat(np.arange(n), m)] +
+                              (np.arange(int(m.sum())) - np.repeat(S.target_off[:-1], m))).to(dev).long()
+    ids_l = torch.from_numpy(S.verify_ids.astype(np.int64)).to(dev)
+    force = torch.rand(int(m.sum()), generator=g, device=dev) < 0.3
+    x[row_of[force], ids_l[force]] = x[row_of[force]].max(dim=1).values + 1.0
+    R = max(1, args.replicas)
+    logits = [x.to(torch.bfloat16)]
+    del x
+    for _ in range(R - 1):
+        logits.append(logits[0].clone())
+    q = (torch.rand(int(m.sum()), generator=g, device=dev) * 0.5 + 0.05).contiguous()
+    it = torch.full((n,), 1.0 / 0.7, dtype=torch.float32, device=dev)
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    ids, off = t(S.verify_ids), t(S.target_off)
+    # uniforms on the 2^-24 grid, as the generator draws them
+    ua = torch.randint(0, 1 << 24, (int(m.sum()),), generator=g, device=dev).float().mul_(2.0 ** -24)
+    us = torch.randint(0, 1 << 24, (n,), generator=g, device=dev).float().mul_(2.0 ** -24)
+    max_m = max(1, int(m.max()))
+    nacc = torch.empty(n, dtype=torch.int32, device=dev)
+    tok = torch.empty(n, dtype=torch.int32, device=dev)
+    lse = None
+    if args.lse:  # what an LM head would emit with its logits: log-sum-exp of logit / T per row
+        row_it = it.repeat_interleave(torch.from_numpy(m + 1).to(dev))
+        lse = torch.cat([(logits[0][i:i + 256].float() * row_it[i:i + 256, None]).logsumexp(dim=1)
+                         for i in range(0, rows, 256)]).contiguous()
+    torch.cuda.synchronize()
+    t_gen = time.time() - t_gen
+
+    def step(r):
+        tt.verify_logits(V, ids, off, q, logits[r], it, ua, us, max_m, lse=lse, out=(nacc, tok))
+
+    for i in range(args.warmup):
+        step(i % R)
+    torch.cuda.synchronize()
+    gs = 1 if args.eager else max(1, min(args.graph_steps, args.steps))
+    reps = max(1, args.steps // gs)
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if args.eager:
+        s0.record()
+        for i in range(reps):
+            step(i % R)
+        s1.record()
+    else:
+        gr = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            with torch.cuda.graph(gr, stream=cap):
+                for i in range(gs):
+                    step(i % R)
+        torch.cuda.current_stream().wait_stream(cap)
+        gr.replay()
+        torch.cuda.synchronize()
+        s0.record()
+        for _ in range(reps):
+            gr.replay()
+        s1.record()
+    torch.cuda.synchronize()
+    ms = s0.elapsed_time(s1) / (reps * gs)
+    step(0)
+    torch.cuda.synchronize()
+    acc = nacc.cpu().numpy()
+    if lse is None:
+        # algorithmic bytes: each row a stream reads (rows 0 .. gamma, once), t_j, q_j, u_j per
+        # position, 1/T, u_sample, n_accepted, out_token
+        rows_read = int((np.minimum(acc, m) + 1).sum())
+        kbytes = int(2 * V * rows_read + 12 * int(m.sum()) + 16 * n)
+    else:
+        # one row per stream (the residual or bonus row) and its L; per position tested
+        # (0 .. min(gamma, M - 1)) t_j, q_j, u_j, L_j and the gathered logit
+        rows_read = n
+        tested = int(np.minimum(acc + 1, m).sum())
+        kbytes = int(2 * V * n + 4 * n + 18 * tested + 16 * n)
+    gbs = kbytes / (ms * 1e-3) / 1e9
+    elems_per_s = V * rows_read / (ms * 1e-3)
+    draft_tokens = int(S.draft_off[-1])
+    result = {
+        "metric": "verified draft tokens/s from bf16 logits (T=0.7) at V_t=151,936; HBM GB/s vs peak",
+        "value": round(draft_tokens / (ms * 1e-3), 1), "unit": "draft tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16+f32+i64", "data": "synthetic",
+        "config": {"workload": f"{n} streams V_t={V} bf16 logits T=0.7 30% forced" +
+                   (" with row log-sum-exp" if lse is not None else ""), "streams": n,
+                   "target_positions": int(m.sum()), "v_t": V, "replicas": R, "path": "tt_verify_logits" + ("+lse" if lse is not None else ""),
+                   "launch": "eager" if args.eager else "hip-graph of %d steps" % gs},
+        "accept": {"mean_gamma": round(float(acc.mean()), 3), "rows_read": rows_read},
+        "roofline": {"kernel": "verify_logits_row", "bound": "hbm", "achieved": round(gbs, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "traffic_note": "no counters for this kernel", "algorithmic_bytes_per_launch": kbytes,
+                     "launch_us": round(ms * 1e3, 2), "logits_per_s": round(elems_per_s, 1)},
+        "gen_seconds": round(t_gen, 1),
+    }
     print(json.dumps(result), flush=True)
 
 

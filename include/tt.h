@@ -244,13 +244,19 @@ int tt_verify_dense(int32_t n_streams, int32_t v,
  * the token is the first index whose prefix exceeds floor(u_sample * Z) (the first
  * largest x when Z = 0).  A stream with M_b outside [0, max_m], an id outside [0, v_t)
  * or inv_temperature <= 0 gets n_accepted = out_token = -1.
- * One kernel on `stream`, a workgroup per stream reading rows 0 .. gamma; no workspace.
+ * lse (device, optional, one fp32 per logits row): the row's log-sum-exp of x, as an LM
+ * head can emit it with its logits.  When given, m = lse and S = 1 (P = clamp(e, 0, 1),
+ * the residual entry at t_r is floor(clamp(P(t_r) - q_r, 0, 1) * 2^39)): the acceptance
+ * test reads one logit per position and only the residual (or bonus) row is read, once.
+ * Without it each stream reads its rows 0 .. gamma twice (max, then sums), one after another.
+ * One kernel on `stream`, a workgroup per stream; no workspace.
  * TT_EINVAL on a bad size or a missing pointer, TT_EUNSUPPORTED for v_t > 2^23.
  */
 int tt_verify_logits(int32_t n_streams, int32_t v_t, const int32_t *target_ids, const int32_t *target_off,
                      const float *q, const uint16_t *target_logits, int64_t target_ld,
-                     const float *inv_temperature, const float *u_accept, const float *u_sample,
-                     int32_t max_m, int32_t *n_accepted, int32_t *out_token, void *stream);
+                     const float *inv_temperature, const float *lse, const float *u_accept,
+                     const float *u_sample, int32_t max_m, int32_t *n_accepted, int32_t *out_token,
+                     void *stream);
 
 /*
  * tt_delta_histogram -- position deviation of the matched tokens of aligned pairs

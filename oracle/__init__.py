@@ -65,7 +65,7 @@ def lib():
         L.orc_delta_histogram.restype = None
         L.orc_sexp.argtypes = [f32]
         L.orc_sexp.restype = f32
-        L.orc_verify_logits.argtypes = [i32, i32, P, P, P, P, i64, P, P, P, i32, P, P, P, ctypes.c_int]
+        L.orc_verify_logits.argtypes = [i32, i32, P, P, P, P, i64, P, P, P, P, i32, P, P, P, ctypes.c_int]
         L.orc_verify_logits.restype = None
         L.orc_threshold.argtypes = [f32, u64]
         L.orc_threshold.restype = u64
@@ -200,10 +200,11 @@ def sexp(x: float) -> np.float32:
 
 
 def verify_logits(v, target_ids, target_off, q, logits_bf16, inv_temp, u_accept, u_sample, max_m=None,
-                  n_threads=None):
+                  lse=None, n_threads=None):
     """Verification from bf16 target logits (uint16 bit patterns, rows off[b]+b+j) and a per-stream
     inverse temperature: the target softmax formed with the specified exponential, then the
-    one-hot acceptance and the residual sample.  Returns (n_accepted, out_token, Z)."""
+    one-hot acceptance and the residual sample.  With per-row log-sum-exp values `lse` the rows'
+    normalisers are taken from them instead.  Returns (n_accepted, out_token, Z)."""
     target_ids, target_off = _c(target_ids, np.int32), _c(target_off, np.int32)
     q, inv_temp = _c(q, np.float32), _c(inv_temp, np.float32)
     u_accept, u_sample = _c(u_accept, np.float32), _c(u_sample, np.float32)
@@ -217,8 +218,9 @@ def verify_logits(v, target_ids, target_off, q, logits_bf16, inv_temp, u_accept,
     ti = target_ids if target_ids.size else np.zeros(1, np.int32)
     q_ = q if q.size else np.zeros(1, np.float32)
     ua = u_accept if u_accept.size else np.zeros(1, np.float32)
+    lse = None if lse is None else _c(lse, np.float32)
     lib().orc_verify_logits(n, int(v), _p(ti), _p(target_off), _p(q_), _p(logits_bf16), logits_bf16.shape[1],
-                            _p(inv_temp), _p(ua), _p(u_sample), int(max_m), _p(nacc), _p(tok), _p(z),
+                            _p(inv_temp), _p(lse), _p(ua), _p(u_sample), int(max_m), _p(nacc), _p(tok), _p(z),
                             n_threads or threads_default())
     return nacc, tok, z
 

@@ -603,10 +603,53 @@ typedef struct {
     const uint16_t *logits;
     int64_t ld;
     const float *inv_temp, *ua, *us;
+    const float *lse; /* per row, or NULL */
     int32_t max_m;
     int32_t *nacc, *tok;
     uint64_t *z;
 } orc_logits_ctx;
+
+/* With per-row log-sum-exp values L_j supplied by the caller (in the units of x):
+ * P(x) = clamp(sexp(x - L_j), 0, 1), the acceptance test on P(t_j) / q_j, and the residual
+ * row r's entries floor(P * 2^39), the one at t_r floor(clamp(P(t_r) - q_r, 0, 1) * 2^39);
+ * only the residual row is read in full. */
+static void orc_logits_stream_lse(orc_logits_ctx *c, int32_t b) {
+    const int32_t t0 = c->off[b], M = c->off[b + 1] - t0;
+    const float it = c->inv_temp[b];
+    int32_t r = M;
+    for (int32_t j = 0; j < M; ++j) {
+        const int64_t row = t0 + b + j;
+        float xt = bf16_to_f32(c->logits[row * c->ld + c->ids[t0 + j]]) * it;
+        if (isnan(xt)) xt = -INFINITY;
+        const float P = fminf(fmaxf(orc_sexp(xt - c->lse[row]), 0.0f), 1.0f);
+        const float qj = c->q[t0 + j];
+        if (!(qj <= 0.0f || c->ua[t0 + j] < P / qj)) {
+            r = j;
+            break;
+        }
+    }
+    const int64_t row = t0 + b + r;
+    const uint16_t *lg = c->logits + row * c->ld;
+    uint64_t *e39 = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)c->v);
+    uint64_t Z = 0;
+    float best = -INFINITY;
+    int32_t arg = 0;
+    for (int32_t i = 0; i < c->v; ++i) {
+        float x = bf16_to_f32(lg[i]) * it;
+        if (isnan(x)) x = -INFINITY;
+        if (x > best) {
+            best = x;
+            arg = i;
+        }
+        float P = fminf(fmaxf(orc_sexp(x - c->lse[row]), 0.0f), 1.0f);
+        if (r < M && i == c->ids[t0 + r]) P = fminf(fmaxf(P - c->q[t0 + r], 0.0f), 1.0f);
+        Z += (e39[i] = q39(P));
+    }
+    c->nacc[b] = r;
+    c->tok[b] = Z == 0 ? arg : sample_quantised(e39, c->v, Z, c->us[b]);
+    c->z[b] = Z;
+    free(e39);
+}
 
 static void orc_logits_stream(orc_logits_ctx *c, int32_t b) {
     const int32_t t0 = c->off[b], M = c->off[b + 1] - t0;
@@ -616,6 +659,10 @@ static void orc_logits_stream(orc_logits_ctx *c, int32_t b) {
         c->nacc[b] = -1;
         c->tok[b] = -1;
         c->z[b] = 0;
+        return;
+    }
+    if (c->lse != NULL) {
+        orc_logits_stream_lse(c, b);
         return;
     }
     float *x = (float *)malloc(sizeof(float) * (size_t)c->v);
@@ -671,9 +718,9 @@ static void orc_logits_range(void *p, int32_t lo, int32_t hi) {
 
 void orc_verify_logits(int32_t n_streams, int32_t v, const int32_t *target_ids, const int32_t *target_off,
                        const float *q, const uint16_t *logits, int64_t ld, const float *inv_temp,
-                       const float *u_accept, const float *u_sample, int32_t max_m, int32_t *n_accepted,
-                       int32_t *out_token, uint64_t *z_out, int n_threads) {
-    orc_logits_ctx c = {v, target_ids, target_off, q, logits, ld, inv_temp, u_accept, u_sample, max_m,
+                       const float *lse, const float *u_accept, const float *u_sample, int32_t max_m,
+                       int32_t *n_accepted, int32_t *out_token, uint64_t *z_out, int n_threads) {
+    orc_logits_ctx c = {v, target_ids, target_off, q, logits, ld, inv_temp, u_accept, u_sample, lse, max_m,
                         n_accepted, out_token, z_out};
     orc_parallel(n_streams, n_threads, orc_logits_range, &c);
 }

@@ -68,7 +68,7 @@ def lib():
         L.tt_verify.restype = ctypes.c_int
         L.tt_verify_dense.argtypes = [i32, i32, P, P, P, i64, P, i64, P, P, i32, P, P, P, P, sz, P]
         L.tt_verify_dense.restype = ctypes.c_int
-        L.tt_verify_logits.argtypes = [i32, i32, P, P, P, P, i64, P, P, P, i32, P, P, P]
+        L.tt_verify_logits.argtypes = [i32, i32, P, P, P, P, i64, P, P, P, P, i32, P, P, P]
         L.tt_verify_logits.restype = ctypes.c_int
         L.tt_delta_histogram.argtypes = [i32, P, P, P, P, i32, P, P]
         L.tt_delta_histogram.restype = ctypes.c_int
@@ -282,9 +282,10 @@ def verify_dense(v: int, draft_ids, off, draft_probs, target_probs, u_accept, u_
 
 
 def verify_logits(v_t: int, target_ids, target_off, q, target_logits, inv_temperature, u_accept, u_sample,
-                  max_m: int, out=None, stream=None):
+                  max_m: int, lse=None, out=None, stream=None):
     """tt_verify_logits: target_logits is a 2-D row-major device tensor of bf16 (or its int16 / uint16
-    bit patterns); inv_temperature float32 [n_streams].  Returns (n_accepted, out_token)."""
+    bit patterns); inv_temperature float32 [n_streams]; lse optional float32 [rows], the rows'
+    log-sum-exp of logit * inv_temperature.  Returns (n_accepted, out_token)."""
     torch = _torch()
     i32, f32 = torch.int32, torch.float32
     n = int(target_off.numel()) - 1
@@ -301,7 +302,7 @@ def verify_logits(v_t: int, target_ids, target_off, q, target_logits, inv_temper
     st = lib().tt_verify_logits(n, int(v_t), _ptr(ids, i32, "target_ids"), _ptr(target_off, i32, "target_off"),
                                 _ptr(qq, f32, "q"), ctypes.c_void_p(target_logits.data_ptr()),
                                 int(target_logits.stride(0)), _ptr(inv_temperature, f32, "inv_temperature"),
-                                _ptr(ua, f32, "u_accept"), _ptr(u_sample, f32, "u_sample"), int(max_m),
+                                _ptr(lse, f32, "lse", allow_none=True), _ptr(ua, f32, "u_accept"), _ptr(u_sample, f32, "u_sample"), int(max_m),
                                 _ptr(nacc, i32, "n_accepted"), _ptr(tok, i32, "out_token"), _stream_handle(stream))
     _check(st, "tt_verify_logits")
     return out

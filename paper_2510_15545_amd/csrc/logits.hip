@@ -17,10 +17,13 @@
 //            after full acceptance the bonus row's e39 is sampled as is
 //   token  = first index whose prefix exceeds floor(u * Z); first largest x when Z = 0.
 //
-// One 1024-thread workgroup per stream walks its rows 0, 1, ... until the first rejection
-// (each row: a max pass, then a pass of chunk sums into LDS -- the second read mostly from
-// the caches), then wave 0 samples: the chunk sums lane-blocked, the crossing chunk's
-// e39 recomputed from its 1024 logits.  A lane reads 16 consecutive bf16 (two 16-byte loads).
+// One 1024-thread workgroup per stream.  Without normalisers it walks its rows 0, 1, ...
+// until the first rejection (each row: a max pass, then a pass of chunk sums into LDS -- the
+// second read mostly from the caches).  With per-row log-sum-exp values L from the caller
+// (an LM head can emit them with its logits) it uses m = L and S = 1: the acceptance test
+// needs one gathered logit per position and only the residual (or bonus) row is read, once.
+// Wave 0 samples: the chunk sums lane-blocked, the crossing chunk's e39 recomputed from its
+// 1024 logits.  A lane reads 16 consecutive bf16 (two 16-byte loads).
 #include "verify_core.h"
 
 namespace tt {
@@ -106,6 +109,106 @@ struct LogitsParams {
     int32_t nc, vec;
 };
 
+// e39 of one logit: floor(clamp(sexp(x - base), 0, 1) * 2^39)
+__device__ __forceinline__ uint64_t e39_of(uint32_t bits16, float it, float base) {
+    return q39(fminf(fmaxf(sexp(scaled(bits16, it) - base), 0.0f), 1.0f));
+}
+
+// Chunk sums of e39 over the row into sh_part (every wave, chunks wave, wave + 16, ...).
+__device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, bool vec, float it, float base,
+                                           uint64_t *sh_part) {
+    const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    for (int c = wave; c < nc; c += kWaves) {
+        uint32_t w[8];
+        const int x0 = c * kChunk + lane * 16;
+        load16(row, x0, v, vec, w);
+        uint64_t acc = 0;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) acc += x0 + k < v ? e39_of(elem(w, k), it, base) : 0ull;
+        acc = wave_inclusive_scan(acc);
+        if (lane == kWave - 1) sh_part[c] = acc;
+    }
+}
+
+// Inverse-CDF sample of a row from its chunk sums (one wave): the entry at t (if >= 0) is adj;
+// the first largest x when Z = 0.
+__device__ inline int sample_row(const uint16_t *row, int v, int nc, bool vec, float it, float base, int t,
+                                 uint64_t adj, uint64_t Z, float u, const uint64_t *sh_part) {
+    const int lane = threadIdx.x % kWave;
+    if (Z == 0) {
+        float bv = -INFINITY;
+        int bi = INT_MAX;
+        for (int x = lane; x < v; x += kWave) {
+            const float xv = scaled(row[x], it);
+            if (xv > bv) {
+                bv = xv;
+                bi = x;
+            }
+        }
+        for (int off = kWave / 2; off > 0; off >>= 1) {
+            const float ov = __shfl_xor(bv, off);
+            const int oi = __shfl_xor(bi, off);
+            if (ov > bv || (ov == bv && oi < bi)) {
+                bv = ov;
+                bi = oi;
+            }
+        }
+        return bi == INT_MAX ? 0 : bi;
+    }
+    const uint64_t T = exact_threshold(u, Z);
+    // chunk sums lane-blocked: lane l holds chunks [l*per, (l+1)*per)
+    const int per = (nc + kWave - 1) / kWave;
+    const int ca = lane * per < nc ? lane * per : nc;
+    const int cb = ca + per < nc ? ca + per : nc;
+    uint64_t local = 0;
+    for (int c = ca; c < cb; ++c) local += sh_part[c];
+    const uint64_t incl = wave_inclusive_scan(local);
+    const uint64_t excl = incl - local;
+    const unsigned long long hit = __ballot(excl <= T && T < incl);
+    if (hit == 0ull) return v - 1;  // only if the sums wrapped (rows longer than allowed)
+    const int owner = __ffsll(hit) - 1;
+    int cs = ca;
+    uint64_t base_sum = excl;
+    if (lane == owner) {
+        uint64_t run = excl;
+        for (int c = ca; c < cb; ++c) {
+            const uint64_t nx = run + sh_part[c];
+            if (nx > T) break;
+            cs = c + 1;
+            base_sum = nx;
+            run = nx;
+        }
+    }
+    cs = __builtin_amdgcn_readlane(cs, owner);
+    base_sum = lane_value(base_sum, owner);
+    // the crossing chunk: lane holds elements cs*1024 + lane*16 + [0, 16)
+    const int x0 = cs * kChunk + lane * 16;
+    uint32_t w[8];
+    load16(row, x0, v, vec, w);
+    uint64_t qv[16];
+    uint64_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        uint64_t e = x0 + k < v ? e39_of(elem(w, k), it, base) : 0ull;
+        if (x0 + k == t) e = adj;
+        qv[k] = e;
+        sum += e;
+    }
+    const uint64_t lincl = wave_inclusive_scan(sum) + base_sum;
+    const uint64_t lexcl = lincl - sum;
+    const unsigned long long lhit = __ballot(lexcl <= T && T < lincl);
+    if (lhit == 0ull) return v - 1;
+    const int tl = __ffsll(lhit) - 1;
+    uint64_t run = lexcl;
+    int k_at = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        run += qv[k];
+        k_at += run <= T ? 1 : 0;
+    }
+    return __builtin_amdgcn_readlane(x0 + k_at, tl);
+}
+
 __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
     const LogitsArgs &a = p.a;
     const int b = blockIdx.x;
@@ -113,12 +216,11 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     extern __shared__ uint64_t sh_part[];  // nc chunk sums of e39
     __shared__ float sh_red[kWaves];
-    __shared__ int sh_ok;
+    __shared__ int sh_ok, sh_r;
     __shared__ float sh_m;
     __shared__ int sh_next;  // 1: accepted, go to the next row
-    __shared__ uint64_t sh_Z;
+    __shared__ uint64_t sh_Z, sh_adj;
     __shared__ int sh_t;
-    __shared__ float sh_rt;
 
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
@@ -139,6 +241,54 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         if (tid == 0) {
             a.n_accepted[b] = -1;
             a.out_token[b] = -1;
+        }
+        return;
+    }
+    if (a.lse != nullptr) {
+        // normalisers given: the acceptance test from one gathered logit per position, then
+        // one pass over the residual (or bonus) row
+        if (wave == 0) {
+            int gamma = M;
+            for (int base = 0; base < M && gamma == M; base += kWave) {
+                const int j = base + lane;
+                bool rej = false;
+                if (j < M) {
+                    const int64_t r = t0 + b + j;
+                    const float P = fminf(fmaxf(sexp(scaled(a.logits[r * a.ld + a.target_ids[t0 + j]], it) -
+                                                     a.lse[r]), 0.0f), 1.0f);
+                    const float qj = a.q[t0 + j];
+                    rej = !(qj <= 0.0f || a.u_accept[t0 + j] < P / qj);
+                }
+                const unsigned long long rm = __ballot(rej);
+                if (rm != 0ull) gamma = base + __ffsll(rm) - 1;
+            }
+            if (lane == 0) sh_r = gamma;
+        }
+        __syncthreads();
+        const int r = sh_r;
+        const int64_t rr = t0 + b + r;
+        const uint16_t *row = a.logits + rr * a.ld;
+        const float L = a.lse[rr];
+        chunk_sums(row, v, nc, vec, it, L, sh_part);
+        __syncthreads();
+        if (wave != 0) return;
+        uint64_t local = 0;
+        for (int c = lane; c < nc; c += kWave) local += sh_part[c];
+        uint64_t Z = lane_value(wave_inclusive_scan(local), kWave - 1);
+        int t = -1;
+        uint64_t adj = 0;
+        if (r < M) {  // the rejected proposal loses q_r of its mass
+            t = a.target_ids[t0 + r];
+            const float Pt = fminf(fmaxf(sexp(scaled(row[t], it) - L), 0.0f), 1.0f);
+            adj = q39(fminf(fmaxf(Pt - a.q[t0 + r], 0.0f), 1.0f));
+            const uint64_t before = q39(Pt);
+            Z = Z - before + adj;
+            if (lane == 0) sh_part[t / kChunk] = sh_part[t / kChunk] - before + adj;
+        }
+        const int token = sample_row(row, v, nc, vec, it, L, t, adj, Z, a.u_sample[b], sh_part);
+        if (lane == 0) {
+            a.n_accepted[b] = r;
+            a.out_token[b] = token;
         }
         return;
     }
@@ -165,17 +315,7 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         __syncthreads();
         m = sh_m;
         // pass 2: chunk sums of e39
-        for (int c = wave; c < nc; c += kWaves) {
-            uint32_t w[8];
-            const int x0 = c * kChunk + lane * 16;
-            load16(row, x0, v, vec, w);
-            uint64_t acc = 0;
-#pragma unroll
-            for (int k = 0; k < 16; ++k)
-                acc += x0 + k < v ? q39(sexp(scaled(elem(w, k), it) - m)) : 0ull;
-            acc = wave_inclusive_scan(acc);
-            if (lane == kWave - 1) sh_part[c] = acc;
-        }
+        chunk_sums(row, v, nc, vec, it, m, sh_part);
         __syncthreads();
         // S, the acceptance test of position j, and the residual's entry at t_j
         if (wave == 0) {
@@ -185,119 +325,33 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
             if (lane == 0) {
                 const float S = q39_to_f32(Sq);
                 int next = 0;
-                uint64_t Z = Sq;
+                uint64_t Z = Sq, adj = 0;
                 int t = -1;
-                float et = 0.0f, rt = 0.0f;
                 if (j < M) {
                     t = a.target_ids[t0 + j];
                     const float qj = a.q[t0 + j];
-                    et = sexp(scaled(row[t], it) - m);
+                    const float et = sexp(scaled(row[t], it) - m);
                     const float P = et / S;
                     if (qj <= 0.0f || a.u_accept[t0 + j] < P / qj) {
                         next = 1;
                     } else {
-                        rt = fminf(fmaxf(et - qj * S, 0.0f), 1.0f);  // NaN -> 0
-                        const uint64_t before = q39(et), after = q39(rt);
-                        Z = Sq - before + after;
-                        sh_part[t / kChunk] = sh_part[t / kChunk] - before + after;
+                        const float rt = fminf(fmaxf(et - qj * S, 0.0f), 1.0f);  // NaN -> 0
+                        const uint64_t before = q39(et);
+                        adj = q39(rt);
+                        Z = Sq - before + adj;
+                        sh_part[t / kChunk] = sh_part[t / kChunk] - before + adj;
                     }
                 }
                 sh_next = next;
                 sh_Z = Z;
                 sh_t = next ? -1 : t;
-                sh_rt = rt;
+                sh_adj = adj;
             }
         }
         __syncthreads();
         if (sh_next) continue;
-        // sample row j (wave 0)
         if (wave == 0) {
-            const uint64_t Z = sh_Z;
-            const int t = sh_t;
-            int token = 0;
-            if (Z == 0) {  // no mass: the first largest x
-                float bv = -INFINITY;
-                int bi = INT_MAX;
-                for (int x = lane; x < v; x += kWave) {
-                    const float xv = scaled(row[x], it);
-                    if (xv > bv) {
-                        bv = xv;
-                        bi = x;
-                    }
-                }
-                for (int off = kWave / 2; off > 0; off >>= 1) {
-                    const float ov = __shfl_xor(bv, off);
-                    const int oi = __shfl_xor(bi, off);
-                    if (ov > bv || (ov == bv && oi < bi)) {
-                        bv = ov;
-                        bi = oi;
-                    }
-                }
-                token = bi == INT_MAX ? 0 : bi;
-            } else {
-                const uint64_t T = exact_threshold(a.u_sample[b], Z);
-                // chunk sums lane-blocked: lane l holds chunks [l*per, (l+1)*per)
-                const int per = (nc + kWave - 1) / kWave;
-                const int ca = lane * per < nc ? lane * per : nc;
-                const int cb = ca + per < nc ? ca + per : nc;
-                uint64_t local = 0;
-                for (int c = ca; c < cb; ++c) local += sh_part[c];
-                const uint64_t incl = wave_inclusive_scan(local);
-                const uint64_t excl = incl - local;
-                const unsigned long long hit = __ballot(excl <= T && T < incl);
-                int cs = 0;
-                uint64_t base = 0;
-                if (hit != 0ull) {
-                    const int owner = __ffsll(hit) - 1;
-                    if (lane == owner) {
-                        uint64_t run = excl;
-                        cs = ca;
-                        base = excl;
-                        for (int c = ca; c < cb; ++c) {
-                            const uint64_t nx = run + sh_part[c];
-                            if (nx > T) break;
-                            cs = c + 1;
-                            base = nx;
-                            run = nx;
-                        }
-                    }
-                    cs = __builtin_amdgcn_readlane(cs, owner);
-                    base = lane_value(base, owner);
-                    // the crossing chunk: lane holds elements cs*1024 + lane*16 + [0, 16)
-                    const int x0 = cs * kChunk + lane * 16;
-                    uint32_t w[8];
-                    load16(row, x0, v, vec, w);
-                    const float mm = sh_m;
-                    const uint64_t adj = q39(sh_rt);
-                    uint64_t qv[16];
-                    uint64_t sum = 0;
-#pragma unroll
-                    for (int k = 0; k < 16; ++k) {
-                        uint64_t e = x0 + k < v ? q39(sexp(scaled(elem(w, k), it) - mm)) : 0ull;
-                        if (x0 + k == t) e = adj;
-                        qv[k] = e;
-                        sum += e;
-                    }
-                    const uint64_t lincl = wave_inclusive_scan(sum) + base;
-                    const uint64_t lexcl = lincl - sum;
-                    const unsigned long long lhit = __ballot(lexcl <= T && T < lincl);
-                    if (lhit != 0ull) {
-                        const int tl = __ffsll(lhit) - 1;
-                        uint64_t run = lexcl;
-                        int k_at = 0;
-#pragma unroll
-                        for (int k = 0; k < 16; ++k) {
-                            run += qv[k];
-                            k_at += run <= T ? 1 : 0;
-                        }
-                        token = __builtin_amdgcn_readlane(x0 + k_at, tl);
-                    } else {
-                        token = v - 1;
-                    }
-                } else {
-                    token = v - 1;  // only if the sums wrapped (rows longer than allowed)
-                }
-            }
+            const int token = sample_row(row, v, nc, vec, it, m, sh_t, sh_adj, sh_Z, a.u_sample[b], sh_part);
             if (lane == 0) {
                 a.n_accepted[b] = j;
                 a.out_token[b] = token;

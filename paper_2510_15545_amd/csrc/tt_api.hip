@@ -165,8 +165,8 @@ int tt_verify_dense(int32_t n_streams, int32_t v, const int32_t *draft_ids, cons
 
 int tt_verify_logits(int32_t n_streams, int32_t v_t, const int32_t *target_ids, const int32_t *target_off,
                      const float *q, const uint16_t *target_logits, int64_t target_ld, const float *inv_temperature,
-                     const float *u_accept, const float *u_sample, int32_t max_m, int32_t *n_accepted,
-                     int32_t *out_token, void *stream) {
+                     const float *lse, const float *u_accept, const float *u_sample, int32_t max_m,
+                     int32_t *n_accepted, int32_t *out_token, void *stream) {
     if (n_streams < 0 || v_t < 1 || target_ld < v_t || max_m < 0 || max_m > kMaxVerifyLen) return TT_EINVAL;
     if (v_t > kMaxLogitsRow) return TT_EUNSUPPORTED;
     if (n_streams == 0) return TT_OK;
@@ -182,6 +182,7 @@ int tt_verify_logits(int32_t n_streams, int32_t v_t, const int32_t *target_ids, 
     a.logits = target_logits;
     a.ld = target_ld;
     a.inv_temp = inv_temperature;
+    a.lse = lse;
     a.u_accept = u_accept;
     a.u_sample = u_sample;
     a.max_m = max_m;

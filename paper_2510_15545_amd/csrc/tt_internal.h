@@ -106,6 +106,7 @@ struct LogitsArgs {
     const uint16_t *logits;  // bf16 bit patterns
     int64_t ld;
     const float *inv_temp, *u_accept, *u_sample;
+    const float *lse;  // per-row log-sum-exp of x, or nullptr
     int32_t max_m;
     int32_t *n_accepted, *out_token;
 };

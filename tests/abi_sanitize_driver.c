@@ -57,8 +57,9 @@ int main(void) {
     EXPECT(tt_vocab_intersection(&big, W, 1 << 20, &v, W, 1 << 20, D, D, NULL) == TT_EUNSUPPORTED);
     EXPECT(tt_tli_proposal(1, 10, 10, D, D, F, 9, F, 10, NULL) == TT_EINVAL);
     EXPECT(tt_tli_proposal(0, 10, 10, NULL, NULL, NULL, 10, NULL, 10, NULL) == TT_OK);
-    EXPECT(tt_verify_logits(1, 10, D, D, F, (const uint16_t *)W, 9, F, F, F, 4, D, D, NULL) == TT_EINVAL);
-    EXPECT(tt_verify_logits(0, 10, NULL, NULL, NULL, NULL, 10, NULL, NULL, NULL, 4, NULL, NULL, NULL) == TT_OK);
+    EXPECT(tt_verify_logits(1, 10, D, D, F, (const uint16_t *)W, 9, F, NULL, F, F, 4, D, D, NULL) == TT_EINVAL);
+    EXPECT(tt_verify_logits(0, 10, NULL, NULL, NULL, NULL, 10, NULL, NULL, NULL, NULL, 4, NULL, NULL, NULL) ==
+           TT_OK);
     printf("done\n");
     return 0;
 }

@@ -36,8 +36,8 @@ uint64_t orc_threshold(float u, uint64_t Z);
 float orc_sexp(float x);
 void orc_verify_logits(int32_t n_streams, int32_t v, const int32_t *target_ids, const int32_t *target_off,
                        const float *q, const uint16_t *logits, int64_t ld, const float *inv_temp,
-                       const float *u_accept, const float *u_sample, int32_t max_m, int32_t *n_accepted,
-                       int32_t *out_token, uint64_t *z_out, int n_threads);
+                       const float *lse, const float *u_accept, const float *u_sample, int32_t max_m,
+                       int32_t *n_accepted, int32_t *out_token, uint64_t *z_out, int n_threads);
 
 static uint32_t rng_state = 12345u;
 static uint32_t next_u32(void) { /* xorshift32 */
@@ -155,7 +155,9 @@ int main(void) {
     float lq[5] = {0.5f, 0.9f, 0.1f, 0.2f, 0.3f}, lit[3] = {1.0f, 1.4f, 2.0f}, lus[3] = {0.25f, 0.75f, 0.5f};
     int32_t lnacc[3], ltok[3];
     uint64_t lz[3];
-    orc_verify_logits(3, VT, lids, loff, lq, lg, VT, lit, sua, lus, 4, lnacc, ltok, lz, 2);
+    orc_verify_logits(3, VT, lids, loff, lq, lg, VT, lit, NULL, sua, lus, 4, lnacc, ltok, lz, 2);
+    float llse[8] = {3.0f, 3.5f, 2.0f, 4.0f, 3.0f, 3.0f, 3.0f, 3.0f};
+    orc_verify_logits(3, VT, lids, loff, lq, lg, VT, lit, llse, sua, lus, 4, lnacc, ltok, lz, 2);
     printf("logits %d/%d %d/%d %d/%d sexp %.7g\n", lnacc[0], ltok[0], lnacc[1], ltok[1], lnacc[2], ltok[2],
            (double)orc_sexp(-1.0f));
     free(lg);

@@ -158,7 +158,8 @@ def test_invalid_arguments_return_before_launch():
     assert isect(vd=ctypes.byref(big)) == tt.TT_EUNSUPPORTED
 
     def logits(n=1, v=10, ld=10, max_m=4, it=dummy, lg=dummy):
-        return L.tt_verify_logits(n, v, dummy, dummy, dummy, lg, ld, it, dummy, dummy, max_m, dummy, dummy, None)
+        return L.tt_verify_logits(n, v, dummy, dummy, dummy, lg, ld, it, None, dummy, dummy, max_m, dummy, dummy,
+                                  None)
     assert logits(n=-1) == tt.TT_EINVAL
     assert logits(v=0) == tt.TT_EINVAL
     assert logits(ld=9) == tt.TT_EINVAL

@@ -1,12 +1,14 @@
 """tt_verify_logits (verification from bf16 logits and a temperature) against the oracle, bit for
 bit: ragged and aligned rows, padded and odd strides, temperatures, NaN and -inf logits, forced
-acceptances (several rows per stream), sentinel streams, and the benchmark's row width."""
+acceptances (several rows per stream), sentinel streams, and the benchmark's row width; each with
+and without caller-supplied per-row log-sum-exp values (exact ones, and shifted ones that push
+P above 1 or below the true softmax)."""
 import numpy as np
 import pytest
 
 import oracle
 from gpu_util import to_dev
-from test_oracle_logits import bf16_bits
+from test_oracle_logits import bf16_bits, row_lse
 
 pytestmark = pytest.mark.gpu
 
@@ -33,16 +35,24 @@ def logits_case(n, V, ld=None, seed=0, max_m=8):
     return ids, off, q, bits, it, ua, us, Ms
 
 
-def run_both(V, case, max_m):
+def case_lse(V, case, shift=0.0):
+    """fp32 log-sum-exp of each row's logit * inv_temp (its stream's), plus shift."""
+    ids, off, q, bits, it, ua, us, Ms = case
+    row_it = np.repeat(it, Ms + 1)
+    return (row_lse(bits[:, :V], row_it) + np.float32(shift)).astype(np.float32)
+
+
+def run_both(V, case, max_m, lse=None):
     import torch
 
     import paper_2510_15545_amd as tt
 
     ids, off, q, bits, it, ua, us, Ms = case
     nacc, tok = tt.verify_logits(V, to_dev(ids), to_dev(off), to_dev(q), to_dev(bits.view(np.int16)),
-                                 to_dev(it), to_dev(ua), to_dev(us), max_m)
+                                 to_dev(it), to_dev(ua), to_dev(us), max_m,
+                                 lse=None if lse is None else to_dev(lse))
     torch.cuda.synchronize()
-    o_nacc, o_tok, _ = oracle.verify_logits(V, ids, off, q, bits, it, ua, us, max_m=max_m)
+    o_nacc, o_tok, _ = oracle.verify_logits(V, ids, off, q, bits, it, ua, us, max_m=max_m, lse=lse)
     assert np.array_equal(nacc.cpu().numpy(), o_nacc), np.nonzero(nacc.cpu().numpy() != o_nacc)[0][:5]
     assert np.array_equal(tok.cpu().numpy(), o_tok), np.nonzero(tok.cpu().numpy() != o_tok)[0][:5]
     return o_nacc, Ms
@@ -55,6 +65,15 @@ def test_logits_parity(n, V, ld):
     assert (nacc > 0).sum() > 0 and (nacc < Ms).sum() > 0  # both acceptances and rejections occur
 
 
+@pytest.mark.parametrize("shift", [0.0, -0.7, 0.4])
+@pytest.mark.parametrize("n,V,ld", [(37, 1000, None), (20, 4099, 4101), (300, 640, None)])
+def test_logits_parity_with_lse(n, V, ld, shift):
+    print(f"[case] logits+lse n={n} V={V} ld={ld} shift={shift}", flush=True)
+    case = logits_case(n, V, ld, seed=3)
+    nacc, Ms = run_both(V, case, 8, lse=case_lse(V, case, shift))
+    assert (nacc > 0).sum() > 0 and (nacc < Ms).sum() > 0
+
+
 def test_logits_sentinels_and_degenerate_rows():
     print("[case] logits sentinels", flush=True)
     V = 2000
@@ -65,10 +84,16 @@ def test_logits_sentinels_and_degenerate_rows():
     bits[off[3] + 3 + Ms[3]] = 0xFF80             # stream 3's last row all -inf: Z = 0 if reached
     bits[off[4] + 4] = 0x7FC0                     # stream 4's first row all NaN
     q[off[5]:off[6]] = 0.0                        # q = 0 keeps every proposal of stream 5
-    run_both(V, (ids, off, q, bits, it, ua, us, Ms), 4)
+    case = (ids, off, q, bits, it, ua, us, Ms)
+    run_both(V, case, 4)
+    lse = case_lse(V, case)
+    lse[off[6] + 6] = np.nan                      # stream 6's first row: a NaN normaliser, no mass
+    run_both(V, case, 4, lse=lse)
 
 
 def test_logits_at_the_benchmark_width():
     print("[case] logits 256 streams V=151936", flush=True)
     V = 151_936
-    run_both(V, logits_case(256, V, seed=9, max_m=3), 3)
+    case = logits_case(256, V, seed=9, max_m=3)
+    run_both(V, case, 3)
+    run_both(V, case, 3, lse=case_lse(V, case))

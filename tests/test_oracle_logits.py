@@ -6,7 +6,9 @@ The software exponential is checked against the C library's exp of the same fp32
 laws computed independently in float64: with a one-hot proposal of mass 1 the emitted token
 follows softmax(logit / T), and after a rejection it follows the closed form of the
 transferred-proposal law (min(1, p/q) at the proposal, the rest in proportion); an exactly
-representable softmax fixes the acceptance boundary; invalid streams give sentinels.
+representable softmax fixes the acceptance boundary; invalid streams give sentinels.  With
+caller-supplied log-sum-exp values the same laws hold, and a normaliser that makes the softmax
+exact fixes the boundary there too.
 """
 import math
 
@@ -31,6 +33,16 @@ def softmax64(x):
     x = np.asarray(x, np.float64)
     e = np.exp(x - x.max())
     return e / e.sum()
+
+
+def row_lse(bits, row_it):
+    """Each row's log-sum-exp of bf16 logit * inv_temp (NaN as -inf), in float64, rounded to fp32."""
+    x = bf16_value(bits).astype(np.float32) * np.asarray(row_it, np.float32)[:, None]
+    x = np.where(np.isnan(x), -np.inf, x).astype(np.float64)
+    m = x.max(axis=1)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        s = np.log(np.exp(x - np.where(np.isfinite(m), m, 0)[:, None]).sum(axis=1)) + m
+    return s.astype(np.float32)
 
 
 def ulps(a: np.float32, b: float) -> float:
@@ -59,8 +71,9 @@ def one_position_batch(rng, logits_rows, q, N, t=None):
     return V, ids, off, np.full(N, q, np.float32), rows
 
 
+@pytest.mark.parametrize("with_lse", [False, True])
 @pytest.mark.parametrize("temp", [1.0, 0.7])
-def test_emitted_token_follows_the_tempered_softmax(orc, temp):
+def test_emitted_token_follows_the_tempered_softmax(orc, temp, with_lse):
     """q = 1 at the proposal: accept with probability p(t), else the residual (p without t,
     renormalised), so the emitted token's law is p = softmax(logit / T)."""
     rng = np.random.default_rng(80)
@@ -68,21 +81,26 @@ def test_emitted_token_follows_the_tempered_softmax(orc, temp):
     bits = bf16_bits(rng.normal(0, 1.5, (2, V)).astype(np.float32))
     it = np.float32(1.0 / temp)
     V, ids, off, q, rows = one_position_batch(rng, bits, 1.0, N, t)
-    nacc, tok, _ = orc.verify_logits(V, ids, off, q, rows, np.full(N, it, np.float32), u24(rng, N), u24(rng, N))
+    lse = row_lse(rows, np.full(len(rows), it)) if with_lse else None
+    nacc, tok, _ = orc.verify_logits(V, ids, off, q, rows, np.full(N, it, np.float32), u24(rng, N), u24(rng, N),
+                                     lse=lse)
     first = np.where(nacc > 0, t, tok)
     p = softmax64(bf16_value(bits[0]) * it)
     assert chi2_pvalue(np.bincount(first, minlength=V), p) > ALPHA
     assert abs(np.mean(nacc) - p[t]) < 5 * math.sqrt(p[t] * (1 - p[t]) / N)
 
 
-def test_rejection_law_closed_form(orc):
+@pytest.mark.parametrize("with_lse", [False, True])
+def test_rejection_law_closed_form(orc, with_lse):
     """One-hot proposal of mass a at t: P(out = t) = min(1, p(t)/a), any other x in proportion
     to p(x) -- the transferred-proposal law, here with p = softmax(logit)."""
     rng = np.random.default_rng(81)
     V, N, t, a = 5, 200_000, 1, 0.6
     bits = bf16_bits(np.array([[0.2, 0.9, -0.4, 0.0, 0.5], [0.0] * 5], np.float32))
     V, ids, off, q, rows = one_position_batch(rng, bits, a, N, t)
-    nacc, tok, _ = orc.verify_logits(V, ids, off, q, rows, np.ones(N, np.float32), u24(rng, N), u24(rng, N))
+    lse = row_lse(rows, np.ones(len(rows))) if with_lse else None
+    nacc, tok, _ = orc.verify_logits(V, ids, off, q, rows, np.ones(N, np.float32), u24(rng, N), u24(rng, N),
+                                     lse=lse)
     out = np.where(nacc > 0, t, tok)
     p = softmax64(bf16_value(bits[0]))
     keep = min(1.0, p[t] / a)
@@ -103,6 +121,27 @@ def test_exact_softmax_fixes_the_accept_boundary(orc):
         assert nacc[0] == want
         if want == 0:  # residual: p(t) - q < 0, so t has no mass; Z = 7 * 2^39; u_sample = 0 -> first token
             assert int(z[0]) == 7 * 2 ** 39 and tok[0] == 0
+
+
+def test_exact_normaliser_fixes_the_accept_boundary(orc):
+    """The normaliser is taken as given: logit 0 with L = 0 gives P = sexp(0) = 1 whatever the
+    other logits are, so with q = 1/2 every u accepts; with L = ln 2 (fp32) and q = 1,
+    P = sexp(-L) is within an ulp of 1/2 and u just below P accepts, u = P rejects."""
+    V = 4
+    bits = bf16_bits(np.array([[0.0, -5.0, -5.0, -5.0], [0.0] * 4], np.float32))
+    one = lambda lse0, qv, u: orc.verify_logits(V, np.array([0], np.int32), np.array([0, 1], np.int32),
+                                                np.array([qv], np.float32), bits, np.ones(1, np.float32),
+                                                np.array([u], np.float32), np.array([0.0], np.float32),
+                                                lse=np.array([lse0, 0.0], np.float32))
+    assert one(0.0, 0.5, 1.0 - 2.0 ** -24)[0][0] == 1
+    L = np.float32(math.log(2.0))
+    P = float(orc.sexp(np.float32(-L)))
+    assert abs(P - 0.5) <= 2.0 ** -24
+    below = np.nextafter(np.float32(P), np.float32(0))
+    assert one(L, 1.0, below)[0][0] == 1 and one(L, 1.0, np.float32(P))[0][0] == 0
+    # rejected: the residual row 0 has mass only off the proposal; u_sample = 0 -> index 1
+    nacc, tok, z = one(L, 1.0, np.float32(P))
+    assert tok[0] == 1 and int(z[0]) > 0
 
 
 def test_sentinels_nan_and_empty_rows(orc):
