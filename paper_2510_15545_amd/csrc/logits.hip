@@ -4,7 +4,7 @@
 // probability rows.
 //
 // Arithmetic (every step specified, so any summation order gives the same token):
-//   x      = fp32(bf16 logit) * inv_temp; NaN counts as minus infinity
+//   x      = fp32(bf16 logit) * inv_temp; NaN counts as minus infinity (no mass, never the max)
 //   m      = max x over the row
 //   e(x)   = sexp(x - m): Cody-Waite reduction x = k ln2 + r (k = rint(x log2 e), r by two
 //            fused multiply-adds), the degree-6 Taylor polynomial of exp(r) by Horner's
@@ -77,10 +77,10 @@ __device__ inline float q39_to_f32(uint64_t n) {
     return ldexpf((float)mant, sh - 39);
 }
 
-__device__ __forceinline__ float scaled(uint32_t bits16, float it) {
-    const float x = bf16_value(bits16) * it;
-    return x == x ? x : -INFINITY;
-}
+// x = logit * inv_temp.  A NaN x is left as is: it acts as minus infinity everywhere it is
+// used -- sexp returns 0 for a NaN argument (as for -inf - m), fmaxf ignores it in the max
+// pass, and it never compares greater in the first-argmax fallback.
+__device__ __forceinline__ float scaled(uint32_t bits16, float it) { return bf16_value(bits16) * it; }
 
 // The 16 logits of a lane in chunk c (elements c*1024 + lane*16 + k, zero bits past v).
 __device__ __forceinline__ void load16(const uint16_t *row, int x0, int v, bool vec, uint32_t (&w)[8]) {
@@ -114,19 +114,28 @@ __device__ __forceinline__ uint64_t e39_of(uint32_t bits16, float it, float base
     return q39(fminf(fmaxf(sexp(scaled(bits16, it) - base), 0.0f), 1.0f));
 }
 
-// Chunk sums of e39 over the row into sh_part (every wave, chunks wave, wave + 16, ...).
+// Chunk sums of e39 over the row into sh_part (every wave, chunks wave, wave + 16, ...; the
+// next chunk's loads are issued before the current chunk's arithmetic).
 __device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, bool vec, float it, float base,
                                            uint64_t *sh_part) {
     const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    uint32_t w[8] = {}, nx[8] = {};
+    if (wave < nc) load16(row, wave * kChunk + lane * 16, v, vec, w);
     for (int c = wave; c < nc; c += kWaves) {
-        uint32_t w[8];
         const int x0 = c * kChunk + lane * 16;
-        load16(row, x0, v, vec, w);
+        if (c + kWaves < nc) load16(row, x0 + kWaves * kChunk, v, vec, nx);
         uint64_t acc = 0;
+        if (x0 + 16 <= v) {
 #pragma unroll
-        for (int k = 0; k < 16; ++k) acc += x0 + k < v ? e39_of(elem(w, k), it, base) : 0ull;
+            for (int k = 0; k < 16; ++k) acc += e39_of(elem(w, k), it, base);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 16; ++k) acc += x0 + k < v ? e39_of(elem(w, k), it, base) : 0ull;
+        }
         acc = wave_inclusive_scan(acc);
         if (lane == kWave - 1) sh_part[c] = acc;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) w[k] = nx[k];
     }
 }
 
@@ -296,13 +305,21 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         const uint16_t *row = a.logits + (int64_t)(t0 + b + j) * a.ld;
         // pass 1: the row's largest x
         float m = -INFINITY;
+        uint32_t w[8] = {}, nx[8] = {};
+        if (wave < nc) load16(row, wave * kChunk + lane * 16, v, vec, w);
         for (int c = wave; c < nc; c += kWaves) {
-            uint32_t w[8];
             const int x0 = c * kChunk + lane * 16;
-            load16(row, x0, v, vec, w);
+            if (c + kWaves < nc) load16(row, x0 + kWaves * kChunk, v, vec, nx);
+            if (x0 + 16 <= v) {
 #pragma unroll
-            for (int k = 0; k < 16; ++k)
-                if (x0 + k < v) m = fmaxf(m, scaled(elem(w, k), it));
+                for (int k = 0; k < 16; ++k) m = fmaxf(m, scaled(elem(w, k), it));
+            } else {
+#pragma unroll
+                for (int k = 0; k < 16; ++k)
+                    if (x0 + k < v) m = fmaxf(m, scaled(elem(w, k), it));
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k) w[k] = nx[k];
         }
         for (int off = kWave / 2; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
         if (lane == 0) sh_red[wave] = m;
