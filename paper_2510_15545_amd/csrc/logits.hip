@@ -40,9 +40,10 @@ constexpr int kChunk = 1024;  // logits per chunk: one wave, 16 per lane
 
 __device__ __forceinline__ float bf16_value(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
 
-// exp(x) for x <= 0 as specified above (0 for x < -87 and NaN)
-__device__ __forceinline__ float sexp(float x) {
-    if (!(x >= -87.0f)) return 0.0f;
+// The reduction, polynomial and scaling of sexp without its cut-off (for any x; garbage, inf
+// or NaN where x is below -87 or not finite).  Branch-free, so a wave takes no divergent
+// branch per logit.
+__device__ __forceinline__ float sexp_core(float x) {
     const float kf = rintf(x * 0x1.715476p+0f);
     float r = fmaf(-kf, 0x1.62e430p-1f, x);
     r = fmaf(-kf, -0x1.05c610p-29f, r);
@@ -56,12 +57,15 @@ __device__ __forceinline__ float sexp(float x) {
     return ldexpf(p, (int)kf);
 }
 
+// exp(x) for x <= 0 as specified above (0 for x < -87 and NaN)
+__device__ __forceinline__ float sexp(float x) { return x >= -87.0f ? sexp_core(x) : 0.0f; }
+
 // floor(e * 2^39) for e in [0, 1] (exact: the high word is trunc(e * 2^7), the low word the
-// remainder scaled by 2^32)
+// fraction s - floor(s), exact for s in [0, 128], scaled by 2^32)
 __device__ __forceinline__ uint64_t q39(float e) {
     const float s = e * 128.0f;
     const uint32_t hi = (uint32_t)s;
-    const uint32_t lo = (uint32_t)((s - (float)hi) * 4294967296.0f);
+    const uint32_t lo = (uint32_t)(__builtin_amdgcn_fractf(s) * 4294967296.0f);
     return ((uint64_t)hi << 32) | lo;
 }
 
@@ -109,9 +113,12 @@ struct LogitsParams {
     int32_t nc, vec;
 };
 
-// e39 of one logit: floor(clamp(sexp(x - base), 0, 1) * 2^39)
+// e39 of one logit: floor(clamp(sexp(x - base), 0, 1) * 2^39).  The argument is raised to at
+// least -100 (NaN becomes -100) and the cut-off of sexp left out: for an argument in
+// [-100, -87) sexp_core gives at most 1.42 * 2^-125, which the floor maps to 0, as it does the
+// specified 0; from -87 up the two agree; +inf and NaN results are clamped as before.
 __device__ __forceinline__ uint64_t e39_of(uint32_t bits16, float it, float base) {
-    return q39(fminf(fmaxf(sexp(scaled(bits16, it) - base), 0.0f), 1.0f));
+    return q39(fminf(fmaxf(sexp_core(fmaxf(scaled(bits16, it) - base, -100.0f)), 0.0f), 1.0f));
 }
 
 // Chunk sums of e39 over the row into sh_part (every wave, chunks wave, wave + 16, ...; the

@@ -74,6 +74,22 @@ def test_logits_parity_with_lse(n, V, ld, shift):
     assert (nacc > 0).sum() > 0 and (nacc < Ms).sum() > 0
 
 
+@pytest.mark.parametrize("with_lse", [False, True])
+def test_logits_wide_range(with_lse):
+    """Logits spread over [-130, 5]: every x - m in the exponential's cut-off band [-100, -87),
+    below it, and near 0, so each e39 on both sides of the cut-off is compared."""
+    print(f"[case] logits wide range lse={with_lse}", flush=True)
+    V = 3000
+    ids, off, q, bits, it, ua, us, Ms = logits_case(40, V, seed=11, max_m=4)
+    rng = np.random.default_rng(12)
+    x = rng.uniform(-130.0, 5.0, bits.shape).astype(np.float32)
+    x[rng.random(x.shape) < 0.01] = -88.0  # exact bf16 values just past the cut-off
+    bits = bf16_bits(x)
+    it[:] = 1.0
+    case = (ids, off, q, bits, it, ua, us, Ms)
+    run_both(V, case, 4, lse=case_lse(V, case) if with_lse else None)
+
+
 def test_logits_sentinels_and_degenerate_rows():
     print("[case] logits sentinels", flush=True)
     V = 2000
