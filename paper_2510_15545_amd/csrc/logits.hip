@@ -233,7 +233,7 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
     extern __shared__ uint64_t sh_part[];  // nc chunk sums of e39
     __shared__ float sh_red[kWaves];
     __shared__ int sh_ok, sh_r;
-    __shared__ float sh_m;
+    __shared__ float sh_m, sh_L, sh_q, sh_P;
     __shared__ int sh_next;  // 1: accepted, go to the next row
     __shared__ uint64_t sh_Z, sh_adj;
     __shared__ int sh_t;
@@ -263,28 +263,48 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
     if (a.lse != nullptr) {
         // normalisers given: the acceptance test from one gathered logit per position, then
         // one pass over the residual (or bonus) row
+        // (the rejecting lane's L, t, q and P, or the bonus row's L, go to LDS with gamma, so
+        // the row pass and the residual entry need no further dependent load)
         if (wave == 0) {
-            int gamma = M;
+            const float L_bonus = a.lse[t0 + b + M];
+            int gamma = M, t_r = -1;
+            float L_r = L_bonus, q_r = 0.0f, P_r = 0.0f;
             for (int base = 0; base < M && gamma == M; base += kWave) {
                 const int j = base + lane;
                 bool rej = false;
+                int tj = 0;
+                float Lj = 0.0f, qj = 0.0f, P = 0.0f;
                 if (j < M) {
                     const int64_t r = t0 + b + j;
-                    const float P = fminf(fmaxf(sexp(scaled(a.logits[r * a.ld + a.target_ids[t0 + j]], it) -
-                                                     a.lse[r]), 0.0f), 1.0f);
-                    const float qj = a.q[t0 + j];
+                    tj = a.target_ids[t0 + j];
+                    Lj = a.lse[r];
+                    P = fminf(fmaxf(sexp(scaled(a.logits[r * a.ld + tj], it) - Lj), 0.0f), 1.0f);
+                    qj = a.q[t0 + j];
                     rej = !(qj <= 0.0f || a.u_accept[t0 + j] < P / qj);
                 }
                 const unsigned long long rm = __ballot(rej);
-                if (rm != 0ull) gamma = base + __ffsll(rm) - 1;
+                if (rm != 0ull) {
+                    const int src = __ffsll(rm) - 1;
+                    gamma = base + src;
+                    t_r = __builtin_amdgcn_readlane(tj, src);
+                    L_r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(Lj), src));
+                    q_r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(qj), src));
+                    P_r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(P), src));
+                }
             }
-            if (lane == 0) sh_r = gamma;
+            if (lane == 0) {
+                sh_r = gamma;
+                sh_t = t_r;
+                sh_L = L_r;
+                sh_q = q_r;
+                sh_P = P_r;
+            }
         }
         __syncthreads();
         const int r = sh_r;
         const int64_t rr = t0 + b + r;
         const uint16_t *row = a.logits + rr * a.ld;
-        const float L = a.lse[rr];
+        const float L = sh_L;
         chunk_sums(row, v, nc, vec, it, L, sh_part);
         __syncthreads();
         if (wave != 0) return;
@@ -294,9 +314,9 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         int t = -1;
         uint64_t adj = 0;
         if (r < M) {  // the rejected proposal loses q_r of its mass
-            t = a.target_ids[t0 + r];
-            const float Pt = fminf(fmaxf(sexp(scaled(row[t], it) - L), 0.0f), 1.0f);
-            adj = q39(fminf(fmaxf(Pt - a.q[t0 + r], 0.0f), 1.0f));
+            t = sh_t;
+            const float Pt = sh_P;  // clamp(sexp(x_t - L), 0, 1), as the chunk sums count it
+            adj = q39(fminf(fmaxf(Pt - sh_q, 0.0f), 1.0f));
             const uint64_t before = q39(Pt);
             Z = Z - before + adj;
             if (lane == 0) sh_part[t / kChunk] = sh_part[t / kChunk] - before + adj;
