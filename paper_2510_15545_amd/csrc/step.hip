@@ -15,7 +15,10 @@
 // Compared with three launches this removes two kernel boundaries and the global round
 // trips of map and q, and every global load of steps 1-3 is issued at the start.
 #include "dtw_rows.h"
+#include "stamps.h"
 #include "verify_core.h"
+
+TT_STAMPS_TABLE(step)
 
 namespace tt {
 namespace {
@@ -27,7 +30,9 @@ constexpr int kThreads = 1024;
 constexpr int kStageThreads = 256;                // waves 0-3 stage tokens
 constexpr int kDraftPrefetch = 256;               // threads 256..319 gather P_d(d_i)
 constexpr int kTargetPrefetch = 320;              // threads 320..383 gather P_t(t_j), u_j, t_j
-constexpr size_t kPartLdsMax = 64 * 1024;
+// dynamic LDS of the streaming part (chunk sums): at most what gfx950's 160 KiB per workgroup
+// leaves beside the largest static use (40 KiB at 32-byte token slots)
+constexpr size_t kDynLdsMax = 160 * 1024 - 40 * 1024;
 
 struct SParams {
     StepArgs s;
@@ -49,16 +54,18 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     __shared__ float ua[rows::kMaxSide];   // acceptance uniforms
     __shared__ int tid_t[rows::kMaxSide];  // target ids
     __shared__ int sh_votes[kThreads / kWave];
-    __shared__ int sh_gamma, sh_ok, sh_rtok;
-    __shared__ float sh_rq;
+    __shared__ int sh_gamma, sh_ok, sh_rtok, sh_next;
+    __shared__ float sh_rq, sh_rp;
     extern __shared__ uint64_t sh_part[];  // Q62 chunk sums of the selected row
 
     const int b = blockIdx.x;
     const int tid = threadIdx.x, lane = tid % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: wave-level branches stay scalar
+    TT_STAMP(0);
     const int d0 = al.draft_off[b], K = al.draft_off[b + 1] - d0;
     const int t0 = al.target_off[b], M = al.target_off[b + 1] - t0;
     const float us = ve.u_sample[b];  // needed only by the sampler, loaded while the rest runs
+
 
     // ---- 1. staging and prefetch
     const bool shape_ok = K >= 1 && K <= al.max_k && M >= 1 && M <= al.max_m;
@@ -89,6 +96,7 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     const int all_votes = dtw::block_or((bad ? 1 : 0) | (vbad ? 2 : 0), sh_votes, kThreads / kWave);
     const bool align_ok = (all_votes & 1) == 0;
     const bool verify_ok = (all_votes & 2) == 0;
+    TT_STAMP(1);
 
     // ---- 2. token distances, cumulative cost, move masks
     const int L = rows::band_half_width(K, M, al.w);
@@ -99,6 +107,7 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
         __syncthreads();
         if (wave == 0) total = rows::recurrence<TB>(s, K, M, L);
         __syncthreads();
+        TT_STAMP(2);
         rows::moves<TB>(s, K, M, L, wave, kThreads / kWave);
     }
     if (pd_thread) pd[tid - kDraftPrefetch] = pv;
@@ -132,11 +141,14 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
                 sh_gamma = gamma;
                 sh_rtok = gamma < M ? tid_t[gamma] : -1;
                 sh_rq = gamma < M ? rq : 0.0f;
+                sh_rp = gamma < M ? pt[gamma] : 0.0f;  // the row's entry at t_gamma, already gathered
+                sh_next = kThreads / kWave;
             }
         }
         if (lane == 0) sh_ok = verify_ok ? 1 : 0;
     }
     __syncthreads();
+    TT_STAMP(3);
     if (!sh_ok) {
         if (tid == 0) {
             ve.n_accepted[b] = -1;
@@ -156,23 +168,32 @@ __global__ void __launch_bounds__(kThreads) step_fused(SParams p) {
     const float rq = sh_rq;
     const int vt = ve.v_t;
     const float *row = ve.target_probs + (int64_t)(t0 + b + r) * ve.target_ld;
-    vcore::stream_chunks(row, vt, p.vec4 != 0, 0, p.nc, kThreads / kWave, rtok, rq,
-                         [&](int c, uint64_t sum) { sh_part[c] = sum; });
+    const bool vec = p.vec4 != 0;
+    const float rp = sh_rp;
+    vcore::stream_chunks(row, vt, vec, 0, p.nc, kThreads / kWave, rtok, rq, rp,
+                         [&](int c, uint64_t sum) { sh_part[c] = sum; }, &sh_next);
+    TT_STAMP(4);
     __syncthreads();
+    TT_STAMP(5);
     if (wave != 0) return;
     uint64_t Z;
     const int token =
-        vcore::wave_sample(row, nullptr, vt, p.nc, p.vec4 != 0, [&](int c) { return sh_part[c]; }, us, rtok, rq, &Z);
-    if (tid == 0) {
+        vcore::wave_sample(row, nullptr, vt, p.nc, vec, [&](int c) { return sh_part[c]; }, us, rtok, rq, &Z);
+    if (lane == 0) {
         ve.n_accepted[b] = r;
         ve.out_token[b] = token;
         p.zsum[b] = Z;
         p.rsel[b] = r;
     }
+    TT_STAMP_WAVE(6);
 }
 
 template <int TB, bool STREAM>
 int launch_tb(const SParams &p, size_t lds, hipStream_t stream) {
+    if (lds > 64 * 1024 &&
+        hipFuncSetAttribute(reinterpret_cast<const void *>(&step_fused<TB, STREAM>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+        return TT_ELAUNCH;
     hipLaunchKernelGGL((step_fused<TB, STREAM>), dim3(p.s.ve.n_streams), dim3(kThreads), lds, stream, p);
     return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
 }
@@ -210,7 +231,7 @@ bool step_fused_fits(const StepArgs &s, int tb) {
     return (tb == 8 || tb == 16 || tb == 32 || tb == 64) && align_rows_fits(s.al.max_k, s.al.max_m) &&
            s.ve.max_m <= rows::kMaxSide &&
            (verify_row_path(s.ve.n_streams, s.ve.v_t) || s.ve.v_t <= kFusedShortRow) &&
-           8 * (size_t)verify_layout(s.ve.n_streams, s.ve.v_t).n_chunks <= kPartLdsMax;
+           8 * (size_t)verify_layout(s.ve.n_streams, s.ve.v_t).n_chunks <= kDynLdsMax;
 }
 
 int launch_step_fused(const StepArgs &s, int tb, hipStream_t stream) {

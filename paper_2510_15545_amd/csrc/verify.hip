@@ -30,6 +30,7 @@
 // In the split path workgroup id -> (stream, split) is XCD-aware: the hardware deals
 // workgroup ids round-robin over the 8 XCDs, so XCD x receives the contiguous work range
 // [x * G/8, (x+1) * G/8) and a stream's splits share one XCD.
+#include "stamps.h"
 #include "verify_core.h"
 
 #ifndef TT_VERIFY_TARGET_WG
@@ -39,6 +40,8 @@
 #define TT_VERIFY_ROW_MIN_STREAMS 256  // row path from this many streams up
 #endif
 
+TT_STAMPS_TABLE(verify)
+
 namespace tt {
 namespace {
 
@@ -47,7 +50,7 @@ using namespace vcore;
 constexpr int kSplitThreads = 256;
 constexpr int kRowThreads = 1024;
 constexpr int kXcds = 8;
-constexpr size_t kRowLdsMax = 64 * 1024;  // row path: chunk sums of one row held in LDS
+constexpr int kRowMaxChunks = 2048;  // row path: rows up to 2M floats (LDS holds their chunk sums)
 
 struct VParams {
     VerifyArgs a;
@@ -57,30 +60,49 @@ struct VParams {
     int32_t nc, splits, cpw, work_items, vec4;
 };
 
-// Acceptance scan by one wave: gamma (first rejection, else M); false if the stream is
-// invalid (M outside [0, max_m] or an id outside [0, v_t)).  The proposal's mass at t_j
-// is q_j (one-hot) or q_rows[t0 + j][t_j] (DENSE).
+// Acceptance scan by one wave: gamma (first rejection, else M) and the rejected
+// position's t, q and P_t(t) (rtok = -1 after full acceptance); false if the stream is invalid (M
+// outside [0, max_m] or an id outside [0, v_t)).  The proposal's mass at t_j is q_j
+// (one-hot) or q_rows[t0 + j][t_j] (DENSE).  t_j, q_j and u_j are loaded together; only
+// P_t(t_j) (and the dense q(t_j)) wait for t_j.
+struct Rejection {
+    int rtok;  // t_gamma (-1 after full acceptance)
+    float rq;  // one-hot q_gamma
+    float rp;  // P_t(t_gamma)
+};
+
 template <bool DENSE>
-__device__ __forceinline__ bool accept_scan(const VerifyArgs &a, int b, int t0, int M, int lane, int &gamma) {
+__device__ __forceinline__ bool accept_scan(const VerifyArgs &a, int b, int t0, int M, int lane, int &gamma,
+                                            Rejection &rj) {
     gamma = M;
+    rj = Rejection{-1, 0.0f, 0.0f};
     if (M < 0 || M > a.max_m) return false;
     for (int base = 0; base < M; base += kWave) {
         const int j = base + lane;
         bool bad = false, rej = false;
+        float pt = 0.0f, q1 = 0.0f;
+        int tok = -1;
         if (j < M) {
-            const int tok = a.target_ids[t0 + j];
-            if (tok < 0 || tok >= a.v_t) {
-                bad = true;
-            } else {
-                const float pt = a.target_probs[(int64_t)(t0 + b + j) * a.target_ld + tok];
-                const float qj = DENSE ? a.q_rows[(int64_t)(t0 + j) * a.q_ld + tok] : a.q[t0 + j];
+            tok = a.target_ids[t0 + j];
+            q1 = DENSE ? 0.0f : a.q[t0 + j];
+            const float uj = a.u_accept[t0 + j];
+            bad = tok < 0 || tok >= a.v_t;
+            if (!bad) {
+                pt = a.target_probs[(int64_t)(t0 + b + j) * a.target_ld + tok];
+                const float qj = DENSE ? a.q_rows[(int64_t)(t0 + j) * a.q_ld + tok] : q1;
                 const float ratio = pt / qj;
-                rej = !((qj <= 0.0f) || (a.u_accept[t0 + j] < ratio));
+                rej = !((qj <= 0.0f) || (uj < ratio));
             }
         }
         if (__any(bad)) return false;
         const unsigned long long rm = __ballot(rej);
-        if (rm != 0ull && gamma == M) gamma = base + __ffsll(rm) - 1;
+        if (rm != 0ull && gamma == M) {
+            const int l = __ffsll(rm) - 1;
+            gamma = base + l;
+            rj.rtok = __shfl(tok, l);
+            rj.rq = __shfl(q1, l);
+            rj.rp = __shfl(pt, l);
+        }
     }
     return true;
 }
@@ -106,36 +128,46 @@ __device__ __forceinline__ Proposal proposal(const VerifyArgs &a, int t0, int M,
     return pr;
 }
 
-// Q62 chunk sums of row's chunks [c0, c1) by the calling workgroup's waves.
+// Q62 chunk sums of row's chunks [c0, c1) by the calling workgroup's waves; rp is the
+// row's entry at the one-hot proposal's token (from the acceptance scan), next the LDS chunk
+// counter (or null).
 template <class Store>
 __device__ __forceinline__ void stream_row(const float *row, const Proposal &pr, int vt, bool vec, int c0, int c1,
-                                           int stride, Store store) {
-    if (pr.qrow != nullptr) stream_chunks_dense(row, pr.qrow, vt, vec, c0, c1, stride, store);
-    else stream_chunks(row, vt, vec, c0, c1, stride, pr.rtok, pr.rq, store);
+                                           int stride, float rp, Store store, int *next) {
+    if (pr.qrow != nullptr) stream_chunks_dense(row, pr.qrow, vt, vec, c0, c1, stride, store, next);
+    else stream_chunks(row, vt, vec, c0, c1, stride, pr.rtok, pr.rq, rp, store, next);
 }
 
 // ------------------------------------------------------------------ row path
 template <bool DENSE, int THREADS>
 __global__ void __launch_bounds__(THREADS) verify_row(VParams p) {
+    constexpr int kWaves = THREADS / kWave;
     const VerifyArgs &a = p.a;
     const int b = blockIdx.x;
     const int tid = threadIdx.x, lane = tid % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: wave-level branches stay scalar
     extern __shared__ uint64_t sh_part[];  // nc chunk sums
-    __shared__ int sh_gamma, sh_ok;
+    __shared__ int sh_gamma, sh_ok, sh_next;
+    __shared__ Rejection sh_rj;
 
+    TT_STAMP(0);
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
     const float us = a.u_sample[b];
     if (wave == 0) {
         int gamma;
-        const bool ok = accept_scan<DENSE>(a, b, t0, M, lane, gamma);
+        Rejection rj;
+        const bool ok = accept_scan<DENSE>(a, b, t0, M, lane, gamma, rj);
         if (lane == 0) {
             sh_gamma = gamma;
             sh_ok = ok ? 1 : 0;
+            sh_rj = rj;
+            sh_next = kWaves;
         }
+        TT_STAMP(1);
     }
     __syncthreads();
+    TT_STAMP(2);
     if (!sh_ok) {
         if (tid == 0) {
             a.n_accepted[b] = -1;
@@ -145,21 +177,26 @@ __global__ void __launch_bounds__(THREADS) verify_row(VParams p) {
         return;
     }
     const int r = sh_gamma;
+    const Rejection rj = sh_rj;
     const int vt = a.v_t;
+    const bool vec = p.vec4 != 0;
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
-    const Proposal pr = proposal<DENSE>(a, t0, M, r);
-    stream_row(row, pr, vt, p.vec4 != 0, 0, p.nc, THREADS / kWave, [&](int c, uint64_t s) { sh_part[c] = s; });
+    const Proposal pr{DENSE && r < M ? a.q_rows + (int64_t)(t0 + r) * a.q_ld : nullptr, rj.rtok, rj.rq};
+    stream_row(row, pr, vt, vec, 0, p.nc, kWaves, rj.rp, [&](int c, uint64_t s) { sh_part[c] = s; }, &sh_next);
+    TT_STAMP(3);
     __syncthreads();
+    TT_STAMP(4);
     if (wave != 0) return;
     uint64_t Z;
-    const int token = wave_sample(row, pr.qrow, vt, p.nc, p.vec4 != 0, [&](int c) { return sh_part[c]; }, us,
-                                  pr.rtok, pr.rq, &Z);
+    const int token =
+        wave_sample(row, pr.qrow, vt, p.nc, vec, [&](int c) { return sh_part[c]; }, us, pr.rtok, pr.rq, &Z);
     if (tid == 0) {
         a.n_accepted[b] = r;
         a.out_token[b] = token;
         p.zsum[b] = Z;
         p.rsel[b] = r;
     }
+    TT_STAMP(5);
 }
 
 // ------------------------------------------------------------------ split path
@@ -175,22 +212,34 @@ __global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
     const int b = work / p.splits, s = work % p.splits;
     const int tid = threadIdx.x, lane = tid % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform: wave-level branches stay scalar
-    __shared__ int sh_gamma, sh_ok;
+    __shared__ int sh_gamma, sh_ok, sh_next;
+    __shared__ float sh_rp;
 
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
+    const int c0 = s * p.cpw;
+    const int c1 = (c0 + p.cpw) < p.nc ? (c0 + p.cpw) : p.nc;
+    if (tid == 0) sh_next = c0 + kSplitThreads / kWave;
     if (GIVEN) {
         const int r = p.rsel[b];
         if (tid == 0) {
             sh_gamma = r;
             sh_ok = r >= 0 ? 1 : 0;
+            // the rejected proposal's entry, if this workgroup's share of the row holds it
+            const int rtok = r >= 0 && r < M ? a.target_ids[t0 + r] : -1;
+            const int x0 = s * p.cpw * kChunk;
+            sh_rp = rtok >= x0 && rtok < x0 + p.cpw * kChunk && rtok < a.v_t
+                        ? a.target_probs[(int64_t)(t0 + b + r) * a.target_ld + rtok]
+                        : 0.0f;
         }
     } else if (wave == 0) {  // every workgroup of the stream recomputes gamma
         int gamma;
-        const bool ok = accept_scan<DENSE>(a, b, t0, M, lane, gamma);
+        Rejection rj;
+        const bool ok = accept_scan<DENSE>(a, b, t0, M, lane, gamma, rj);
         if (lane == 0) {
             sh_gamma = gamma;
             sh_ok = ok ? 1 : 0;
+            sh_rp = rj.rp;
         }
     }
     __syncthreads();
@@ -206,10 +255,9 @@ __global__ void __launch_bounds__(kSplitThreads) verify_stream(VParams p) {
     if (!GIVEN && s == 0 && tid == 0) p.rsel[b] = r;
     const float *row = a.target_probs + (int64_t)(t0 + b + r) * a.target_ld;
     const Proposal pr = proposal<DENSE>(a, t0, M, r);
-    const int c0 = s * p.cpw;
-    const int c1 = (c0 + p.cpw) < p.nc ? (c0 + p.cpw) : p.nc;
     uint64_t *out = p.partials + (int64_t)b * p.nc;
-    stream_row(row, pr, a.v_t, p.vec4 != 0, c0, c1, kSplitThreads / kWave, [&](int c, uint64_t sum) { out[c] = sum; });
+    stream_row(row, pr, a.v_t, p.vec4 != 0, c0, c1, kSplitThreads / kWave, sh_rp,
+               [&](int c, uint64_t sum) { out[c] = sum; }, &sh_next);
 }
 
 // One wave per stream: exact threshold, crossing chunk, crossing index.
@@ -284,7 +332,7 @@ VerifyLayout verify_layout(int32_t n_streams, int32_t v_t) {
 
 bool verify_row_path(int32_t n_streams, int32_t v_t) {
     const VerifyLayout L = verify_layout(n_streams, v_t);
-    return n_streams >= TT_VERIFY_ROW_MIN_STREAMS && 8 * (size_t)L.n_chunks <= kRowLdsMax;
+    return n_streams >= TT_VERIFY_ROW_MIN_STREAMS && L.n_chunks <= kRowMaxChunks;
 }
 
 namespace {
@@ -338,21 +386,31 @@ int launch_split(VParams &p, hipStream_t stream) {
     return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
 }
 
+// One workgroup of THREADS per stream.  The chunk sums in dynamic LDS can pass the 64 KiB a
+// launch gets by default; the kernel is then allowed the size it asks for.
+template <bool DENSE, int THREADS>
+int launch_row(const VParams &p, hipStream_t stream) {
+    const size_t lds = 8 * (size_t)p.nc;
+    if (lds > 64 * 1024 &&
+        hipFuncSetAttribute(reinterpret_cast<const void *>(&verify_row<DENSE, THREADS>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+        return TT_ELAUNCH;
+    hipLaunchKernelGGL((verify_row<DENSE, THREADS>), dim3(p.a.n_streams), dim3(THREADS), lds, stream, p);
+    return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+}
+
 template <bool DENSE>
 int launch_verify_kernels(VParams &p, hipStream_t stream) {
     const VerifyArgs &a = p.a;
     if (verify_row_path(a.n_streams, a.v_t)) {
         // about eight chunks per wave: short rows take small workgroups, so that several
         // streams share a compute unit and their acceptance scans and samples overlap
-        const size_t lds = 8 * (size_t)p.nc;
         const int waves = (p.nc + 7) / 8;
-        const dim3 g(a.n_streams);
-        if (waves <= 1) hipLaunchKernelGGL((verify_row<DENSE, 64>), g, dim3(64), lds, stream, p);
-        else if (waves <= 2) hipLaunchKernelGGL((verify_row<DENSE, 128>), g, dim3(128), lds, stream, p);
-        else if (waves <= 4) hipLaunchKernelGGL((verify_row<DENSE, 256>), g, dim3(256), lds, stream, p);
-        else if (waves <= 8) hipLaunchKernelGGL((verify_row<DENSE, 512>), g, dim3(512), lds, stream, p);
-        else hipLaunchKernelGGL((verify_row<DENSE, kRowThreads>), g, dim3(kRowThreads), lds, stream, p);
-        return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+        if (waves <= 1) return launch_row<DENSE, 64>(p, stream);
+        if (waves <= 2) return launch_row<DENSE, 128>(p, stream);
+        if (waves <= 4) return launch_row<DENSE, 256>(p, stream);
+        if (waves <= 8) return launch_row<DENSE, 512>(p, stream);
+        return launch_row<DENSE, kRowThreads>(p, stream);
     }
     return launch_split<DENSE, false>(p, stream);
 }

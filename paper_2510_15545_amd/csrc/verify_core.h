@@ -6,11 +6,9 @@
 #include <climits>
 #include <cmath>
 
+#include "stamps.h"
 #include "tt_internal.h"
 
-#ifndef TT_VERIFY_PREFETCH
-#define TT_VERIFY_PREFETCH 1  // chunks each wave keeps in flight ahead of the one it sums
-#endif
 #ifndef TT_VERIFY_NT_LOADS
 #define TT_VERIFY_NT_LOADS 1  // row loads carry the non-temporal hint (0: ordinary loads)
 #endif
@@ -129,11 +127,11 @@ __device__ __forceinline__ void load_chunk(const float *row, int xb, int lane, i
     }
 }
 
-// Q62 sums of chunks c0 + wave, c0 + wave + stride, ... < c1 (one chunk ahead in flight);
-// lane 63 hands each sum to store(c, sum).
+// Q62 sum of one loaded chunk c; lane 63 hands it to store(c, sum).  The rejected
+// proposal's token rtok loses q_r = rq of its mass: rp is its entry P(rtok), which the
+// acceptance test has already gathered, so the chunk holding it needs no second load.
 template <class Store>
-__device__ __forceinline__ void sum_chunk(const float4 (&v)[4], const float *row, int c, int rtok, float rq,
-                                          Store &store) {
+__device__ __forceinline__ void sum_chunk(const float4 (&v)[4], int c, int rtok, float rq, float rp, Store &store) {
     const int lane = threadIdx.x % kWave;
     uint64_t acc = 0;
 #pragma unroll
@@ -142,45 +140,46 @@ __device__ __forceinline__ void sum_chunk(const float4 (&v)[4], const float *row
     acc = wave_inclusive_scan(acc);
     if (lane == kWave - 1) {
         const int xb = c * kChunk;
-        if (rtok >= xb && rtok < xb + kChunk) {  // the rejected proposal loses q_r of its mass
-            const float pr = row[rtok];
-            acc += q62(clamp01(pr - rq)) - q62(clamp01(pr));
-        }
+        if (rtok >= xb && rtok < xb + kChunk) acc += q62(clamp01(rp - rq)) - q62(clamp01(rp));
         store(c, acc);
     }
 }
 
-// Q62 sums of chunks c0 + wave, c0 + wave + stride, ... < c1, with TT_VERIFY_PREFETCH
-// chunks in flight ahead of the one being summed; lane 63 hands each sum to store(c, sum).
+// The chunk a wave takes after its current one.  With an LDS counter (next != nullptr,
+// initialised by the caller to c0 + the number of waves before a barrier) chunks are handed
+// out in order to whichever wave asks first, so waves that the memory system serves faster
+// take more of the row; without one the wave strides by the number of waves.
+__device__ __forceinline__ int next_chunk(int *next, int c, int stride) {
+    if (next == nullptr) return c + stride;
+    int n = 0;
+    if (threadIdx.x % kWave == 0) n = atomicAdd(next, 1);
+    return __builtin_amdgcn_readfirstlane(n);
+}
+
+// Q62 sums of chunks [c0, c1): wave w starts at c0 + w and keeps one chunk in flight ahead of
+// the one it sums; lane 63 hands each sum to store(c, sum).
 template <class Store>
 __device__ __forceinline__ void stream_chunks(const float *row, int vt, bool vec, int c0, int c1, int stride,
-                                              int rtok, float rq, Store store) {
+                                              int rtok, float rq, float rp, Store store, int *next = nullptr) {
     const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     int c = c0 + wave;
-#if TT_VERIFY_PREFETCH >= 2
-    float4 v0[4], v1[4], v2[4];
-    if (c < c1) load_chunk(row, c * kChunk, lane, vt, vec, v0);
-    if (c + stride < c1) load_chunk(row, (c + stride) * kChunk, lane, vt, vec, v1);
-    for (; c < c1; c += stride) {
-        if (c + 2 * stride < c1) load_chunk(row, (c + 2 * stride) * kChunk, lane, vt, vec, v2);
-        sum_chunk(v0, row, c, rtok, rq, store);
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            v0[u] = v1[u];
-            v1[u] = v2[u];
-        }
-    }
-#else
+    if (c >= c1) return;
     float4 v[4], nx[4];
-    if (c < c1) load_chunk(row, c * kChunk, lane, vt, vec, v);
-    for (; c < c1; c += stride) {
-        const int cn = c + stride;
-        if (cn < c1) load_chunk(row, cn * kChunk, lane, vt, vec, nx);
-        sum_chunk(v, row, c, rtok, rq, store);
+    load_chunk(row, c * kChunk, lane, vt, vec, v);
+    int cn = next_chunk(next, c, stride);
+    for (;;) {
+        int cnn = c1;
+        if (cn < c1) {
+            load_chunk(row, cn * kChunk, lane, vt, vec, nx);
+            cnn = next_chunk(next, cn, stride);
+        }
+        sum_chunk(v, c, rtok, rq, rp, store);
+        if (cn >= c1) break;
 #pragma unroll
         for (int u = 0; u < 4; ++u) v[u] = nx[u];
+        c = cn;
+        cn = cnn;
     }
-#endif
 }
 
 // 16 consecutive floats row[x0 .. x0 + 16) (zero past vt).
@@ -213,23 +212,24 @@ __device__ __forceinline__ void sum_chunk_dense(const float4 (&vp)[4], const flo
     if (threadIdx.x % kWave == kWave - 1) store(c, acc);
 }
 
-// As stream_chunks for the dense residual: chunks c0 + wave, c0 + wave + stride, ... < c1
-// of both rows, one chunk of each ahead in flight.
+// As stream_chunks for the dense residual: chunks [c0, c1) of both rows, one chunk of each
+// ahead in flight.
 template <class Store>
 __device__ __forceinline__ void stream_chunks_dense(const float *prow, const float *qrow, int vt, bool vec, int c0,
-                                                    int c1, int stride, Store store) {
+                                                    int c1, int stride, Store store, int *next = nullptr) {
     const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     int c = c0 + wave;
+    if (c >= c1) return;
     float4 vp[4], vq[4], np_[4], nq[4];
-    if (c < c1) {
-        load_chunk(prow, c * kChunk, lane, vt, vec, vp);
-        load_chunk(qrow, c * kChunk, lane, vt, vec, vq);
-    }
-    for (; c < c1; c += stride) {
-        const int cn = c + stride;
+    load_chunk(prow, c * kChunk, lane, vt, vec, vp);
+    load_chunk(qrow, c * kChunk, lane, vt, vec, vq);
+    int cn = next_chunk(next, c, stride);
+    while (c < c1) {
+        int cnn = c1;
         if (cn < c1) {
             load_chunk(prow, cn * kChunk, lane, vt, vec, np_);
             load_chunk(qrow, cn * kChunk, lane, vt, vec, nq);
+            cnn = next_chunk(next, cn, stride);
         }
         sum_chunk_dense(vp, vq, c, store);
 #pragma unroll
@@ -237,17 +237,20 @@ __device__ __forceinline__ void stream_chunks_dense(const float *prow, const flo
             vp[u] = np_[u];
             vq[u] = nq[u];
         }
+        c = cn;
+        cn = cnn;
     }
 }
 
-// Inverse-CDF sample of the row from its nc chunk sums part(c), by one wave: every lane
-// returns the token and *Zout the Q62 mass.  The residual is max(0, row - qrow) when qrow
-// is given (dense proposal), else row less rq at the rejected proposal rtok (one-hot).  Chunk sums are scanned lane-blocked (lane l
-// holds chunks [l * per, (l + 1) * per)), the crossing chunk is re-read as 16 consecutive
-// floats per lane and scanned the same way.  Searches inside a lane are branch-free counts.
+// Z (the row's Q62 mass), T = floor(u * Z) and the chunk cs holding the crossing, with the
+// mass `base` of the chunks before it, from the nc chunk sums part(c), by one wave.  Chunk
+// sums are scanned lane-blocked (lane l holds chunks [l * per, (l + 1) * per)); searches
+// inside a lane are branch-free counts.  Returns 0 when cs is found, 1 when Z = 0, 2 when no
+// chunk holds the crossing (the Q62 mass wrapped: not a probability row).  Z, T, cs and base
+// are the same in every lane.
 template <class Part>
-__device__ inline int wave_sample(const float *row, const float *qrow, int vt, int nc, bool vec, Part part, float u,
-                                  int rtok, float rq, uint64_t *Zout) {
+__device__ __forceinline__ int find_crossing(int nc, Part part, float u, uint64_t &Z, uint64_t &T, int &cs,
+                                             uint64_t &base) {
     constexpr int kPerMax = 4;  // chunk sums kept in registers per lane (rows up to 256K floats)
     const int lane = threadIdx.x % kWave;
     const int per = (nc + kWave - 1) / kWave;
@@ -265,24 +268,26 @@ __device__ inline int wave_sample(const float *row, const float *qrow, int vt, i
         for (int c = ca; c < cb; ++c) local += part(c);
     }
     const uint64_t incl = wave_inclusive_scan(local);
-    const uint64_t Z = lane_value(incl, kWave - 1);
-    *Zout = Z;
-    if (Z == 0) return wave_first_argmax(row, vt);
-    const uint64_t T = exact_threshold(u, Z);
+    Z = lane_value(incl, kWave - 1);
+    T = 0;
+    cs = 0;
+    base = 0;
+    if (Z == 0) return 1;
+    T = exact_threshold(u, Z);
     // lane whose block of chunks holds the crossing, then the chunk inside it
     const uint64_t excl = incl - local;
     const unsigned long long hit = __ballot(excl <= T && T < incl);
-    if (hit == 0ull) return vt - 1;  // only if the Q62 mass wrapped (not a probability row)
+    if (hit == 0ull) return 2;
     const int owner = __ffsll(hit) - 1;
-    int cs = ca;
-    uint64_t base = excl;
+    int c_at = ca;
+    uint64_t b_at = excl;
     if (per <= kPerMax) {
         uint64_t run = excl;
 #pragma unroll
         for (int k = 0; k < kPerMax; ++k) {  // chunks of this lane wholly at or below T
             const bool below = ca + k < cb && run + ps[k] <= T;
-            cs += below ? 1 : 0;
-            base = below ? run + ps[k] : base;
+            c_at += below ? 1 : 0;
+            b_at = below ? run + ps[k] : b_at;
             run += ps[k];
         }
     } else if (lane == owner) {
@@ -290,17 +295,35 @@ __device__ inline int wave_sample(const float *row, const float *qrow, int vt, i
         for (int c = ca; c < cb; ++c) {
             const uint64_t nx = run + part(c);
             if (nx > T) break;
-            cs = c + 1;
-            base = nx;
+            c_at = c + 1;
+            b_at = nx;
             run = nx;
         }
     }
-    cs = __builtin_amdgcn_readlane(cs, owner);
-    base = lane_value(base, owner);
+    cs = __builtin_amdgcn_readlane(c_at, owner);
+    base = lane_value(b_at, owner);
+    return 0;
+}
+
+// Inverse-CDF sample of the row from its nc chunk sums part(c), by one wave: every lane
+// returns the token and *Zout the Q62 mass.  The residual is max(0, row - qrow) when qrow
+// is given (dense proposal), else row less rq at the rejected proposal rtok (one-hot).  The
+// crossing chunk's row values come as 16 consecutive floats per lane from chunk16(cs, x0, pv)
+// (wave_sample: read again from the row) and are scanned.
+template <class Part, class Chunk16>
+__device__ inline int wave_sample_with(const float *row, const float *qrow, int vt, int nc, bool vec, Part part,
+                                       Chunk16 chunk16, float u, int rtok, float rq, uint64_t *Zout) {
+    const int lane = threadIdx.x % kWave;
+    uint64_t Z, T, base;
+    int cs;
+    const int st = find_crossing(nc, part, u, Z, T, cs, base);
+    *Zout = Z;
+    if (st == 1) return wave_first_argmax(row, vt);
+    if (st == 2) return vt - 1;
     // the crossing chunk: lane holds elements cs*1024 + lane*16 + [0, 16)
     const int x0 = cs * kChunk + lane * 16;
     float pv[16], dv[16];
-    read16(row, x0, vt, vec, pv);
+    chunk16(cs, x0, pv);
     if (qrow != nullptr) {
         read16(qrow, x0, vt, vec, dv);
     } else {
@@ -328,6 +351,14 @@ __device__ inline int wave_sample(const float *row, const float *qrow, int vt, i
         k_at += run <= T ? 1 : 0;
     }
     return __builtin_amdgcn_readlane(x0 + k_at, tl);
+}
+
+template <class Part>
+__device__ inline int wave_sample(const float *row, const float *qrow, int vt, int nc, bool vec, Part part, float u,
+                                  int rtok, float rq, uint64_t *Zout) {
+    return wave_sample_with(
+        row, qrow, vt, nc, vec, part, [&](int, int x0, float(&pv)[16]) { read16(row, x0, vt, vec, pv); }, u, rtok,
+        rq, Zout);
 }
 
 }  // namespace vcore
