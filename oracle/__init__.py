@@ -63,6 +63,8 @@ def lib():
         L.orc_sd_verify.restype = None
         L.orc_delta_histogram.argtypes = [i32, P, P, P, P, i32, P]
         L.orc_delta_histogram.restype = None
+        L.orc_delta_quantile.argtypes = [P, i32, i32, i32]
+        L.orc_delta_quantile.restype = i32
         L.orc_sexp.argtypes = [f32]
         L.orc_sexp.restype = f32
         L.orc_verify_logits.argtypes = [i32, i32, P, P, P, P, i64, P, P, P, P, i32, P, P, P, ctypes.c_int]
@@ -234,6 +236,13 @@ def delta_histogram(draft_off, target_off, path_len, path, n_bins):
     lib().orc_delta_histogram(len(draft_off) - 1, _p(draft_off), _p(target_off), _p(path_len), _p(path),
                               int(n_bins), _p(hist))
     return hist
+
+
+def delta_quantile(hist, num=9, den=10):
+    """App. K: the smallest deviation d whose CDF over the histogram reaches num/den (exact
+    integer comparison); 0 for an empty histogram."""
+    h = _c(hist, np.int64) if np.size(hist) else np.zeros(1, np.int64)
+    return int(lib().orc_delta_quantile(_p(h), int(np.size(hist)), int(num), int(den)))
 
 
 def retokenize(vd_bytes, vd_off, vt_bytes, vt_off, draft_ids, draft_off, max_m=None, max_bytes=None):

@@ -25,6 +25,7 @@
  *                     speculative decoding, the homogeneous-vocabulary case)
  *   orc_delta_histogram  Sec. 5 Fig. CDF / App. K: position deviation |i - j| of the
  *                     matched pairs on the optimal paths
+ *   orc_delta_quantile   App. K: the deviation where that distribution reaches a quantile
  *   orc_verify_logits the verification from bf16 logits and a temperature (App. F), the
  *                     target softmax formed with a specified software exponential
  *
@@ -520,18 +521,40 @@ void orc_sd_verify(int32_t n_streams, int32_t V, const int32_t *draft_ids, const
  * draft / proxy target token pair (i, j) on an optimal warping path is |i - j|.  hist[d]
  * counts the path cells of all pairs with |i - j| = d for d < n_bins - 1; the last bin
  * counts every cell with |i - j| >= n_bins - 1.  Pair b's cells are path[2*(draft_off[b] +
- * target_off[b]) ...] (path_len[b] of them, as orc_align writes them); a pair with
- * path_len <= 0 (a sentinel pair) contributes nothing. */
+ * target_off[b]) ...] (path_len[b] of them, as orc_align writes them).  A pair with
+ * path_len <= 0 (a sentinel pair) contributes nothing, and so does one whose path_len
+ * exceeds K_b + M_b: a warping path from (1,1) to (K,M) has at most K + M - 1 cells, and
+ * the path area of pair b holds K_b + M_b of them. */
 void orc_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
                          const int32_t *path_len, const int32_t *path, int32_t n_bins, int64_t *hist) {
     for (int32_t d = 0; d < n_bins; ++d) hist[d] = 0;
     for (int32_t b = 0; b < n_pairs; ++b) {
+        const int32_t K = draft_off[b + 1] - draft_off[b], M = target_off[b + 1] - target_off[b];
+        if (path_len[b] > K + M) continue;
         const int32_t *cells = path + 2 * (int64_t)(draft_off[b] + target_off[b]);
         for (int32_t c = 0; c < path_len[b]; ++c) {
             int32_t dev = abs(cells[2 * c] - cells[2 * c + 1]);
             hist[dev < n_bins - 1 ? dev : n_bins - 1] += 1;
         }
     }
+}
+
+/* App. K "Settings of w": w is placed where the cumulative distribution of the position
+ * deviation reaches 0.9 (read off the histogram above, collected without a band).  For a
+ * quantile num/den (0 <= num <= den, 1 <= den <= 65536) this is the smallest d with
+ * hist[0] + ... + hist[d] >= (num/den) * total, decided exactly as
+ * (hist[0] + ... + hist[d]) * den >= num * total; 0 for an empty histogram.  If d is the
+ * last bin the deviation at the quantile is at least n_bins - 1. */
+int32_t orc_delta_quantile(const int64_t *hist, int32_t n_bins, int32_t num, int32_t den) {
+    int64_t total = 0;
+    for (int32_t d = 0; d < n_bins; ++d) total += hist[d];
+    if (total == 0) return 0;
+    int64_t cum = 0;
+    for (int32_t d = 0; d < n_bins; ++d) {
+        cum += hist[d];
+        if (cum * (int64_t)den >= (int64_t)num * total) return d;
+    }
+    return n_bins - 1;
 }
 
 /* ------------------------------------------------------------------------------------ */

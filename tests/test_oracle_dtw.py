@@ -206,3 +206,52 @@ def test_delta_histogram_invariants(orc):
     plen2 = plen.copy()
     plen2[1] = 0  # a sentinel pair
     assert orc.delta_histogram(do, to, plen2, path, 4).tolist() == [4, 0, 0, 0]
+
+
+def test_delta_histogram_oversize_path_len(orc):
+    """A pair whose path_len exceeds K + M (more cells than its path area holds) contributes
+    nothing; path_len = K + M still counts its cells."""
+    toks = [bytes([c]) for c in b"abcdefgh"]
+    pairs = [([0, 1, 2, 3], [0, 1, 2, 3]), ([4, 5], [4, 6])]
+    (cost, plen, path, mp), do, to = run(orc, toks, toks, pairs, 8)
+    full = orc.delta_histogram(do, to, plen, path, 4)
+    one = orc.delta_histogram(do[:2], to[:2], plen[:1], path, 4)
+    p2 = plen.copy()
+    p2[1] = 2 + 2 + 1  # K + M + 1
+    assert orc.delta_histogram(do, to, p2, path, 4).tolist() == one.tolist()
+    p2[1] = 2 + 2  # K + M: the area's last cell is counted too
+    assert orc.delta_histogram(do, to, p2, path, 4).sum() == full.sum() - plen[1] + 4
+
+
+def test_delta_quantile_fig2_and_hand_cases(orc):
+    """App. K's rule on the Fig. 2 path (deviations 0,1,1,1,0: hist [2, 3]): the CDF is 2/5 at
+    0 and 1 at 1, so the 0.9 quantile is 1, the 2/5 quantile is exactly reached at 0 and the
+    41/100 quantile is 1; an empty histogram gives 0, q = 0 gives 0 and q = 1 the last bin
+    holding any count."""
+    g = load_golden("fig2_alignment.json")
+    h = g["delta_pos_hist"]
+    assert orc.delta_quantile(h, 9, 10) == 1
+    assert orc.delta_quantile(h, 2, 5) == 0
+    assert orc.delta_quantile(h, 41, 100) == 1
+    assert orc.delta_quantile(h, 0, 1) == 0
+    assert orc.delta_quantile([0, 0, 0], 9, 10) == 0
+    assert orc.delta_quantile([1, 0, 2, 0, 0], 1, 1) == 2
+    assert orc.delta_quantile([0, 0, 7], 1, 65536) == 2
+
+
+def test_delta_quantile_against_sorted_deviations(orc):
+    """The quantile from the histogram equals the ceil(q n)-th smallest deviation of the
+    underlying list (an order statistic, exact rationals), for random lists and quantiles."""
+    from fractions import Fraction
+    import math
+
+    rng = np.random.default_rng(5)
+    for _ in range(300):
+        n_bins = int(rng.integers(1, 40))
+        devs = rng.integers(0, n_bins, int(rng.integers(1, 200)))
+        hist = np.bincount(devs, minlength=n_bins)
+        den = int(rng.integers(1, 65537))
+        num = int(rng.integers(0, den + 1))
+        k = math.ceil(Fraction(num, den) * len(devs))
+        want = 0 if k == 0 else int(np.sort(devs)[k - 1])  # q = 0: the CDF reaches it at 0
+        assert orc.delta_quantile(hist, num, den) == want, (hist, num, den)
