@@ -413,7 +413,7 @@ def main():
         "dtw": {"band_cells": cells, "cells_per_s": round(cells_per_s, 1),
                 "full_cells": int((Ka * Ma).sum()),
                 "full_cells_per_s": round(int((Ka * Ma).sum()) / (times["align"] * 1e-3), 1),
-                "delta_pos_w90": tt.w_at_quantile(hist, 0.9), "path_cells": int(a_out[1].sum().item())},
+                "delta_pos_w90": tt.w_at_quantile(hist, 9, 10), "path_cells": int(a_out[1].sum().item())},
         "retokenize": {"us": round(times["retokenize"] * 1e3, 2) if "retokenize" in times else None,
                        "string_bytes": rt_bytes,
                        "target_tokens": int(A.target_off[-1])},

@@ -279,6 +279,23 @@ int tt_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t 
                        int32_t *hist, void *stream);
 
 /*
+ * tt_delta_quantile -- App. K "Settings of w": where the cumulative distribution of
+ * the deviation counted by tt_delta_histogram reaches a quantile (the paper reads it
+ * at 0.9 from an alignment without a band and searches w at or below it).
+ *
+ * Inputs: hist[n_bins] int32 counts (device), n_bins in [1, 8192]; the quantile as a
+ * fraction num/den of host integers, 0 <= num <= den, 1 <= den <= 65536 (0.9 is 9/10).
+ * Output (device): *d_out = the smallest d with
+ *     (hist[0] + ... + hist[d]) * den >= num * (hist[0] + ... + hist[n_bins - 1]),
+ * compared exactly in 64-bit integers; 0 when the counts sum to 0.  d_out = n_bins - 1
+ * means the deviation at the quantile is at least n_bins - 1 (the overflow bin).
+ * One kernel on `stream`; nothing is allocated.  TT_EINVAL on a missing pointer or an
+ * argument outside these ranges.
+ */
+int tt_delta_quantile(const int32_t *hist, int32_t n_bins, int32_t num, int32_t den, int32_t *d_out,
+                      void *stream);
+
+/*
  * Token index for longest-match lookups in a vocabulary (used by tt_retokenize for
  * the target vocabulary).  tt_token_index_size gives its bytes for n_tokens
  * (16 bytes per hash slot, a power of two >= 4 * n_tokens slots); n_tokens in

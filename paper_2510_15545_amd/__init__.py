@@ -11,6 +11,7 @@ raised.
     verify    tt_verify    acceptance, residual / bonus sampling (Sec. 3, 4.2.2-4.2.3, App. D Alg. 4)
     verify_dense  tt_verify_dense  the same with dense proposals over one vocabulary (App. D Alg. 4)
     delta_histogram  tt_delta_histogram  |i - j| over the optimal paths' cells (Fig. CDF, App. K)
+    delta_quantile / w_at_quantile  tt_delta_quantile  where that distribution reaches 0.9 (App. K)
     token_index / retokenize  tt_token_index_build / tt_retokenize  draft tokens -> proxy target
               tokens by greedy longest match (Sec. 4.2.1, Alg. 2, App. A.1)
 """
@@ -20,7 +21,7 @@ import ctypes
 import os
 
 __all__ = ["Vocab", "align", "align_workspace", "transfer", "verify", "verify_dense", "verify_workspace", "lib",
-           "delta_histogram", "w_at_quantile", "token_index", "retokenize", "LIB_PATH",
+           "delta_histogram", "delta_quantile", "w_at_quantile", "token_index", "retokenize", "LIB_PATH",
            "TTError", "path_capacity"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtt.so")
@@ -72,6 +73,8 @@ def lib():
         L.tt_verify_logits.restype = ctypes.c_int
         L.tt_delta_histogram.argtypes = [i32, P, P, P, P, i32, P, P]
         L.tt_delta_histogram.restype = ctypes.c_int
+        L.tt_delta_quantile.argtypes = [P, i32, i32, i32, P, P]
+        L.tt_delta_quantile.restype = ctypes.c_int
         L.tt_token_index_size.argtypes = [i32, ctypes.POINTER(sz)]
         L.tt_token_index_size.restype = ctypes.c_int
         L.tt_token_index_build.argtypes = [VP, P, sz, P]
@@ -322,17 +325,21 @@ def delta_histogram(draft_off, target_off, path_len, path, n_bins: int, out=None
     return hist
 
 
-def w_at_quantile(hist, quantile: float = 0.9) -> int:
-    """App. K: the smallest deviation d whose CDF reaches `quantile` (host arithmetic on a
-    histogram returned by delta_histogram); the band half-width search stays at or below it."""
-    import numpy as np
+def delta_quantile(hist, num: int = 9, den: int = 10, out=None, stream=None):
+    """tt_delta_quantile: (int32 device tensor of one element) the smallest deviation d at which
+    the cumulative counts of `hist` reach num/den of their total (App. K)."""
+    torch = _torch()
+    i32 = torch.int32
+    d = torch.empty(1, dtype=i32, device=hist.device) if out is None else out
+    st = lib().tt_delta_quantile(_ptr(hist, i32, "hist"), int(hist.numel()), int(num), int(den), _ptr(d, i32, "d_out"),
+                                 _stream_handle(stream))
+    _check(st, "tt_delta_quantile")
+    return d
 
-    h = np.asarray(hist.cpu() if hasattr(hist, "cpu") else hist, dtype=np.int64)
-    total = int(h.sum())
-    if total == 0:
-        return 0
-    need = quantile * total
-    return int(np.searchsorted(np.cumsum(h), need, side="left"))
+
+def w_at_quantile(hist, num: int = 9, den: int = 10) -> int:
+    """App. K's bound on w from a device histogram: tt_delta_quantile's result as a host int."""
+    return int(delta_quantile(hist, num, den).item())
 
 
 def token_index(v: Vocab, stream=None):

@@ -2,7 +2,7 @@
 // "Settings of w"): a draft / proxy target pair (i, j) on an optimal warping path deviates
 // by |i - j| positions.  The histogram over a batch of aligned pairs is what App. K's
 // procedure reads to place the band half-width w (the offset where the CDF reaches 0.9,
-// collected with w = infinity).
+// collected with w = infinity); delta_quantile reads that offset off the histogram.
 //
 // Two launches: a fill kernel clears the histogram (no memset node, so the call can be
 // captured in a HIP graph), then up to 256 workgroups of 256 threads count their pairs into
@@ -57,7 +57,54 @@ __global__ void __launch_bounds__(kThreads) delta_hist(int32_t n_pairs, const in
         if (sh_hist[d] != 0) atomicAdd(&hist[d], sh_hist[d]);
 }
 
+// App. K: the smallest d with (hist[0] + ... + hist[d]) * den >= num * total, exact in int64
+// (|hist| < 2^31 and n_bins <= 8192 keep the prefixes below 2^44, den <= 65536 the products
+// below 2^60); 0 when the total is 0.  One workgroup: 32 bins per thread, a scan of the
+// thread sums in LDS, the first bin reaching the quantile by an LDS minimum.
+constexpr int kQuantBins = 32;
+
+__global__ void __launch_bounds__(kThreads) delta_quantile(const int32_t *hist, int n_bins, int32_t num, int32_t den,
+                                                           int32_t *out) {
+    __shared__ int64_t sums[kThreads];
+    __shared__ int first;
+    const int t = threadIdx.x;
+    const int b0 = t * kQuantBins;
+    int64_t own = 0;
+    for (int k = 0; k < kQuantBins && b0 + k < n_bins; ++k) own += hist[b0 + k];
+    sums[t] = own;
+    if (t == 0) first = n_bins - 1;
+    __syncthreads();
+    for (int off = 1; off < kThreads; off <<= 1) {  // inclusive scan of the thread sums
+        const int64_t v = t >= off ? sums[t - off] : 0;
+        __syncthreads();
+        sums[t] += v;
+        __syncthreads();
+    }
+    const int64_t total = sums[kThreads - 1];
+    if (total == 0) {
+        if (t == 0) *out = 0;
+        return;
+    }
+    const int64_t need = (int64_t)num * total;
+    int64_t cum = sums[t] - own;
+    for (int k = 0; k < kQuantBins && b0 + k < n_bins; ++k) {
+        cum += hist[b0 + k];
+        if (cum * (int64_t)den >= need) {
+            atomicMin(&first, b0 + k);
+            break;
+        }
+    }
+    __syncthreads();
+    if (t == 0) *out = first;
+}
+
 }  // namespace
+
+int launch_delta_quantile(const int32_t *hist, int32_t n_bins, int32_t num, int32_t den, int32_t *d_out,
+                          hipStream_t stream) {
+    hipLaunchKernelGGL(delta_quantile, dim3(1), dim3(kThreads), 0, stream, hist, n_bins, num, den, d_out);
+    return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+}
 
 int launch_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
                            const int32_t *path_len, const int32_t *path, int32_t n_bins, int32_t *hist,

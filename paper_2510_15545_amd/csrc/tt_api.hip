@@ -12,6 +12,7 @@ namespace {
 constexpr int32_t kMaxAlignLen = 4096;   // bound on K_b / M_b accepted by tt_align
 constexpr int32_t kMaxVerifyLen = 65536; // bound on M_b accepted by tt_verify
 constexpr int32_t kMaxHistBins = 8192;   // bins of tt_delta_histogram (its LDS copy: 32 KB)
+constexpr int32_t kMaxQuantileDen = 65536;  // denominator of tt_delta_quantile's quantile (int64-exact)
 constexpr int32_t kMaxIndexTokens = 1 << 28;  // vocabulary size a token index accepts
 constexpr int32_t kMaxTokenBytes = 64;        // longest target token the index and lookups handle
 constexpr int32_t kMaxLogitsRow = 1 << 23;     // logits per row tt_verify_logits accepts (64-bit exact sums)
@@ -197,6 +198,14 @@ int tt_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t 
     if (n_pairs > 0 && (!draft_off || !target_off || !path_len || !path)) return TT_EINVAL;
     return tt::launch_delta_histogram(n_pairs, draft_off, target_off, path_len, path, n_bins, hist,
                                       static_cast<hipStream_t>(stream));
+}
+
+int tt_delta_quantile(const int32_t *hist, int32_t n_bins, int32_t num, int32_t den, int32_t *d_out,
+                      void *stream) {
+    if (hist == nullptr || d_out == nullptr || n_bins < 1 || n_bins > kMaxHistBins || den < 1 ||
+        den > kMaxQuantileDen || num < 0 || num > den)
+        return TT_EINVAL;
+    return tt::launch_delta_quantile(hist, n_bins, num, den, d_out, static_cast<hipStream_t>(stream));
 }
 
 int tt_token_index_size(int32_t n_tokens, size_t *bytes) {

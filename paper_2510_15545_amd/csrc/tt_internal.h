@@ -79,6 +79,8 @@ int launch_verify_after_gamma(const VerifyArgs &a, hipStream_t stream);
 int launch_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
                            const int32_t *path_len, const int32_t *path, int32_t n_bins, int32_t *hist,
                            hipStream_t stream);
+int launch_delta_quantile(const int32_t *hist, int32_t n_bins, int32_t num, int32_t den, int32_t *d_out,
+                          hipStream_t stream);
 
 // ---------------------------------------------------------------- re-tokenisation (retok.hip)
 uint32_t token_index_capacity(int32_t n_tokens);  // hash slots for a vocabulary of n_tokens

@@ -49,6 +49,8 @@ int main(void) {
     EXPECT(tt_step(&v, &v, 1, 10, 10, D, D, D, D, 4, 4, 8, F, 10, F, 10, F, F, D, D, D, D, F, D, D, NULL, W, 16,
                    NULL) == TT_EWORKSPACE);
     EXPECT(tt_delta_histogram(1, D, D, D, D, 0, D, NULL) == TT_EINVAL);
+    EXPECT(tt_delta_quantile(D, 0, 9, 10, D, NULL) == TT_EINVAL);
+    EXPECT(tt_delta_quantile(D, 8, 11, 10, D, NULL) == TT_EINVAL);
     EXPECT(tt_token_index_build(&big, W, 1 << 30, NULL) == TT_EUNSUPPORTED);
     EXPECT(tt_token_index_build(&v, (void *)0x1004, 1 << 30, NULL) == TT_EINVAL);
     EXPECT(tt_retokenize(&v, &v, W, 1 << 20, 1, D, D, 0, 16, D, D, W, 1 << 20, NULL) == TT_EINVAL);

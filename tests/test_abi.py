@@ -187,11 +187,15 @@ def test_binding_refuses_host_tensors():
         tt._ptr(torch.zeros(3, dtype=torch.int32), torch.int32, "x")
 
 
-def test_w_at_quantile_host_rule():
-    """App. K: the offset where the CDF of the deviation first reaches the quantile."""
-    assert tt.w_at_quantile([2, 3], 0.9) == 1
-    assert tt.w_at_quantile([9, 1], 0.9) == 0  # CDF(0) = 0.9 exactly
-    assert tt.w_at_quantile([89, 10, 1], 0.9) == 1
-    assert tt.w_at_quantile([0, 0, 5], 0.5) == 2
-    assert tt.w_at_quantile([0, 0, 0], 0.9) == 0
-    assert tt.w_at_quantile([1] * 10, 1.0) == 9
+def test_delta_quantile_argument_checks():
+    """App. K's quantile call rejects bad sizes and fractions on the host."""
+    L = tt.lib()
+    dummy = ctypes.c_void_p(16)
+    assert L.tt_delta_quantile(None, 8, 9, 10, dummy, None) == tt.TT_EINVAL
+    assert L.tt_delta_quantile(dummy, 8, 9, 10, None, None) == tt.TT_EINVAL
+    assert L.tt_delta_quantile(dummy, 0, 9, 10, dummy, None) == tt.TT_EINVAL
+    assert L.tt_delta_quantile(dummy, 8193, 9, 10, dummy, None) == tt.TT_EINVAL
+    assert L.tt_delta_quantile(dummy, 8, 11, 10, dummy, None) == tt.TT_EINVAL
+    assert L.tt_delta_quantile(dummy, 8, -1, 10, dummy, None) == tt.TT_EINVAL
+    assert L.tt_delta_quantile(dummy, 8, 1, 0, dummy, None) == tt.TT_EINVAL
+    assert L.tt_delta_quantile(dummy, 8, 1, 65537, dummy, None) == tt.TT_EINVAL

@@ -108,3 +108,48 @@ def test_full_size_workload(c):
     o = oracle_run(wl)
     compare_align(wl, g, o)
     compare_verify(g, o)
+
+
+_LONG = {}
+
+
+def _long_pairs():
+    """Workload 4 at its full size (1,024 long pairs), built once per session."""
+    if "wl" not in _LONG:
+        _LONG["wl"] = _case(4, {4: None})
+    return _LONG["wl"]
+
+
+@pytest.mark.parametrize("w", [8, -1])
+def test_full_size_long_pair_alignment(w):
+    """The DTW stress batch at full size, every pair's cost, path and map checked: 1,024 pairs
+    are ranked by band work over several workgroups before the strip kernel runs."""
+    wl = _long_pairs()
+    print(f"[case] long pairs full size w={w}", flush=True)
+    g = gpu_run(wl, w=w)
+    o = oracle_run(wl, w=w)
+    compare_align(wl, g, o)
+
+
+def _tiled(wl, times):
+    """The alignment batch repeated `times` times (pairs keep their own tokens and offsets)."""
+    t = copy.copy(wl)
+    nd, nt = int(wl.draft_off[-1]), int(wl.target_off[-1])
+    t.draft_ids = np.tile(wl.draft_ids, times)
+    t.target_ids = np.tile(wl.target_ids, times)
+    t.draft_off = np.concatenate([wl.draft_off[:-1] + k * nd for k in range(times)] + [[times * nd]]).astype(np.int32)
+    t.target_off = np.concatenate([wl.target_off[:-1] + k * nt for k in range(times)] + [[times * nt]]).astype(np.int32)
+    t.verify_ids = t.target_ids
+    t.prob = None
+    return t
+
+
+def test_alignment_past_the_ranked_dispatch():
+    """3,072 long pairs: above 2,048 pairs the strip kernel takes them in batch order (no
+    ranking); every pair still matches the oracle."""
+    wl = _tiled(_long_pairs(), 3)
+    assert wl.n == 3072
+    print("[case] long pairs x3 (3072) w=8", flush=True)
+    g = gpu_run(wl, w=8)
+    o = oracle_run(wl, w=8)
+    compare_align(wl, g, o)

@@ -132,3 +132,32 @@ def test_step_workspace_reuse():
     for o in outs[1:]:
         for a, b in zip(outs[0], o):
             assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+
+
+@pytest.mark.parametrize("v_t", [2_097_152, 2_097_153])
+def test_row_width_at_the_row_path_limit(v_t):
+    """256 streams over rows of 2,048 chunks (the widest rows the one-workgroup-per-stream kernels
+    take: tt_verify's row path and the fused tt_step) and one float more (the split path and the
+    fused front): tt_step equals the three calls and the oracle.  Most streams propose nothing
+    (M = 0: the bonus row is sampled), 16 propose one token."""
+    import copy
+
+    print(f"[case] wide rows v_t={v_t}", flush=True)
+    rng = np.random.default_rng(7)
+    toks = random_tokens(rng, 64, 1, 4)
+    v = vocab_of(toks)
+    pairs = [([int(rng.integers(0, len(toks)))], [int(rng.integers(0, len(toks)))] if b % 16 == 0 else [])
+             for b in range(256)]
+    wl = workload(v, v, pairs, len(toks), len(toks), probs=True)
+    wl = copy.copy(wl)
+    n_rows = int(wl.target_off[-1]) + wl.n
+    rows = rng.random((n_rows, v_t), dtype=np.float32)
+    rows /= rows.sum(axis=1, keepdims=True, dtype=np.float32)
+    wl.v_t = v_t
+    wl.target_probs = rows
+    d = upload(wl)
+    s = step_run(wl, d, bounds=(64, 64))
+    g = gpu_run(wl, d=d, bounds=(64, 64))
+    same_as_three_calls(wl, s, g)
+    o = oracle_run(wl)
+    compare_verify(s, o)
