@@ -176,7 +176,7 @@ int tt_verify_workspace_size(int32_t n_streams, int32_t v_t, size_t *bytes);
  * sums and per-stream scratch); it needs no initialisation.  Calls that overlap
  * in time must not share it.
  * Launches: with at least 256 streams (one per compute unit) and rows of at most
- * 8M floats, one kernel with a workgroup per stream; otherwise one streaming kernel
+ * 2,097,152 floats, one kernel with a workgroup per stream; otherwise one streaming kernel
  * over B x S workgroups and one sampling kernel.  If residual != NULL, one more
  * kernel writes the residual rows.
  */
@@ -398,7 +398,7 @@ int tt_step_workspace_size(int32_t n_streams, int32_t v_t, int32_t max_k, int32_
  * (transfer), Sec. 3, Sec. 4.2.2-4.2.3, App. D Alg. 4 (verification).
  *
  * When max_k <= 64, max_m <= 64, and either n_streams >= 256 with verify rows of
- * at most 8M floats or v_t <= 16384 (short rows, any batch size), the path runs as
+ * at most 2,097,152 floats or v_t <= 16384 (short rows, any batch size), the path runs as
  * ONE kernel with a workgroup per stream: the
  * pair is aligned in LDS, map and q never leave the chip before they are used,
  * and the selected target row is read once.  Other batches of pairs with
