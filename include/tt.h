@@ -188,6 +188,25 @@ int tt_verify(int32_t n_streams, int32_t v_t,
               void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * tt_verify_noalloc -- tt_verify for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same arguments, kernels and results, without the workspace.
+ * Its scratch is a device array of 8 MiB inside the library; each GPU the library
+ * runs on holds its own copy until the process ends.  Batches whose workspace
+ * (tt_verify_workspace_size) exceeds 8 MiB are refused with TT_EWORKSPACE (for
+ * example 4,096 streams at v_t = 151,936 fit, 8,192 do not).  Nothing is
+ * allocated: no hipMalloc, hipFree or allocating library call.  Every call on one
+ * GPU shares that GPU's scratch, so calls that overlap in time on one GPU race;
+ * calls in one stream (or otherwise ordered) do not.  TT_ELAUNCH if the scratch's
+ * device address cannot be found.
+ */
+int tt_verify_noalloc(int32_t n_streams, int32_t v_t,
+                      const int32_t *target_ids, const int32_t *target_off, const float *q,
+                      const float *target_probs, int64_t target_ld,
+                      const float *u_accept, const float *u_sample, int32_t max_m,
+                      int32_t *n_accepted, int32_t *out_token, float *residual, void *stream);
+
+/*
  * tt_verify_dense -- standard speculative sampling with dense proposals over one
  * vocabulary (App. D Alg. 4; the homogeneous-vocabulary case, where the draft
  * model's whole distribution over the target's tokens is the proposal).  It is

@@ -20,7 +20,7 @@ from __future__ import annotations
 import ctypes
 import os
 
-__all__ = ["Vocab", "align", "align_workspace", "transfer", "verify", "verify_dense", "verify_workspace", "lib",
+__all__ = ["Vocab", "align", "align_workspace", "transfer", "verify", "verify_noalloc", "verify_dense", "verify_workspace", "lib",
            "delta_histogram", "delta_quantile", "w_at_quantile", "token_index", "retokenize", "LIB_PATH",
            "TTError", "path_capacity"]
 
@@ -67,6 +67,8 @@ def lib():
         L.tt_verify_workspace_size.restype = ctypes.c_int
         L.tt_verify.argtypes = [i32, i32, P, P, P, P, i64, P, P, i32, P, P, P, P, sz, P]
         L.tt_verify.restype = ctypes.c_int
+        L.tt_verify_noalloc.argtypes = [i32, i32, P, P, P, P, i64, P, P, i32, P, P, P, P]
+        L.tt_verify_noalloc.restype = ctypes.c_int
         L.tt_verify_dense.argtypes = [i32, i32, P, P, P, i64, P, i64, P, P, i32, P, P, P, P, sz, P]
         L.tt_verify_dense.restype = ctypes.c_int
         L.tt_verify_logits.argtypes = [i32, i32, P, P, P, P, i64, P, P, P, P, i32, P, P, P]
@@ -252,6 +254,30 @@ def verify(v_t: int, target_ids, target_off, q, target_probs, u_accept, u_sample
                          _ptr(tok, i32, "out_token"), _ptr(res, f32, "residual", allow_none=True),
                          ctypes.c_void_p(workspace.data_ptr()), int(workspace.numel()), _stream_handle(stream))
     _check(st, "tt_verify")
+    return out
+
+
+def verify_noalloc(v_t: int, target_ids, target_off, q, target_probs, u_accept, u_sample, max_m: int,
+                   residual: bool = False, out=None, stream=None):
+    """tt_verify_noalloc: tt_verify with the library's own scratch (no workspace).  Returns
+    (n_accepted, out_token, residual or None); pass `out` to allocate nothing here either."""
+    torch = _torch()
+    i32, f32 = torch.int32, torch.float32
+    n = int(target_off.numel()) - 1
+    dev = target_off.device
+    if target_probs.dim() != 2 or target_probs.stride(1) != 1 or target_probs.dtype != f32 or not target_probs.is_cuda:
+        raise ValueError("target_probs must be a 2-D row-major float32 device tensor")
+    if out is None:
+        out = (torch.empty(n, dtype=i32, device=dev), torch.empty(n, dtype=i32, device=dev),
+               torch.zeros((n, target_probs.stride(0)), dtype=f32, device=dev) if residual else None)
+    nacc, tok, res = out
+    st = lib().tt_verify_noalloc(n, int(v_t), _ptr(target_ids, i32, "target_ids"), _ptr(target_off, i32, "target_off"),
+                                 _ptr(q, f32, "q"), ctypes.c_void_p(target_probs.data_ptr()),
+                                 int(target_probs.stride(0)), _ptr(u_accept, f32, "u_accept"),
+                                 _ptr(u_sample, f32, "u_sample"), int(max_m), _ptr(nacc, i32, "n_accepted"),
+                                 _ptr(tok, i32, "out_token"), _ptr(res, f32, "residual", allow_none=True),
+                                 _stream_handle(stream))
+    _check(st, "tt_verify_noalloc")
     return out
 
 
