@@ -574,12 +574,15 @@ int32_t orc_delta_quantile(const int64_t *hist, int32_t n_bins, int32_t num, int
  *            probability rows; if Z = 0 the first index of the largest x (0 if none).
  * Rows of at most 2^23 entries keep every sum below 2^63. */
 
-/* exp(x) for x <= 0: Cody-Waite reduction x = k ln2 + r (k = x log2(e) rounded to the
- * nearest integer, ties to even; r by two fused multiply-adds with ln2 split into its fp32
- * value and the fp32 value of the remainder), the degree-6 Taylor polynomial of exp(r) by
- * Horner's rule with fused multiply-adds, then scaling by 2^k.  0 below -87 and for NaN. */
+/* exp(x): Cody-Waite reduction x = k ln2 + r (k = x log2(e) rounded to the nearest
+ * integer, ties to even; r by two fused multiply-adds with ln2 split into its fp32 value and
+ * the fp32 value of the remainder), the degree-6 Taylor polynomial of exp(r) by Horner's rule
+ * with fused multiply-adds, then scaling by 2^k.  0 below -87 and for NaN.  An argument above
+ * 88 is taken as 88 (x - m <= 0 always; x - L is positive only when a caller's log-sum-exp L
+ * is below the row's logits), so 2^k stays finite and k fits an int. */
 float orc_sexp(float x) {
     if (!(x >= -87.0f)) return 0.0f;
+    if (x > 88.0f) x = 88.0f;
     const float kf = rintf(x * 0x1.715476p+0f);
     float r = fmaf(-kf, 0x1.62e430p-1f, x);
     r = fmaf(-kf, -0x1.05c610p-29f, r);

@@ -62,6 +62,20 @@ def test_sexp_ulp_bound_and_special_values(orc):
     assert np.all(np.diff(vals) >= 0)  # non-decreasing in x
 
 
+def test_sexp_above_zero_and_the_upper_clamp(orc):
+    """Positive arguments (a caller's log-sum-exp below the row's logits): within 3 ulp of exp
+    up to 88, arguments above 88 (+inf included) give exp(88), finite, and the function stays
+    non-decreasing across the clamp."""
+    xs = np.linspace(0.0, 88.0, 4001).astype(np.float32)
+    assert max(ulps(orc.sexp(x), math.exp(float(x))) for x in xs) <= 3.0
+    top = orc.sexp(88.0)
+    assert np.isfinite(top) and ulps(top, math.exp(88.0)) <= 3.0
+    for x in (88.001, 89.0, 1e3, 1.5e9, 3e38, float("inf")):
+        assert orc.sexp(x) == top, x
+    ys = np.linspace(80.0, 200.0, 500).astype(np.float32)
+    assert np.all(np.diff(np.array([orc.sexp(y) for y in ys])) >= 0)
+
+
 def one_position_batch(rng, logits_rows, q, N, t=None):
     """N streams with M = 1 over the same two rows (position 0 and the bonus row)."""
     V = logits_rows.shape[1]
