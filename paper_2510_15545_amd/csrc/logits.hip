@@ -8,7 +8,8 @@
 //   m      = max x over the row
 //   e(x)   = sexp(x - m): Cody-Waite reduction x = k ln2 + r (k = rint(x log2 e), r by two
 //            fused multiply-adds), the degree-6 Taylor polynomial of exp(r) by Horner's
-//            rule with fused multiply-adds, scaling by 2^k; 0 below -87
+//            rule with fused multiply-adds, scaling by 2^k; 0 below -87, an argument above 88
+//            taken as 88
 //   e39    = floor(e * 2^39), summed exactly in 64 bits (rows of at most 2^23 entries)
 //   S      = sum * 2^-39 rounded once to the nearest fp32 (ties to even)
 //   P(t_j) = e(t_j) / S; accept while q_j <= 0 or u_j < P(t_j) / q_j
@@ -57,8 +58,8 @@ __device__ __forceinline__ float sexp_core(float x) {
     return ldexpf(p, (int)kf);
 }
 
-// exp(x) for x <= 0 as specified above (0 for x < -87 and NaN)
-__device__ __forceinline__ float sexp(float x) { return x >= -87.0f ? sexp_core(x) : 0.0f; }
+// exp(x) as specified above (0 for x < -87 and NaN; an argument above 88 taken as 88)
+__device__ __forceinline__ float sexp(float x) { return x >= -87.0f ? sexp_core(fminf(x, 88.0f)) : 0.0f; }
 
 // floor(e * 2^39) for e in [0, 1] (exact: the high word is trunc(e * 2^7), the low word the
 // fraction s - floor(s), exact for s in [0, 128], scaled by 2^32)
@@ -113,12 +114,12 @@ struct LogitsParams {
     int32_t nc, vec;
 };
 
-// e39 of one logit: floor(clamp(sexp(x - base), 0, 1) * 2^39).  The argument is raised to at
-// least -100 (NaN becomes -100) and the cut-off of sexp left out: for an argument in
+// e39 of one logit: floor(clamp(sexp(x - base), 0, 1) * 2^39).  The argument is held in
+// [-100, 88] (NaN becomes -100) and the cut-off of sexp left out: for an argument in
 // [-100, -87) sexp_core gives at most 1.42 * 2^-125, which the floor maps to 0, as it does the
-// specified 0; from -87 up the two agree; +inf and NaN results are clamped as before.
+// specified 0; from -87 up the two agree.
 __device__ __forceinline__ uint64_t e39_of(uint32_t bits16, float it, float base) {
-    return q39(fminf(fmaxf(sexp_core(fmaxf(scaled(bits16, it) - base, -100.0f)), 0.0f), 1.0f));
+    return q39(fminf(fmaxf(sexp_core(fminf(fmaxf(scaled(bits16, it) - base, -100.0f), 88.0f)), 0.0f), 1.0f));
 }
 
 // Chunk sums of e39 over the row into sh_part (every wave, chunks wave, wave + 16, ...; the

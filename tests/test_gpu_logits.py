@@ -74,6 +74,17 @@ def test_logits_parity_with_lse(n, V, ld, shift):
     assert (nacc > 0).sum() > 0 and (nacc < Ms).sum() > 0
 
 
+@pytest.mark.parametrize("shift", [-100.0, -3e9])
+def test_logits_lse_far_below_the_logits(shift):
+    """A caller's log-sum-exp far below the row's logits: x - L runs past 88 (up to about 3e9,
+    where converting k to an int would overflow without the clamp at 88); every P clamps to 1
+    and each e39 saturates, on both sides alike."""
+    print(f"[case] logits+lse shift={shift}", flush=True)
+    case = logits_case(37, 1000, None, seed=4)
+    nacc, Ms = run_both(V=1000, case=case, max_m=8, lse=case_lse(1000, case, shift))
+    assert np.array_equal(nacc, Ms)  # P = 1 >= q: every proposal is accepted
+
+
 @pytest.mark.parametrize("with_lse", [False, True])
 def test_logits_wide_range(with_lse):
     """Logits spread over [-130, 5]: every x - m in the exponential's cut-off band [-100, -87),
