@@ -106,6 +106,8 @@ def parse():
     ap.add_argument("--eager", action="store_true", help="launch every call from Python (no HIP graph)")
     ap.add_argument("--graph-steps", type=int, default=8, help="consecutive steps captured in one HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="leave out the DTW stress batch and the high-acceptance batch of the default run")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="also run one plain device copy of this many MiB (counter calibration)")
@@ -422,12 +424,14 @@ def main():
                        "transfer_share_of_three_calls": round(times["transfer"] / (times["align"] + times["transfer"] +
                                                                                    times["verify"]), 4)},
         "tli_proposal": tli,
-        "verify": {"GBps": round(gbs_verify, 1), "frac_of_peak": round(gbs_verify / HBM_PEAK_GBS, 4),
-                   "algorithmic_bytes": verify_bytes, "accept_rate": round(float(acc[acc >= 0].sum()) /
-                                                                           max(1, int(m_s.sum())), 4)},
+        "verify": dict({"GBps": round(gbs_verify, 1), "frac_of_peak": round(gbs_verify / HBM_PEAK_GBS, 4),
+                        "algorithmic_bytes": verify_bytes}, **acceptance(acc, S.target_off)),
         "roofline": roof,
         "gen_seconds": round(t_gen, 1),
     }
+    if args.workload == 3 and args.streams is None and not args.no_extras:
+        result["dtw_stress"] = dtw_stress(dev, args.w)
+        result["high_acceptance"] = high_acceptance(dev, args, R)
 
     if not args.no_cpu_baseline:
         nacc_step = step_outputs[0] if step_outputs is not None else nacc
@@ -671,7 +675,126 @@ def main_logits(args):
 
 def synth_fits_fused(S):
     """The fused kernel's shape conditions (mirrors the library's dispatch rule)."""
-    return S.max_k <= 64 and S.max_m <= 64 and S.n >= 256 and (S.v_t + 1023) // 1024 * 8 <= 64 * 1024
+    nc = (S.v_t + 1023) // 1024
+    return S.max_k <= 64 and S.max_m <= 64 and ((S.n >= 256 and nc <= 2048) or S.v_t <= 16384)
+
+
+def graph_ms(fn, k=20, reps=10):
+    """ms per call: k calls captured in one HIP graph, replayed `reps` times, HIP events on the
+    stream the graph runs on."""
+    import torch
+
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            for i in range(k):
+                fn(i)
+    torch.cuda.current_stream().wait_stream(cap)
+    g.replay()
+    torch.cuda.synchronize()
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record()
+    for _ in range(reps):
+        g.replay()
+    s1.record()
+    torch.cuda.synchronize()
+    return s0.elapsed_time(s1) / (k * reps)
+
+
+def acceptance(nacc, target_off):
+    """Acceptance of a verified batch: accepted / proposed positions (sum gamma / sum M), accepted /
+    tested positions (a stream tests positions up to and including its first rejection), the
+    share of streams accepting at least one position and the mean gamma."""
+    g = np.asarray(nacc, np.int64)
+    M = np.diff(np.asarray(target_off, np.int64))
+    ok = g >= 0
+    g, M = g[ok], M[ok]
+    tested = np.minimum(g + 1, M)
+    return {"accept_rate": round(float(g.sum()) / max(1, int(M.sum())), 4),
+            "per_position_accept_rate": round(float(g.sum()) / max(1, int(tested.sum())), 4),
+            "streams_with_gamma_above_0": round(float((g > 0).mean()) if g.size else 0.0, 4),
+            "mean_gamma": round(float(g.mean()) if g.size else 0.0, 3)}
+
+
+def dtw_stress(dev, w):
+    """The DTW stress batch (workload 4: 1,024 pairs of 64-512 tokens each side) through tt_align,
+    with the strip kernel's VALU issue fraction and LDS bank-conflict rate from the counter
+    summary (when it covers the current kernel sources)."""
+    import torch
+
+    import paper_2510_15545_amd as tt
+    from paper_2510_15545_amd import synth
+
+    t0 = time.time()
+    wl = synth.make(4, probs=False, w=w)
+    gen = time.time() - t0
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    vd = tt.Vocab.from_host(wl.vocab_d.data, wl.vocab_d.offsets, wl.vocab_d.max_len, dev)
+    vt = tt.Vocab.from_host(wl.vocab_t.data, wl.vocab_t.offsets, wl.vocab_t.max_len, dev)
+    di, do, ti, to = t(wl.draft_ids), t(wl.draft_off), t(wl.target_ids), t(wl.target_off)
+    mtb = max(wl.vocab_d.max_len, wl.vocab_t.max_len)
+    ws = tt.align_workspace(wl.n, wl.max_k, wl.max_m, w, mtb, dev)
+    out = tt.align(vd, vt, di, do, ti, to, w, wl.max_k, wl.max_m,
+                   n_path=tt.path_capacity(wl.draft_off[-1], wl.target_off[-1]), workspace=ws)
+    torch.cuda.synchronize()
+    ms = graph_ms(lambda i: tt.align(vd, vt, di, do, ti, to, w, wl.max_k, wl.max_m, out=out, workspace=ws),
+                  k=10, reps=5)
+    K, M = np.diff(wl.draft_off), np.diff(wl.target_off)
+    cells = band_cells(K, M, w)
+    kv, why = read_counters(os.path.join(ROOT, "profiles", "dtw_band_counters.txt"), wl.spec.name, "dtw_band")
+    issue = None
+    if kv is not None:  # wave instructions over the 1,024 SIMDs' issue slots (one per 4 cycles)
+        issue = int(kv["valu_instructions_per_launch"]) / (256 * 4 * 2.4e9 / 4 * ms * 1e-3)
+    return {"workload": wl.spec.name, "pairs": wl.n, "w": w, "tt_align_us": round(ms * 1e3, 2),
+            "band_cells": cells, "band_cells_per_s": round(cells / (ms * 1e-3), 1),
+            "full_cells_per_s": round(int((K * M).sum()) / (ms * 1e-3), 1),
+            "valu_issue_frac": None if issue is None else round(issue, 4),
+            "lds_bank_conflict_rate": None if kv is None else float(kv["lds_bank_conflict_rate"]),
+            "counter_note": why or "dtw_band SQ_INSTS_VALU per launch over the tt_align call's time",
+            "gen_seconds": round(gen, 1)}
+
+
+def high_acceptance(dev, args, R):
+    """The benchmark batch with leading runs of forced positions instead of independent ones
+    (synth force_runs = 0.9): most streams accept several positions, so the rows after the
+    first position are the ones streamed.  One tt_step per step, and tt_verify alone."""
+    import torch
+
+    import paper_2510_15545_amd as tt
+    from paper_2510_15545_amd import synth
+
+    S = synth.make(3, w=args.w, force_runs=0.9)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    vd = tt.Vocab.from_host(S.vocab_d.data, S.vocab_d.offsets, S.vocab_d.max_len, dev)
+    vt = tt.Vocab.from_host(S.vocab_t.data, S.vocab_t.offsets, S.vocab_t.max_len, dev)
+    di, do, ti, to = t(S.draft_ids), t(S.draft_off), t(S.target_ids), t(S.target_off)
+    dp = t(S.draft_probs)
+    rows = [t(S.target_probs)]
+    for _ in range(R - 1):
+        rows.append(rows[0].clone())
+    ua, us = t(S.u_accept), t(S.u_sample)
+    n, mtb = S.n, max(S.vocab_d.max_len, S.vocab_t.max_len)
+    st_ws = tt.step_workspace(n, S.v_t, S.max_k, S.max_m, args.w, mtb, dev)
+    out = tt.step(vd, vt, S.v_d, S.v_t, di, do, ti, to, args.w, S.max_k, S.max_m, dp, rows[0], ua, us,
+                  workspace=st_ws)
+    step = lambda i: tt.step(vd, vt, S.v_d, S.v_t, di, do, ti, to, args.w, S.max_k, S.max_m, dp,  # noqa: E731
+                             rows[i % R], ua, us, workspace=st_ws, out=out)
+    ms_step = graph_ms(step, k=8, reps=10)
+    q = out[4]
+    ws = tt.verify_workspace(n, S.v_t, dev)
+    vo = (torch.empty(n, dtype=torch.int32, device=dev), torch.empty(n, dtype=torch.int32, device=dev), None)
+    ms_verify = graph_ms(lambda i: tt.verify(S.v_t, ti, to, q, rows[i % R], ua, us, S.max_m, workspace=ws, out=vo))
+    torch.cuda.synchronize()
+    m = np.diff(S.target_off)
+    vbytes = int(n * 4 * S.v_t + 16 * int(m.sum()) + 12 * n)
+    res = {"workload": S.spec.name.replace("30% forced", "forced leading runs (p 0.9)"),
+           "ms_per_step": round(ms_step, 5), "draft_tokens_per_s": round(int(S.draft_off[-1]) / (ms_step * 1e-3), 1),
+           "verify_us": round(ms_verify * 1e3, 2),
+           "verify_frac_of_peak": round(vbytes / (ms_verify * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    res.update(acceptance(out[5].cpu().numpy(), S.target_off))
+    return res
 
 
 def cpu_baseline(args, S, A, nacc, tok, s_out, a_out):

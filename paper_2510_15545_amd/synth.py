@@ -292,8 +292,13 @@ def _normal_row(width: int, sigma: float, seed) -> np.ndarray:
 
 
 def make(index: int, n_streams: int | None = None, seed_shift: int = 0, probs: bool = True,
-         w: int | None = None) -> Workload:
-    """Build workload `index` (1-5), optionally only its first `n_streams` streams."""
+         w: int | None = None, force_runs: float | None = None) -> Workload:
+    """Build workload `index` (1-5), optionally only its first `n_streams` streams.
+
+    force_runs (workload 3 only): instead of forcing each target position independently with
+    probability 0.3, force a leading run of positions per stream whose length is the number
+    of leading successes of Bernoulli(force_runs) trials, so that streams accept long
+    prefixes as a well-matched draft model would (force_runs = 0.9: mean run about 9)."""
     spec = SPECS[index]
     vd, vt = vocabs(index)
     n = spec.n_streams if n_streams is None else int(n_streams)
@@ -308,11 +313,11 @@ def make(index: int, n_streams: int | None = None, seed_shift: int = 0, probs: b
         wl.prob = _long_pair_prob_stage(spec, vd, vt, pairs, seed_shift, probs, wl.w)
         return wl
     if probs:
-        _make_probs(wl, seed_shift)
+        _make_probs(wl, seed_shift, force_runs)
     return wl
 
 
-def _make_probs(wl: Workload, seed_shift: int) -> None:
+def _make_probs(wl: Workload, seed_shift: int, force_runs: float | None = None) -> None:
     spec, n = wl.spec, wl.n
     c = spec.index
     seed_l = SEED_LOGITS + c + seed_shift
@@ -345,7 +350,11 @@ def _make_probs(wl: Workload, seed_shift: int) -> None:
             d = wl.draft_ids[wl.draft_off[b]:wl.draft_off[b + 1]]
             t = wl.target_ids[wl.target_off[b]:wl.target_off[b + 1]]
             owner = _span_owner(wl.vocab_d, wl.vocab_t, d, t)
-            hit = rng.random(len(t)) < 0.3
+            if force_runs is None:
+                hit = rng.random(len(t)) < 0.3
+            else:  # a leading run: positions before the first failed Bernoulli(force_runs) trial
+                trials = rng.random(len(t)) < force_runs
+                hit = np.cumprod(trials).astype(bool)
             for j in np.nonzero(hit)[0]:
                 forced[wl.target_off[b] + j] = 1
                 t_force[b][int(j)] = int(t[j])
