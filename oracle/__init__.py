@@ -65,8 +65,10 @@ def lib():
         L.orc_delta_histogram.restype = None
         L.orc_delta_quantile.argtypes = [P, i32, i32, i32]
         L.orc_delta_quantile.restype = i32
-        L.orc_sexp.argtypes = [f32]
-        L.orc_sexp.restype = f32
+        L.orc_exp2.argtypes = [f32]
+        L.orc_exp2.restype = f32
+        L.orc_logit_prob.argtypes = [f32, f32, f32]
+        L.orc_logit_prob.restype = f32
         L.orc_verify_logits.argtypes = [i32, i32, P, P, P, P, i64, P, P, P, P, i32, P, P, P, ctypes.c_int]
         L.orc_verify_logits.restype = None
         L.orc_threshold.argtypes = [f32, u64]
@@ -196,9 +198,14 @@ def sd_verify(v, draft_ids, off, draft_probs, target_probs, u_accept, u_sample, 
     return nacc, tok, res, z
 
 
-def sexp(x: float) -> np.float32:
-    """The software exponential of the logits path (x <= 0)."""
-    return np.float32(lib().orc_sexp(float(np.float32(x))))
+def exp2(z: float) -> np.float32:
+    """The logits path's specified 2^z (z held in [-1, 31])."""
+    return np.float32(lib().orc_exp2(float(np.float32(z))))
+
+
+def logit_prob(x: float, inv_temp: float, lse: float) -> np.float32:
+    """P_t of one logit (the fp32 value of its bf16) under a caller's log-sum-exp."""
+    return np.float32(lib().orc_logit_prob(float(np.float32(x)), float(np.float32(inv_temp)), float(np.float32(lse))))
 
 
 def verify_logits(v, target_ids, target_off, q, logits_bf16, inv_temp, u_accept, u_sample, max_m=None,

@@ -27,7 +27,7 @@
  *                     matched pairs on the optimal paths
  *   orc_delta_quantile   App. K: the deviation where that distribution reaches a quantile
  *   orc_verify_logits the verification from bf16 logits and a temperature (App. F), the
- *                     target softmax formed with a specified software exponential
+ *                     target softmax formed with a specified base-2 exponential
  *
  * Readings where the paper is silent or ambiguous (each is listed in the design
  * notes of the repository):
@@ -560,59 +560,80 @@ int32_t orc_delta_quantile(const int64_t *hist, int32_t n_bins, int32_t num, int
 /* ------------------------------------------------------------------------------------ */
 /* Verification from bf16 target logits with a temperature (the step before Sec. 3's target
  * distribution, App. F sampling temperatures): P_t = softmax(logit * inv_temp) formed inside
- * the verification.  Readings (the paper fixes none of this arithmetic):
- *   x        = fp32(bf16 logit) * inv_temp (fp32); NaN logits count as minus infinity;
- *   m        = the largest x of the row;
- *   e(x)     = orc_sexp(x - m), a specified software exponential (below);
- *   e39(x)   = floor(e(x) * 2^39) (exact: e <= 1 has 24 significant bits);
- *   S        = (sum of e39) * 2^-39 rounded once to the nearest fp32, ties to even;
- *   P_t(t_j) = e(t_j) / S (fp32), and the acceptance test of the one-hot path;
- *   residual on rejection at r: the row's e39 with the entry at t_r replaced by
- *            floor(clamp(e(t_r) - q_r * S, 0, 1) * 2^39) -- proportional to
- *            max(0, P_t - q_r e_{t_r}); after full acceptance the bonus row's e39;
+ * the verification, in base 2.  Readings (the paper fixes none of this arithmetic):
+ *   c        = inv_temp * log2(e), one fp32 product per stream (log2(e) rounded to fp32);
+ *   y        = fp32(bf16 logit) * c (fp32); NaN logits count as minus infinity;
+ *   mu       = the largest y of the row, or, with a caller's log-sum-exp L of the row (in the
+ *              natural units of logit * inv_temp), L * log2(e) (fp32);
+ *   z        = fma(fp32(bf16 logit), c, 31 - mu) (31 - mu rounded to fp32 first), the base-2
+ *              exponent of the logit's weight scaled by 2^31, held in [-1, 31] (NaN -> -1);
+ *   2^z      = p * 2^k with k = rint(z), f = z - k in [-1/2, 1/2] and p the degree-5 Taylor
+ *              polynomial of 2^f = exp(f ln 2) (coefficients (ln 2)^n / n! rounded to fp32,
+ *              Horner's rule with fused multiply-adds; relative error below 3.3e-6);
+ *   e31      = floor(p * 2^k), the logit's weight in Q31 (exact: p * 2^k < 2^32);
+ *   E        = p * 2^(k - 31) as fp32 when z >= 0, else 0 (the weight as a fraction of the
+ *              largest, cut where e31 is 0);
+ *   S        = (sum of e31) * 2^-31 rounded once to the nearest fp32, ties to even;
+ *   P_t(t_j) = E(t_j) / S (fp32), or E(t_j) when L is given (S = 1); accept iff q_j <= 0
+ *              or u_j < P_t(t_j) / q_j;
+ *   residual on rejection at r: the row's e31 with the entry at t_r replaced by
+ *            floor(clamp(E(t_r) - q_r * S, 0, 1) * 2^31) (with L: clamp(P - q_r, 0, 1)) --
+ *            proportional to max(0, P_t - q_r e_{t_r}); after full acceptance the bonus
+ *            row's e31;
  *   sample   T = floor(u * Z) and the first index whose prefix exceeds T, as for the
- *            probability rows; if Z = 0 the first index of the largest x (0 if none).
- * Rows of at most 2^23 entries keep every sum below 2^63. */
+ *            probability rows; if Z = 0 the first index of the largest y (0 if none).
+ * Weights below 2^-31 of the largest count as 0.  Rows of at most 2^23 entries keep every
+ * sum below 2^55. */
+#define ORC_L2E 0x1.715476p+0f
 
-/* exp(x): Cody-Waite reduction x = k ln2 + r (k = x log2(e) rounded to the nearest
- * integer, ties to even; r by two fused multiply-adds with ln2 split into its fp32 value and
- * the fp32 value of the remainder), the degree-6 Taylor polynomial of exp(r) by Horner's rule
- * with fused multiply-adds, then scaling by 2^k.  0 below -87 and for NaN.  An argument above
- * 88 is taken as 88 (x - m <= 0 always; x - L is positive only when a caller's log-sum-exp L
- * is below the row's logits), so 2^k stays finite and k fits an int. */
-float orc_sexp(float x) {
-    if (!(x >= -87.0f)) return 0.0f;
-    if (x > 88.0f) x = 88.0f;
-    const float kf = rintf(x * 0x1.715476p+0f);
-    float r = fmaf(-kf, 0x1.62e430p-1f, x);
-    r = fmaf(-kf, -0x1.05c610p-29f, r);
-    float p = 0x1.6c16c2p-10f;     /* 1/6! */
-    p = fmaf(p, r, 0x1.111112p-7f); /* 1/5! */
-    p = fmaf(p, r, 0x1.555556p-5f); /* 1/4! */
-    p = fmaf(p, r, 0x1.555556p-3f); /* 1/3! */
-    p = fmaf(p, r, 0.5f);
-    p = fmaf(p, r, 1.0f);
-    p = fmaf(p, r, 1.0f);
-    return ldexpf(p, (int)kf);
+/* 2^z = p * 2^k for z held in [-1, 31] (NaN -> -1): k = rint(z) (ties to even), f = z - k
+ * (exact), p = 1 + f ln2 + (f ln2)^2/2! + ... + (f ln2)^5/5! by Horner's rule in f. */
+static float orc_exp2_parts(float z, int *k) {
+    z = fminf(fmaxf(z, -1.0f), 31.0f);
+    const float kf = rintf(z);
+    const float f = z - kf;
+    float p = 0x1.5d87fep-10f;      /* (ln 2)^5 / 5! */
+    p = fmaf(p, f, 0x1.3b2ab6p-7f); /* (ln 2)^4 / 4! */
+    p = fmaf(p, f, 0x1.c6b08ep-5f); /* (ln 2)^3 / 3! */
+    p = fmaf(p, f, 0x1.ebfbe0p-3f); /* (ln 2)^2 / 2! */
+    p = fmaf(p, f, 0x1.62e430p-1f); /* ln 2 */
+    p = fmaf(p, f, 1.0f);
+    *k = (int)kf;
+    return p;
 }
 
-static uint64_t q39(float e) { /* floor(e * 2^39) for e in [0, 1] */
-    const float s = e * 128.0f;
-    const uint32_t hi = (uint32_t)s;
-    const uint32_t lo = (uint32_t)((s - (float)hi) * 4294967296.0f);
-    return ((uint64_t)hi << 32) | lo;
+/* Test hook: the specified 2^z as fp32 (z held in [-1, 31]). */
+float orc_exp2(float z) {
+    int k;
+    const float p = orc_exp2_parts(z, &k);
+    return ldexpf(p, k);
 }
 
-static float q39_to_f32(uint64_t n) { /* n * 2^-39 rounded to the nearest fp32, ties to even */
+static uint32_t orc_e31(float z) { /* floor(2^z) */
+    int k;
+    const float p = orc_exp2_parts(z, &k);
+    return (uint32_t)ldexpf(p, k);
+}
+
+static float orc_weight(float z) { /* E = 2^(z - 31), 0 when z < 0 or NaN */
+    if (!(z >= 0.0f)) return 0.0f;
+    int k;
+    const float p = orc_exp2_parts(z, &k);
+    return ldexpf(p, k - 31);
+}
+
+static uint32_t orc_q31(float r) { return (uint32_t)ldexpf(r, 31); } /* floor(r * 2^31), r in [0, 1] */
+
+static float q31_to_f32(uint64_t n) { /* n * 2^-31 rounded to the nearest fp32, ties to even */
     if (n == 0) return 0.0f;
     int bl = 64;
     while (!((n >> (bl - 1)) & 1u)) --bl;
-    if (bl <= 24) return ldexpf((float)n, -39);
+    if (bl <= 24) return ldexpf((float)n, -31);
     const int sh = bl - 24;
     uint64_t mant = n >> sh;
     const uint64_t rem = n & ((1ull << sh) - 1), half = 1ull << (sh - 1);
     if (rem > half || (rem == half && (mant & 1u))) ++mant;
-    return ldexpf((float)mant, sh - 39);
+    return ldexpf((float)mant, sh - 31);
 }
 
 static float bf16_to_f32(uint16_t h) {
@@ -620,6 +641,13 @@ static float bf16_to_f32(uint16_t h) {
     float f;
     memcpy(&f, &u, 4);
     return f;
+}
+
+/* Test hook: P_t of one logit x (fp32 value of its bf16) with a caller's log-sum-exp L. */
+float orc_logit_prob(float x, float inv_temp, float L) {
+    const float c = inv_temp * ORC_L2E;
+    const float mu = L * ORC_L2E;
+    return fminf(fmaxf(orc_weight(fmaf(x, c, 31.0f - mu)), 0.0f), 1.0f);
 }
 
 typedef struct {
@@ -635,46 +663,60 @@ typedef struct {
     uint64_t *z;
 } orc_logits_ctx;
 
-/* With per-row log-sum-exp values L_j supplied by the caller (in the units of x):
- * P(x) = clamp(sexp(x - L_j), 0, 1), the acceptance test on P(t_j) / q_j, and the residual
- * row r's entries floor(P * 2^39), the one at t_r floor(clamp(P(t_r) - q_r, 0, 1) * 2^39);
- * only the residual row is read in full. */
+/* Sample row `row` of weights e31 (the entry at t replaced by adj when t >= 0): returns the
+ * token and the mass Z. */
+static int32_t orc_logits_sample(const uint16_t *lg, int32_t v, float c, float b31, int32_t t, uint32_t adj,
+                                 float u, uint64_t *Zout) {
+    uint64_t *w = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)v);
+    uint64_t Z = 0;
+    float best = -INFINITY;
+    int32_t arg = 0;
+    for (int32_t i = 0; i < v; ++i) {
+        const float x = bf16_to_f32(lg[i]);
+        float y = x * c;
+        if (isnan(y)) y = -INFINITY;
+        if (y > best) {
+            best = y;
+            arg = i;
+        }
+        w[i] = (i == t) ? adj : orc_e31(fmaf(x, c, b31));
+        Z += w[i];
+    }
+    const int32_t token = Z == 0 ? arg : sample_quantised(w, v, Z, u);
+    free(w);
+    *Zout = Z;
+    return token;
+}
+
+/* With per-row log-sum-exp values L_j supplied by the caller: mu = L_j * log2(e), S = 1, the
+ * acceptance test on P = E(t_j), and one pass over the residual (or bonus) row. */
 static void orc_logits_stream_lse(orc_logits_ctx *c, int32_t b) {
     const int32_t t0 = c->off[b], M = c->off[b + 1] - t0;
-    const float it = c->inv_temp[b];
+    const float cs = c->inv_temp[b] * ORC_L2E;
     int32_t r = M;
+    float Pr = 0.0f;
     for (int32_t j = 0; j < M; ++j) {
         const int64_t row = t0 + b + j;
-        float xt = bf16_to_f32(c->logits[row * c->ld + c->ids[t0 + j]]) * it;
-        if (isnan(xt)) xt = -INFINITY;
-        const float P = fminf(fmaxf(orc_sexp(xt - c->lse[row]), 0.0f), 1.0f);
+        const float mu = c->lse[row] * ORC_L2E;
+        const float x = bf16_to_f32(c->logits[row * c->ld + c->ids[t0 + j]]);
+        const float P = fminf(fmaxf(orc_weight(fmaf(x, cs, 31.0f - mu)), 0.0f), 1.0f);
         const float qj = c->q[t0 + j];
         if (!(qj <= 0.0f || c->ua[t0 + j] < P / qj)) {
             r = j;
+            Pr = P;
             break;
         }
     }
     const int64_t row = t0 + b + r;
-    const uint16_t *lg = c->logits + row * c->ld;
-    uint64_t *e39 = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)c->v);
-    uint64_t Z = 0;
-    float best = -INFINITY;
-    int32_t arg = 0;
-    for (int32_t i = 0; i < c->v; ++i) {
-        float x = bf16_to_f32(lg[i]) * it;
-        if (isnan(x)) x = -INFINITY;
-        if (x > best) {
-            best = x;
-            arg = i;
-        }
-        float P = fminf(fmaxf(orc_sexp(x - c->lse[row]), 0.0f), 1.0f);
-        if (r < M && i == c->ids[t0 + r]) P = fminf(fmaxf(P - c->q[t0 + r], 0.0f), 1.0f);
-        Z += (e39[i] = q39(P));
+    const float mu = c->lse[row] * ORC_L2E;
+    int32_t t = -1;
+    uint32_t adj = 0;
+    if (r < M) {
+        t = c->ids[t0 + r];
+        adj = orc_q31(fminf(fmaxf(Pr - c->q[t0 + r], 0.0f), 1.0f)); /* NaN -> 0 */
     }
     c->nacc[b] = r;
-    c->tok[b] = Z == 0 ? arg : sample_quantised(e39, c->v, Z, c->us[b]);
-    c->z[b] = Z;
-    free(e39);
+    c->tok[b] = orc_logits_sample(c->logits + row * c->ld, c->v, cs, 31.0f - mu, t, adj, c->us[b], &c->z[b]);
 }
 
 static void orc_logits_stream(orc_logits_ctx *c, int32_t b) {
@@ -691,51 +733,32 @@ static void orc_logits_stream(orc_logits_ctx *c, int32_t b) {
         orc_logits_stream_lse(c, b);
         return;
     }
-    float *x = (float *)malloc(sizeof(float) * (size_t)c->v);
-    uint64_t *e39 = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)c->v);
-    const float it = c->inv_temp[b];
+    const float cs = c->inv_temp[b] * ORC_L2E;
     for (int32_t j = 0; j <= M; ++j) {
         const uint16_t *row = c->logits + (int64_t)(t0 + b + j) * c->ld;
-        float m = -INFINITY;
+        float mu = -INFINITY;
         for (int32_t i = 0; i < c->v; ++i) {
-            x[i] = bf16_to_f32(row[i]) * it;
-            if (isnan(x[i])) x[i] = -INFINITY;
-            if (x[i] > m) m = x[i];
+            const float y = bf16_to_f32(row[i]) * cs;
+            if (y > mu) mu = y; /* NaN never compares greater */
         }
+        const float b31 = 31.0f - mu;
         uint64_t Sq = 0;
-        for (int32_t i = 0; i < c->v; ++i) Sq += (e39[i] = q39(orc_sexp(x[i] - m)));
-        const float S = q39_to_f32(Sq);
-        uint64_t Z = Sq;
+        for (int32_t i = 0; i < c->v; ++i) Sq += orc_e31(fmaf(bf16_to_f32(row[i]), cs, b31));
+        const float S = q31_to_f32(Sq);
+        int32_t t = -1;
+        uint32_t adj = 0;
         if (j < M) {
-            const int32_t t = c->ids[t0 + j];
+            t = c->ids[t0 + j];
             const float qj = c->q[t0 + j];
-            const float et = orc_sexp(x[t] - m);
-            const float P = et / S;
+            const float Et = orc_weight(fmaf(bf16_to_f32(row[t]), cs, b31));
+            const float P = Et / S;
             if (qj <= 0.0f || c->ua[t0 + j] < P / qj) continue; /* accepted: next position */
-            float rt = et - qj * S;
-            rt = fminf(fmaxf(rt, 0.0f), 1.0f); /* NaN -> 0 */
-            const uint64_t before = e39[t];
-            e39[t] = q39(rt);
-            Z = Sq - before + e39[t];
-        }
-        int32_t token = 0;
-        if (Z == 0) {
-            float best = -INFINITY;
-            for (int32_t i = 0; i < c->v; ++i)
-                if (x[i] > best) {
-                    best = x[i];
-                    token = i;
-                }
-        } else {
-            token = sample_quantised(e39, c->v, Z, c->us[b]);
+            adj = orc_q31(fminf(fmaxf(Et - qj * S, 0.0f), 1.0f)); /* NaN -> 0 */
         }
         c->nacc[b] = j;
-        c->tok[b] = token;
-        c->z[b] = Z;
-        break;
+        c->tok[b] = orc_logits_sample(row, c->v, cs, b31, t, adj, c->us[b], &c->z[b]);
+        return;
     }
-    free(x);
-    free(e39);
 }
 
 static void orc_logits_range(void *p, int32_t lo, int32_t hi) {

@@ -33,7 +33,7 @@ void orc_sd_verify(int32_t n_streams, int32_t V, const int32_t *draft_ids, const
 void orc_delta_histogram(int32_t n_pairs, const int32_t *draft_off, const int32_t *target_off,
                          const int32_t *path_len, const int32_t *path, int32_t n_bins, int64_t *hist);
 uint64_t orc_threshold(float u, uint64_t Z);
-float orc_sexp(float x);
+float orc_exp2(float z);
 void orc_verify_logits(int32_t n_streams, int32_t v, const int32_t *target_ids, const int32_t *target_off,
                        const float *q, const uint16_t *logits, int64_t ld, const float *inv_temp,
                        const float *lse, const float *u_accept, const float *u_sample, int32_t max_m,
@@ -158,8 +158,8 @@ int main(void) {
     orc_verify_logits(3, VT, lids, loff, lq, lg, VT, lit, NULL, sua, lus, 4, lnacc, ltok, lz, 2);
     float llse[8] = {3.0f, 3.5f, 2.0f, 4.0f, 3.0f, 3.0f, 3.0f, 3.0f};
     orc_verify_logits(3, VT, lids, loff, lq, lg, VT, lit, llse, sua, lus, 4, lnacc, ltok, lz, 2);
-    printf("logits %d/%d %d/%d %d/%d sexp %.7g\n", lnacc[0], ltok[0], lnacc[1], ltok[1], lnacc[2], ltok[2],
-           (double)orc_sexp(-1.0f));
+    printf("logits %d/%d %d/%d %d/%d exp2 %.7g\n", lnacc[0], ltok[0], lnacc[1], ltok[1], lnacc[2], ltok[2],
+           (double)orc_exp2(-0.5f));
     free(lg);
 
     free(vdb); free(vtb); free(vdo); free(vto); free(dids); free(tids); free(path); free(map);

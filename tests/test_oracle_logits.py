@@ -1,8 +1,9 @@
 """Pins for the oracle's verification from bf16 logits (the target softmax formed inside the
 verification, with the sampling temperatures of App. F).
 
-The software exponential is checked against the C library's exp of the same fp32 argument
-(an ulp bound over a dense grid, exact special values); the verification is checked against
+The specified base-2 exponential is checked against 2^z in float64 (a relative bound over a
+dense grid, exact powers of two) and the per-logit probability against exp in float64; the
+verification is checked against
 laws computed independently in float64: with a one-hot proposal of mass 1 the emitted token
 follows softmax(logit / T), and after a rejection it follows the closed form of the
 transferred-proposal law (min(1, p/q) at the proposal, the rest in proportion); an exactly
@@ -50,30 +51,35 @@ def ulps(a: np.float32, b: float) -> float:
     return abs(float(a) - b) / float(np.spacing(np.float32(b)))
 
 
-def test_sexp_ulp_bound_and_special_values(orc):
-    xs = np.concatenate([-np.geomspace(1e-7, 86.99, 4000), np.linspace(-86.99, 0.0, 4001)]).astype(np.float32)
-    worst = max(ulps(orc.sexp(x), math.exp(float(x))) for x in xs)
-    assert worst <= 3.0, worst  # the reduction error grows with |k|: 2.6 ulp at x = -81
-    assert orc.sexp(0.0) == np.float32(1.0)
-    assert orc.sexp(-87.01) == 0 and orc.sexp(-1e30) == 0 and orc.sexp(float("nan")) == 0
-    assert orc.sexp(float("-inf")) == 0
-    ys = np.sort(xs)
-    vals = np.array([orc.sexp(y) for y in ys])
-    assert np.all(np.diff(vals) >= 0)  # non-decreasing in x
+def test_exp2_relative_error_and_exact_points(orc):
+    """The specified 2^z (degree-5 Taylor polynomial of 2^f on [-1/2, 1/2] after k = rint(z)):
+    within 3.5e-6 of 2^z (float64) over [-1, 31], exactly 2^k at integers, held at the ends of
+    [-1, 31] (NaN as -1)."""
+    zs = np.concatenate([np.linspace(-1.0, 31.0, 64001), np.linspace(-1.0, 1.0, 4001)]).astype(np.float32)
+    rel = max(abs(float(orc.exp2(z)) / 2.0 ** float(z) - 1.0) for z in zs)
+    assert rel <= 3.5e-6, rel
+    for k in range(-1, 32):
+        assert orc.exp2(float(k)) == np.float32(2.0 ** k)
+    assert orc.exp2(40.0) == orc.exp2(31.0) == np.float32(2.0 ** 31)
+    assert orc.exp2(-7.0) == orc.exp2(-1.0) == np.float32(0.5)
+    assert orc.exp2(float("nan")) == np.float32(0.5) and orc.exp2(float("-inf")) == np.float32(0.5)
+    assert orc.exp2(float("inf")) == np.float32(2.0 ** 31)
 
 
-def test_sexp_above_zero_and_the_upper_clamp(orc):
-    """Positive arguments (a caller's log-sum-exp below the row's logits): within 3 ulp of exp
-    up to 88, arguments above 88 (+inf included) give exp(88), finite, and the function stays
-    non-decreasing across the clamp."""
-    xs = np.linspace(0.0, 88.0, 4001).astype(np.float32)
-    assert max(ulps(orc.sexp(x), math.exp(float(x))) for x in xs) <= 3.0
-    top = orc.sexp(88.0)
-    assert np.isfinite(top) and ulps(top, math.exp(88.0)) <= 3.0
-    for x in (88.001, 89.0, 1e3, 1.5e9, 3e38, float("inf")):
-        assert orc.sexp(x) == top, x
-    ys = np.linspace(80.0, 200.0, 500).astype(np.float32)
-    assert np.all(np.diff(np.array([orc.sexp(y) for y in ys])) >= 0)
+def test_logit_prob_against_the_natural_softmax(orc):
+    """With a caller's log-sum-exp L, P(x) approximates exp(x * it - L) (float64) within the
+    exponential's error and the fp32 rounding of its arguments, is 0 where exp(x * it - L) is
+    below 2^-31 and 1 above the normaliser."""
+    rng = np.random.default_rng(9)
+    for _ in range(2000):
+        x = np.float32(rng.normal(0, 4))
+        it = np.float32(rng.uniform(0.5, 2.0))
+        L = np.float32(x * it + rng.uniform(0.0, 20.0))
+        want = math.exp(float(x) * float(it) - float(L))
+        got = float(orc.logit_prob(x, it, L))
+        assert abs(got - want) <= 2e-5 * want + 2.0 ** -31, (x, it, L, got, want)
+    assert orc.logit_prob(0.0, 1.0, 30.0) == 0.0  # exp(-30) < 2^-31 x 2^... : below the cut
+    assert orc.logit_prob(5.0, 1.0, 0.0) == 1.0
 
 
 def one_position_batch(rng, logits_rows, q, N, t=None):
@@ -124,23 +130,23 @@ def test_rejection_law_closed_form(orc, with_lse):
 
 
 def test_exact_softmax_fixes_the_accept_boundary(orc):
-    """Eight equal logits: every e = 1, S = 8 exactly, p(t) = 1/8; with q = 1/4 the ratio is 1/2,
-    so u = 1/2 - 2^-24 accepts and u = 1/2 rejects."""
+    """Eight logits 0: every z = 31 exactly, e31 = 2^31, S = 8, p(t) = 1/8; with q = 1/4 the
+    ratio is 1/2, so u = 1/2 - 2^-24 accepts and u = 1/2 rejects."""
     V = 8
-    bits = bf16_bits(np.full((2, V), 3.0, np.float32))
+    bits = bf16_bits(np.full((2, V), 0.0, np.float32))
     for u, want in ((0.5 - 2.0 ** -24, 1), (0.5, 0)):
         nacc, tok, z = orc.verify_logits(V, np.array([3], np.int32), np.array([0, 1], np.int32),
                                          np.array([0.25], np.float32), bits, np.ones(1, np.float32),
                                          np.array([u], np.float32), np.array([0.0], np.float32))
         assert nacc[0] == want
-        if want == 0:  # residual: p(t) - q < 0, so t has no mass; Z = 7 * 2^39; u_sample = 0 -> first token
-            assert int(z[0]) == 7 * 2 ** 39 and tok[0] == 0
+        if want == 0:  # residual: p(t) - q < 0, so t has no mass; Z = 7 * 2^31; u_sample = 0 -> first token
+            assert int(z[0]) == 7 * 2 ** 31 and tok[0] == 0
 
 
 def test_exact_normaliser_fixes_the_accept_boundary(orc):
-    """The normaliser is taken as given: logit 0 with L = 0 gives P = sexp(0) = 1 whatever the
+    """The normaliser is taken as given: logit 0 with L = 0 gives P = 2^0 = 1 whatever the
     other logits are, so with q = 1/2 every u accepts; with L = ln 2 (fp32) and q = 1,
-    P = sexp(-L) is within an ulp of 1/2 and u just below P accepts, u = P rejects."""
+    P = 2^(-L log2 e) is within an ulp of 1/2 and u just below P accepts, u = P rejects."""
     V = 4
     bits = bf16_bits(np.array([[0.0, -5.0, -5.0, -5.0], [0.0] * 4], np.float32))
     one = lambda lse0, qv, u: orc.verify_logits(V, np.array([0], np.int32), np.array([0, 1], np.int32),
@@ -149,7 +155,7 @@ def test_exact_normaliser_fixes_the_accept_boundary(orc):
                                                 lse=np.array([lse0, 0.0], np.float32))
     assert one(0.0, 0.5, 1.0 - 2.0 ** -24)[0][0] == 1
     L = np.float32(math.log(2.0))
-    P = float(orc.sexp(np.float32(-L)))
+    P = float(orc.logit_prob(0.0, 1.0, L))
     assert abs(P - 0.5) <= 2.0 ** -24
     below = np.nextafter(np.float32(P), np.float32(0))
     assert one(L, 1.0, below)[0][0] == 1 and one(L, 1.0, np.float32(P))[0][0] == 0
