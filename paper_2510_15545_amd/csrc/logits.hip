@@ -3,27 +3,26 @@
 // (App. F lists the sampling temperatures), so the caller never materialises fp32
 // probability rows.
 //
-// Arithmetic (every step specified, so any summation order gives the same token):
-//   x      = fp32(bf16 logit) * inv_temp; NaN counts as minus infinity (no mass, never the max)
-//   m      = max x over the row
-//   e(x)   = sexp(x - m): Cody-Waite reduction x = k ln2 + r (k = rint(x log2 e), r by two
-//            fused multiply-adds), the degree-6 Taylor polynomial of exp(r) by Horner's
-//            rule with fused multiply-adds, scaling by 2^k; 0 below -87, an argument above 88
-//            taken as 88
-//   e39    = floor(e * 2^39), summed exactly in 64 bits (rows of at most 2^23 entries)
-//   S      = sum * 2^-39 rounded once to the nearest fp32 (ties to even)
-//   P(t_j) = e(t_j) / S; accept while q_j <= 0 or u_j < P(t_j) / q_j
+// Arithmetic (every step specified, so any summation order gives the same token), in base 2:
+//   c      = inv_temp * log2(e) (fp32, once per stream); y = fp32(bf16 logit) * c, NaN counts
+//            as minus infinity (no mass, never the max)
+//   mu     = max y over the row, or L * log2(e) for a caller's log-sum-exp L (natural units)
+//   z      = fma(logit, c, 31 - mu) held in [-1, 31]: the logit's scaled base-2 exponent
+//   2^z    = p * 2^k, k = rint(z), p the degree-5 Taylor polynomial of 2^(z - k) (Horner, FMAs)
+//   e31    = floor(p * 2^k), the weight in Q31, summed exactly in 64 bits (rows <= 2^23 entries)
+//   E      = p * 2^(k - 31) (0 for z < 0); S = sum * 2^-31 rounded once to fp32 (ties to even)
+//   P(t_j) = E(t_j) / S (E(t_j) with L); accept while q_j <= 0 or u_j < P(t_j) / q_j
 //   after a rejection at r the entry t_r of the residual is
-//            floor(clamp(e(t_r) - q_r S, 0, 1) * 2^39), proportional to max(0, P - q_r e_t);
-//            after full acceptance the bonus row's e39 is sampled as is
-//   token  = first index whose prefix exceeds floor(u * Z); first largest x when Z = 0.
+//            floor(clamp(E(t_r) - q_r S, 0, 1) * 2^31), proportional to max(0, P - q_r e_t);
+//            after full acceptance the bonus row's e31 is sampled as is
+//   token  = first index whose prefix exceeds floor(u * Z); first largest y when Z = 0.
 //
 // One 1024-thread workgroup per stream.  Without normalisers it walks its rows 0, 1, ...
 // until the first rejection (each row: a max pass, then a pass of chunk sums into LDS -- the
 // second read mostly from the caches).  With per-row log-sum-exp values L from the caller
 // (an LM head can emit them with its logits) it uses m = L and S = 1: the acceptance test
 // needs one gathered logit per position and only the residual (or bonus) row is read, once.
-// Wave 0 samples: the chunk sums lane-blocked, the crossing chunk's e39 recomputed from its
+// Wave 0 samples: the chunk sums lane-blocked, the crossing chunk's e31 recomputed from its
 // 1024 logits.  A lane reads 16 consecutive bf16 (two 16-byte loads).
 #include "verify_core.h"
 
@@ -41,51 +40,60 @@ constexpr int kChunk = 1024;  // logits per chunk: one wave, 16 per lane
 
 __device__ __forceinline__ float bf16_value(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
 
-// The reduction, polynomial and scaling of sexp without its cut-off (for any x; garbage, inf
-// or NaN where x is below -87 or not finite).  Branch-free, so a wave takes no divergent
-// branch per logit.
-__device__ __forceinline__ float sexp_core(float x) {
-    const float kf = rintf(x * 0x1.715476p+0f);
-    float r = fmaf(-kf, 0x1.62e430p-1f, x);
-    r = fmaf(-kf, -0x1.05c610p-29f, r);
-    float p = 0x1.6c16c2p-10f;
-    p = fmaf(p, r, 0x1.111112p-7f);
-    p = fmaf(p, r, 0x1.555556p-5f);
-    p = fmaf(p, r, 0x1.555556p-3f);
-    p = fmaf(p, r, 0.5f);
-    p = fmaf(p, r, 1.0f);
-    p = fmaf(p, r, 1.0f);
-    return ldexpf(p, (int)kf);
+constexpr float kLog2e = 0x1.715476p+0f;  // log2(e) rounded to fp32
+
+// 2^z = p * 2^k for z held in [-1, 31] (NaN gives p * 2^k < 1, a zero weight): k = rint(z),
+// f = z - k in [-1/2, 1/2] (exact), p = 1 + f ln2 + ... + (f ln2)^5 / 5! by Horner's rule.
+__device__ __forceinline__ float exp2_parts(float z, int &k) {
+    z = fminf(fmaxf(z, -1.0f), 31.0f);
+    const float kf = rintf(z);
+    const float f = z - kf;
+    float p = 0x1.5d87fep-10f;
+    p = fmaf(p, f, 0x1.3b2ab6p-7f);
+    p = fmaf(p, f, 0x1.c6b08ep-5f);
+    p = fmaf(p, f, 0x1.ebfbe0p-3f);
+    p = fmaf(p, f, 0x1.62e430p-1f);
+    p = fmaf(p, f, 1.0f);
+    k = (int)kf;
+    return p;
 }
 
-// exp(x) as specified above (0 for x < -87 and NaN; an argument above 88 taken as 88)
-__device__ __forceinline__ float sexp(float x) { return x >= -87.0f ? sexp_core(fminf(x, 88.0f)) : 0.0f; }
-
-// floor(e * 2^39) for e in [0, 1] (exact: the high word is trunc(e * 2^7), the low word the
-// fraction s - floor(s), exact for s in [0, 128], scaled by 2^32)
-__device__ __forceinline__ uint64_t q39(float e) {
-    const float s = e * 128.0f;
-    const uint32_t hi = (uint32_t)s;
-    const uint32_t lo = (uint32_t)(__builtin_amdgcn_fractf(s) * 4294967296.0f);
-    return ((uint64_t)hi << 32) | lo;
+// floor(2^z): the weight in Q31 of a logit whose scaled exponent is z (p * 2^k < 2^32)
+__device__ __forceinline__ uint32_t e31_at(float z) {
+    int k;
+    const float p = exp2_parts(z, k);
+    return (uint32_t)ldexpf(p, k);
 }
 
-// n * 2^-39 rounded to the nearest fp32, ties to even
-__device__ inline float q39_to_f32(uint64_t n) {
+// E = 2^(z - 31) as fp32, 0 when z < 0 or NaN (where the Q31 weight is 0)
+__device__ __forceinline__ float weight_at(float z) {
+    if (!(z >= 0.0f)) return 0.0f;
+    int k;
+    const float p = exp2_parts(z, k);
+    return ldexpf(p, k - 31);
+}
+
+// floor(r * 2^31) for r in [0, 1]
+__device__ __forceinline__ uint32_t q31(float r) { return (uint32_t)ldexpf(r, 31); }
+
+// n * 2^-31 rounded to the nearest fp32, ties to even
+__device__ inline float q31_to_f32(uint64_t n) {
     if (n == 0) return 0.0f;
     const int bl = 64 - __clzll(n);
-    if (bl <= 24) return ldexpf((float)n, -39);
+    if (bl <= 24) return ldexpf((float)n, -31);
     const int sh = bl - 24;
     uint64_t mant = n >> sh;
     const uint64_t rem = n & ((1ull << sh) - 1), half = 1ull << (sh - 1);
     if (rem > half || (rem == half && (mant & 1u))) ++mant;
-    return ldexpf((float)mant, sh - 39);
+    return ldexpf((float)mant, sh - 31);
 }
 
-// x = logit * inv_temp.  A NaN x is left as is: it acts as minus infinity everywhere it is
-// used -- sexp returns 0 for a NaN argument (as for -inf - m), fmaxf ignores it in the max
-// pass, and it never compares greater in the first-argmax fallback.
-__device__ __forceinline__ float scaled(uint32_t bits16, float it) { return bf16_value(bits16) * it; }
+// y = logit * c.  A NaN y is left as is: fmaxf ignores it in the max pass and it never
+// compares greater in the first-argmax fallback; its scaled exponent gives a zero weight.
+__device__ __forceinline__ float scaled(uint32_t bits16, float c) { return bf16_value(bits16) * c; }
+
+// the scaled exponent z of a logit: fma(logit, c, b31) with b31 = 31 - mu
+__device__ __forceinline__ float expo(uint32_t bits16, float c, float b31) { return fmaf(bf16_value(bits16), c, b31); }
 
 // The 16 logits of a lane in chunk c (elements c*1024 + lane*16 + k, zero bits past v).
 __device__ __forceinline__ void load16(const uint16_t *row, int x0, int v, bool vec, uint32_t (&w)[8]) {
@@ -114,17 +122,9 @@ struct LogitsParams {
     int32_t nc, vec;
 };
 
-// e39 of one logit: floor(clamp(sexp(x - base), 0, 1) * 2^39).  The argument is held in
-// [-100, 88] (NaN becomes -100) and the cut-off of sexp left out: for an argument in
-// [-100, -87) sexp_core gives at most 1.42 * 2^-125, which the floor maps to 0, as it does the
-// specified 0; from -87 up the two agree.
-__device__ __forceinline__ uint64_t e39_of(uint32_t bits16, float it, float base) {
-    return q39(fminf(fmaxf(sexp_core(fminf(fmaxf(scaled(bits16, it) - base, -100.0f), 88.0f)), 0.0f), 1.0f));
-}
-
-// Chunk sums of e39 over the row into sh_part (every wave, chunks wave, wave + 16, ...; the
+// Chunk sums of e31 over the row into sh_part (every wave, chunks wave, wave + 16, ...; the
 // next chunk's loads are issued before the current chunk's arithmetic).
-__device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, bool vec, float it, float base,
+__device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, bool vec, float sc, float b31,
                                            uint64_t *sh_part) {
     const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     uint32_t w[8] = {}, nx[8] = {};
@@ -135,10 +135,10 @@ __device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, b
         uint64_t acc = 0;
         if (x0 + 16 <= v) {
 #pragma unroll
-            for (int k = 0; k < 16; ++k) acc += e39_of(elem(w, k), it, base);
+            for (int k = 0; k < 16; ++k) acc += e31_at(expo(elem(w, k), sc, b31));
         } else {
 #pragma unroll
-            for (int k = 0; k < 16; ++k) acc += x0 + k < v ? e39_of(elem(w, k), it, base) : 0ull;
+            for (int k = 0; k < 16; ++k) acc += x0 + k < v ? e31_at(expo(elem(w, k), sc, b31)) : 0u;
         }
         acc = wave_inclusive_scan(acc);
         if (lane == kWave - 1) sh_part[c] = acc;
@@ -149,14 +149,14 @@ __device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, b
 
 // Inverse-CDF sample of a row from its chunk sums (one wave): the entry at t (if >= 0) is adj;
 // the first largest x when Z = 0.
-__device__ inline int sample_row(const uint16_t *row, int v, int nc, bool vec, float it, float base, int t,
+__device__ inline int sample_row(const uint16_t *row, int v, int nc, bool vec, float sc, float b31, int t,
                                  uint64_t adj, uint64_t Z, float u, const uint64_t *sh_part) {
     const int lane = threadIdx.x % kWave;
     if (Z == 0) {
         float bv = -INFINITY;
         int bi = INT_MAX;
         for (int x = lane; x < v; x += kWave) {
-            const float xv = scaled(row[x], it);
+            const float xv = scaled(row[x], sc);
             if (xv > bv) {
                 bv = xv;
                 bi = x;
@@ -206,7 +206,7 @@ __device__ inline int sample_row(const uint16_t *row, int v, int nc, bool vec, f
     uint64_t sum = 0;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
-        uint64_t e = x0 + k < v ? e39_of(elem(w, k), it, base) : 0ull;
+        uint64_t e = x0 + k < v ? e31_at(expo(elem(w, k), sc, b31)) : 0u;
         if (x0 + k == t) e = adj;
         qv[k] = e;
         sum += e;
@@ -231,7 +231,7 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
     const int b = blockIdx.x;
     const int tid = threadIdx.x, lane = tid % kWave;
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-    extern __shared__ uint64_t sh_part[];  // nc chunk sums of e39
+    extern __shared__ uint64_t sh_part[];  // nc chunk sums of e31
     __shared__ float sh_red[kWaves];
     __shared__ int sh_ok, sh_r;
     __shared__ float sh_m, sh_L, sh_q, sh_P;
@@ -242,6 +242,7 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
     const float it = a.inv_temp[b];
+    const float cb = it * kLog2e;  // the stream's base-2 scale
     const int v = a.v_t, nc = p.nc;
     const bool vec = p.vec != 0;
     if (wave == 0) {
@@ -279,7 +280,7 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
                     const int64_t r = t0 + b + j;
                     tj = a.target_ids[t0 + j];
                     Lj = a.lse[r];
-                    P = fminf(fmaxf(sexp(scaled(a.logits[r * a.ld + tj], it) - Lj), 0.0f), 1.0f);
+                    P = fminf(fmaxf(weight_at(expo(a.logits[r * a.ld + tj], cb, 31.0f - Lj * kLog2e)), 0.0f), 1.0f);
                     qj = a.q[t0 + j];
                     rej = !(qj <= 0.0f || a.u_accept[t0 + j] < P / qj);
                 }
@@ -306,7 +307,8 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         const int64_t rr = t0 + b + r;
         const uint16_t *row = a.logits + rr * a.ld;
         const float L = sh_L;
-        chunk_sums(row, v, nc, vec, it, L, sh_part);
+        const float b31 = 31.0f - L * kLog2e;
+        chunk_sums(row, v, nc, vec, cb, b31, sh_part);
         __syncthreads();
         if (wave != 0) return;
         uint64_t local = 0;
@@ -316,13 +318,13 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         uint64_t adj = 0;
         if (r < M) {  // the rejected proposal loses q_r of its mass
             t = sh_t;
-            const float Pt = sh_P;  // clamp(sexp(x_t - L), 0, 1), as the chunk sums count it
-            adj = q39(fminf(fmaxf(Pt - sh_q, 0.0f), 1.0f));
-            const uint64_t before = q39(Pt);
+            const float Pt = sh_P;  // E(t) held in [0, 1]: floor(Pt * 2^31) is the e31 the chunk sums count
+            adj = q31(fminf(fmaxf(Pt - sh_q, 0.0f), 1.0f));
+            const uint64_t before = q31(Pt);
             Z = Z - before + adj;
             if (lane == 0) sh_part[t / kChunk] = sh_part[t / kChunk] - before + adj;
         }
-        const int token = sample_row(row, v, nc, vec, it, L, t, adj, Z, a.u_sample[b], sh_part);
+        const int token = sample_row(row, v, nc, vec, cb, b31, t, adj, Z, a.u_sample[b], sh_part);
         if (lane == 0) {
             a.n_accepted[b] = r;
             a.out_token[b] = token;
@@ -340,11 +342,11 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
             if (c + kWaves < nc) load16(row, x0 + kWaves * kChunk, v, vec, nx);
             if (x0 + 16 <= v) {
 #pragma unroll
-                for (int k = 0; k < 16; ++k) m = fmaxf(m, scaled(elem(w, k), it));
+                for (int k = 0; k < 16; ++k) m = fmaxf(m, scaled(elem(w, k), cb));
             } else {
 #pragma unroll
                 for (int k = 0; k < 16; ++k)
-                    if (x0 + k < v) m = fmaxf(m, scaled(elem(w, k), it));
+                    if (x0 + k < v) m = fmaxf(m, scaled(elem(w, k), cb));
             }
 #pragma unroll
             for (int k = 0; k < 8; ++k) w[k] = nx[k];
@@ -359,8 +361,9 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         }
         __syncthreads();
         m = sh_m;
-        // pass 2: chunk sums of e39
-        chunk_sums(row, v, nc, vec, it, m, sh_part);
+        // pass 2: chunk sums of e31
+        const float b31 = 31.0f - m;
+        chunk_sums(row, v, nc, vec, cb, b31, sh_part);
         __syncthreads();
         // S, the acceptance test of position j, and the residual's entry at t_j
         if (wave == 0) {
@@ -368,21 +371,21 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
             for (int c = lane; c < nc; c += kWave) local += sh_part[c];
             const uint64_t Sq = lane_value(wave_inclusive_scan(local), kWave - 1);
             if (lane == 0) {
-                const float S = q39_to_f32(Sq);
+                const float S = q31_to_f32(Sq);
                 int next = 0;
                 uint64_t Z = Sq, adj = 0;
                 int t = -1;
                 if (j < M) {
                     t = a.target_ids[t0 + j];
                     const float qj = a.q[t0 + j];
-                    const float et = sexp(scaled(row[t], it) - m);
+                    const float et = weight_at(expo(row[t], cb, b31));
                     const float P = et / S;
                     if (qj <= 0.0f || a.u_accept[t0 + j] < P / qj) {
                         next = 1;
                     } else {
                         const float rt = fminf(fmaxf(et - qj * S, 0.0f), 1.0f);  // NaN -> 0
-                        const uint64_t before = q39(et);
-                        adj = q39(rt);
+                        const uint64_t before = e31_at(expo(row[t], cb, b31));
+                        adj = q31(rt);
                         Z = Sq - before + adj;
                         sh_part[t / kChunk] = sh_part[t / kChunk] - before + adj;
                     }
@@ -396,7 +399,7 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         __syncthreads();
         if (sh_next) continue;
         if (wave == 0) {
-            const int token = sample_row(row, v, nc, vec, it, m, sh_t, sh_adj, sh_Z, a.u_sample[b], sh_part);
+            const int token = sample_row(row, v, nc, vec, cb, b31, sh_t, sh_adj, sh_Z, a.u_sample[b], sh_part);
             if (lane == 0) {
                 a.n_accepted[b] = j;
                 a.out_token[b] = token;
