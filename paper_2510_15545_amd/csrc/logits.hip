@@ -26,6 +26,8 @@
 // 1024 logits.  A lane reads 16 consecutive bf16 (two 16-byte loads).
 #include "verify_core.h"
 
+TT_STAMPS_TABLE(logits)
+
 namespace tt {
 namespace {
 
@@ -122,36 +124,162 @@ struct LogitsParams {
     int32_t nc, vec;
 };
 
-// Chunk sums of e31 over the row into sh_part (every wave, chunks wave, wave + 16, ...; the
-// next chunk's loads are issued before the current chunk's arithmetic).
-__device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, bool vec, float sc, float b31,
-                                           uint64_t *sh_part) {
-    const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    uint32_t w[8] = {}, nx[8] = {};
-    if (wave < nc) load16(row, wave * kChunk + lane * 16, v, vec, w);
-    for (int c = wave; c < nc; c += kWaves) {
-        const int x0 = c * kChunk + lane * 16;
-        if (c + kWaves < nc) load16(row, x0 + kWaves * kChunk, v, vec, nx);
-        uint64_t acc = 0;
-        if (x0 + 16 <= v) {
-#pragma unroll
-            for (int k = 0; k < 16; ++k) acc += e31_at(expo(elem(w, k), sc, b31));
-        } else {
-#pragma unroll
-            for (int k = 0; k < 16; ++k) acc += x0 + k < v ? e31_at(expo(elem(w, k), sc, b31)) : 0u;
-        }
-        acc = wave_inclusive_scan(acc);
-        if (lane == kWave - 1) sh_part[c] = acc;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) w[k] = nx[k];
+// Per-row table of the Q31 weights.  For a fixed scale and offset the weight of a logit is a
+// function of its 16 bits, so the row pass looks it up instead of evaluating the exponential:
+// the table holds e31_at(expo(bits)) for every pattern whose magnitude lies in [2^-20, 2^8)
+// (exponent fields 107 .. 134, 3,584 patterns a sign), as 64-bit entries that add straight into
+// the 64-bit sums.  Each sign owns a half of 4,096 slots (32 KiB, so the pattern's sign bit,
+// left in place, is the byte offset of its half); slot 0 and slot 3,585 of a half are sentinels,
+// 2^40 (a weight is at most 2^31: z <= 31), onto which magnitudes outside the domain clamp
+// (tiny values, |x| >= 256, infinities, NaNs).  A lane group whose sum reaches 2^40 met one and
+// is summed again from the formula.
+constexpr uint32_t kMagLo = 107u << 7;  // bf16 magnitude bits of 2^-20
+constexpr uint32_t kTabMags = 28u << 7;
+constexpr int kTabHalf = 4096;
+constexpr int kTabSlots = 2 * kTabHalf;
+constexpr uint64_t kSentinel = 1ull << 40;
+
+__device__ __forceinline__ void build_table(uint64_t *tab, float sc, float b31) {
+    for (int i = threadIdx.x; i < kTabSlots; i += kThreads) {
+        const uint32_t s = (uint32_t)i / kTabHalf, j = (uint32_t)i % kTabHalf;
+        if (j > kTabMags + 1) continue;  // never addressed
+        uint64_t e = kSentinel;
+        if (j > 0 && j <= kTabMags) e = e31_at(expo((s << 15) | (kMagLo + j - 1), sc, b31));
+        tab[i] = e;
     }
 }
 
-// Inverse-CDF sample of a row from its chunk sums (one wave): the entry at t (if >= 0) is adj;
-// the first largest x when Z = 0.
-__device__ inline int sample_row(const uint16_t *row, int v, int nc, bool vec, float sc, float b31, int t,
-                                 uint64_t adj, uint64_t Z, float u, const uint64_t *sh_part) {
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// The LDS byte offsets of the two bf16 in a 32-bit word (low half first), both formed at once
+// with packed 16-bit operations: the magnitude clamped to the domain's frame, rebased and
+// scaled to a byte offset, and the pattern's sign bit kept as the half's offset.
+__device__ __forceinline__ uint32_t tab_offsets(uint32_t w) {
+    u16x2 t = __builtin_bit_cast(u16x2, w & 0x7FFF7FFFu);
+    t = __builtin_elementwise_max(t, (u16x2)(unsigned short)(kMagLo - 1));
+    t = __builtin_elementwise_min(t, (u16x2)(unsigned short)(kMagLo + kTabMags));
+    // (t - (kMagLo - 1)) * 8, modulo 2^16 (the true value is below 2^15)
+    t = t * (u16x2)(unsigned short)8 - (u16x2)(unsigned short)((kMagLo - 1) * 8);
+    return __builtin_bit_cast(uint32_t, t) | (w & 0x80008000u);
+}
+
+__device__ __forceinline__ uint64_t tab_at(const uint64_t *tab, uint32_t byte_off) {
+    return *reinterpret_cast<const uint64_t *>(reinterpret_cast<const char *>(tab) + byte_off);
+}
+
+// The 16 weights of a lane's logits x0 .. x0+15 (0 past v) into e; a sentinel for a logit
+// outside the table's domain is replaced by the formula's weight.
+__device__ __forceinline__ void lane_weights(const uint64_t *tab, const uint32_t (&w)[8], int x0, int v, float sc,
+                                             float b31, uint64_t (&e)[16]) {
+    uint64_t any = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const uint32_t o = tab_offsets(w[k]);
+        e[2 * k] = x0 + 2 * k < v ? tab_at(tab, o & 0xFFFFu) : 0u;
+        e[2 * k + 1] = x0 + 2 * k + 1 < v ? tab_at(tab, o >> 16) : 0u;
+        any |= e[2 * k] | e[2 * k + 1];
+    }
+    if (any >= kSentinel) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) e[k] = x0 + k < v ? e31_at(expo(elem(w, k), sc, b31)) : 0u;
+    }
+}
+
+// v plus v shifted across lanes by a DPP control (32 bits; lanes without a source add 0)
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_add32(uint32_t v) {
+    return v + __builtin_amdgcn_update_dpp(0u, v, CTRL, ROW_MASK, 0xF, true);
+}
+
+__device__ __forceinline__ uint32_t wave_total32(uint32_t v) {  // valid in lane 63
+    v = dpp_add32<0x111, 0xF>(v);  // row_shr:1
+    v = dpp_add32<0x112, 0xF>(v);  // row_shr:2
+    v = dpp_add32<0x114, 0xF>(v);  // row_shr:4
+    v = dpp_add32<0x118, 0xF>(v);  // row_shr:8
+    v = dpp_add32<0x142, 0xA>(v);  // row_bcast:15
+    v = dpp_add32<0x143, 0xC>(v);  // row_bcast:31
+    return v;
+}
+
+// The wave's total of per-lane sums of 16 weights (each at most 2^35), in lane 63: the low 20
+// and the high 15 bits are summed as 32-bit values (64 of them stay below 2^26 and 2^21).
+__device__ __forceinline__ uint64_t chunk_total(uint64_t a) {
+    const uint32_t lo = wave_total32((uint32_t)a & 0xFFFFFu);
+    const uint32_t hi = wave_total32((uint32_t)(a >> 20));
+    return ((uint64_t)hi << 20) + lo;
+}
+
+// The row's weight table, then its chunk sums of e31 into sh_part.  Every wave first issues the
+// loads of its first two chunks, so that their latency passes while the table is built; waves
+// take chunks from the LDS counter *next (which the caller sets to kWaves before a barrier that
+// precedes the call; wave w starts at chunk w), one chunk in flight ahead of the one summed.
+__device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, bool vec, float sc, float b31,
+                                           uint64_t *tab, uint64_t *sh_part, int *next) {
+    const int lane = threadIdx.x % kWave, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    uint32_t w[8] = {}, nx[8] = {};
+    int c = wave, cn = nc, cnn = nc;  // chunk summed, chunk in flight, the one after it
+    if (c < nc) {
+        load16(row, c * kChunk + lane * 16, v, vec, w);
+        cn = vcore::next_chunk(next, c, kWaves);
+        if (cn < nc) {
+            load16(row, cn * kChunk + lane * 16, v, vec, nx);
+            cnn = vcore::next_chunk(next, cn, kWaves);
+        }
+    }
+    build_table(tab, sc, b31);
+    __syncthreads();
+    while (c < nc) {
+        const int x0 = c * kChunk + lane * 16;
+        uint64_t acc = 0;
+        if (x0 + 16 <= v) {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const uint32_t o = tab_offsets(w[k]);
+                acc += tab_at(tab, o & 0xFFFFu) + tab_at(tab, o >> 16);
+            }
+            if (acc >= kSentinel) {  // a logit outside the table's domain: the lane group by the formula
+                acc = 0;
+#pragma unroll
+                for (int k = 0; k < 16; ++k) acc += e31_at(expo(elem(w, k), sc, b31));
+            }
+        } else {  // the row's ragged end
+            uint64_t e[16];
+            lane_weights(tab, w, x0, v, sc, b31, e);
+#pragma unroll
+            for (int k = 0; k < 16; ++k) acc += e[k];
+        }
+        acc = chunk_total(acc);
+        if (lane == kWave - 1) sh_part[c] = acc;
+        c = cn;
+        if (c < nc) {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) w[k] = nx[k];
+            cn = cnn;
+            if (cn < nc) {
+                load16(row, cn * kChunk + lane * 16, v, vec, nx);
+                cnn = vcore::next_chunk(next, cn, kWaves);
+            }
+        }
+    }
+}
+
+// Inverse-CDF sample of a row from its chunk sums (one wave).  When t >= 0 the entry at t
+// counts adj instead of the before its chunk sum holds (the residual's entry); Z is the row's
+// total so adjusted.  The first largest x when Z = 0.
+__device__ inline int sample_row(const uint16_t *row, int v, int nc, bool vec, float sc, float b31,
+                                 const uint64_t *tab, int t, uint64_t adj, uint64_t before, float u,
+                                 const uint64_t *sh_part) {
     const int lane = threadIdx.x % kWave;
+    // chunk sums lane-blocked: lane l holds chunks [l*per, (l+1)*per)
+    const int per = (nc + kWave - 1) / kWave;
+    const int ca = lane * per < nc ? lane * per : nc;
+    const int cb = ca + per < nc ? ca + per : nc;
+    const int ct = t >= 0 ? t / kChunk : -1;
+    uint64_t local = 0;
+    for (int c = ca; c < cb; ++c) local += sh_part[c];
+    if (ct >= ca && ct < cb) local = local - before + adj;
+    const uint64_t incl = wave_inclusive_scan(local);
+    const uint64_t Z = lane_value(incl, kWave - 1);
     if (Z == 0) {
         float bv = -INFINITY;
         int bi = INT_MAX;
@@ -173,13 +301,6 @@ __device__ inline int sample_row(const uint16_t *row, int v, int nc, bool vec, f
         return bi == INT_MAX ? 0 : bi;
     }
     const uint64_t T = exact_threshold(u, Z);
-    // chunk sums lane-blocked: lane l holds chunks [l*per, (l+1)*per)
-    const int per = (nc + kWave - 1) / kWave;
-    const int ca = lane * per < nc ? lane * per : nc;
-    const int cb = ca + per < nc ? ca + per : nc;
-    uint64_t local = 0;
-    for (int c = ca; c < cb; ++c) local += sh_part[c];
-    const uint64_t incl = wave_inclusive_scan(local);
     const uint64_t excl = incl - local;
     const unsigned long long hit = __ballot(excl <= T && T < incl);
     if (hit == 0ull) return v - 1;  // only if the sums wrapped (rows longer than allowed)
@@ -189,7 +310,7 @@ __device__ inline int sample_row(const uint16_t *row, int v, int nc, bool vec, f
     if (lane == owner) {
         uint64_t run = excl;
         for (int c = ca; c < cb; ++c) {
-            const uint64_t nx = run + sh_part[c];
+            const uint64_t nx = run + (c == ct ? sh_part[c] - before + adj : sh_part[c]);
             if (nx > T) break;
             cs = c + 1;
             base_sum = nx;
@@ -203,13 +324,12 @@ __device__ inline int sample_row(const uint16_t *row, int v, int nc, bool vec, f
     uint32_t w[8];
     load16(row, x0, v, vec, w);
     uint64_t qv[16];
+    lane_weights(tab, w, x0, v, sc, b31, qv);
     uint64_t sum = 0;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
-        uint64_t e = x0 + k < v ? e31_at(expo(elem(w, k), sc, b31)) : 0u;
-        if (x0 + k == t) e = adj;
-        qv[k] = e;
-        sum += e;
+        if (x0 + k == t) qv[k] = adj;
+        sum += qv[k];
     }
     const uint64_t lincl = wave_inclusive_scan(sum) + base_sum;
     const uint64_t lexcl = lincl - sum;
@@ -236,8 +356,10 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
     __shared__ int sh_ok, sh_r;
     __shared__ float sh_m, sh_L, sh_q, sh_P;
     __shared__ int sh_next;  // 1: accepted, go to the next row
-    __shared__ uint64_t sh_Z, sh_adj;
-    __shared__ int sh_t;
+    __shared__ uint64_t sh_before, sh_adj;
+    __shared__ int sh_t, sh_x;
+    __shared__ int sh_ctr;  // the row pass's chunk counter
+    __shared__ uint64_t sh_tab[kTabSlots];  // the row's weight table
 
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
@@ -245,8 +367,16 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
     const float cb = it * kLog2e;  // the stream's base-2 scale
     const int v = a.v_t, nc = p.nc;
     const bool vec = p.vec != 0;
-    if (wave == 0) {
-        bool ok = M >= 0 && M <= a.max_m && it > 0.0f;
+    TT_STAMP(0);
+    if (!(M >= 0 && M <= a.max_m && it > 0.0f)) {
+        if (tid == 0) {
+            a.n_accepted[b] = -1;
+            a.out_token[b] = -1;
+        }
+        return;
+    }
+    if (wave == kWaves - 1) {  // every proposal's id inside the vocabulary (beside wave 0's scan)
+        bool ok = true;
         for (int base = 0; ok && base < M; base += kWave) {
             const int j = base + lane;
             const bool bad = j < M && (a.target_ids[t0 + j] < 0 || a.target_ids[t0 + j] >= v);
@@ -254,80 +384,92 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         }
         if (lane == 0) sh_ok = ok ? 1 : 0;
     }
-    __syncthreads();
-    if (!sh_ok) {
-        if (tid == 0) {
-            a.n_accepted[b] = -1;
-            a.out_token[b] = -1;
-        }
-        return;
-    }
     if (a.lse != nullptr) {
         // normalisers given: the acceptance test from one gathered logit per position, then
         // one pass over the residual (or bonus) row
-        // (the rejecting lane's L, t, q and P, or the bonus row's L, go to LDS with gamma, so
-        // the row pass and the residual entry need no further dependent load)
+        // (the rejecting lane's L, t, q, P and logit, or the bonus row's L, go to LDS with
+        // gamma, so the row pass and the residual entry need no further dependent load; an id
+        // outside the vocabulary is not gathered, and the stream then ends as a sentinel)
         if (wave == 0) {
             const float L_bonus = a.lse[t0 + b + M];
-            int gamma = M, t_r = -1;
+            int gamma = M, t_r = -1, x_r = 0;
             float L_r = L_bonus, q_r = 0.0f, P_r = 0.0f;
             for (int base = 0; base < M && gamma == M; base += kWave) {
                 const int j = base + lane;
                 bool rej = false;
-                int tj = 0;
+                int tj = 0, xj = 0;
                 float Lj = 0.0f, qj = 0.0f, P = 0.0f;
                 if (j < M) {
                     const int64_t r = t0 + b + j;
                     tj = a.target_ids[t0 + j];
                     Lj = a.lse[r];
-                    P = fminf(fmaxf(weight_at(expo(a.logits[r * a.ld + tj], cb, 31.0f - Lj * kLog2e)), 0.0f), 1.0f);
                     qj = a.q[t0 + j];
-                    rej = !(qj <= 0.0f || a.u_accept[t0 + j] < P / qj);
+                    if (tj >= 0 && tj < v) {
+                        xj = a.logits[r * a.ld + tj];
+                        P = fminf(fmaxf(weight_at(expo(xj, cb, 31.0f - Lj * kLog2e)), 0.0f), 1.0f);
+                        rej = !(qj <= 0.0f || a.u_accept[t0 + j] < P / qj);
+                    }
                 }
                 const unsigned long long rm = __ballot(rej);
                 if (rm != 0ull) {
                     const int src = __ffsll(rm) - 1;
                     gamma = base + src;
                     t_r = __builtin_amdgcn_readlane(tj, src);
+                    x_r = __builtin_amdgcn_readlane(xj, src);
                     L_r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(Lj), src));
                     q_r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(qj), src));
                     P_r = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(P), src));
                 }
             }
             if (lane == 0) {
+                sh_ctr = kWaves;
                 sh_r = gamma;
                 sh_t = t_r;
+                sh_x = x_r;
                 sh_L = L_r;
                 sh_q = q_r;
                 sh_P = P_r;
             }
         }
         __syncthreads();
+        TT_STAMP(1);
+        if (!sh_ok) {
+            if (tid == 0) {
+                a.n_accepted[b] = -1;
+                a.out_token[b] = -1;
+            }
+            return;
+        }
         const int r = sh_r;
         const int64_t rr = t0 + b + r;
         const uint16_t *row = a.logits + rr * a.ld;
         const float L = sh_L;
         const float b31 = 31.0f - L * kLog2e;
-        chunk_sums(row, v, nc, vec, cb, b31, sh_part);
+        chunk_sums(row, v, nc, vec, cb, b31, sh_tab, sh_part, &sh_ctr);
+        if (wave < 12) TT_STAMP_WAVE(4 + wave);
         __syncthreads();
+        TT_STAMP(2);
         if (wave != 0) return;
-        uint64_t local = 0;
-        for (int c = lane; c < nc; c += kWave) local += sh_part[c];
-        uint64_t Z = lane_value(wave_inclusive_scan(local), kWave - 1);
         int t = -1;
-        uint64_t adj = 0;
-        if (r < M) {  // the rejected proposal loses q_r of its mass
+        uint64_t adj = 0, before = 0;
+        if (r < M) {  // the rejected proposal loses q_r of its mass: its entry is E(t) - q_r, clamped
             t = sh_t;
-            const float Pt = sh_P;  // E(t) held in [0, 1]: floor(Pt * 2^31) is the e31 the chunk sums count
-            adj = q31(fminf(fmaxf(Pt - sh_q, 0.0f), 1.0f));
-            const uint64_t before = q31(Pt);
-            Z = Z - before + adj;
-            if (lane == 0) sh_part[t / kChunk] = sh_part[t / kChunk] - before + adj;
+            adj = q31(fminf(fmaxf(sh_P - sh_q, 0.0f), 1.0f));
+            before = e31_at(expo((uint32_t)sh_x, cb, b31));  // the weight the chunk sums counted at t
         }
-        const int token = sample_row(row, v, nc, vec, cb, b31, t, adj, Z, a.u_sample[b], sh_part);
+        const int token = sample_row(row, v, nc, vec, cb, b31, sh_tab, t, adj, before, a.u_sample[b], sh_part);
         if (lane == 0) {
             a.n_accepted[b] = r;
             a.out_token[b] = token;
+        }
+        TT_STAMP(3);
+        return;
+    }
+    __syncthreads();
+    if (!sh_ok) {
+        if (tid == 0) {
+            a.n_accepted[b] = -1;
+            a.out_token[b] = -1;
         }
         return;
     }
@@ -358,12 +500,13 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
             float mm = -INFINITY;
             for (int k = 0; k < kWaves; ++k) mm = fmaxf(mm, sh_red[k]);
             sh_m = mm;
+            sh_ctr = kWaves;
         }
         __syncthreads();
         m = sh_m;
         // pass 2: chunk sums of e31
         const float b31 = 31.0f - m;
-        chunk_sums(row, v, nc, vec, cb, b31, sh_part);
+        chunk_sums(row, v, nc, vec, cb, b31, sh_tab, sh_part, &sh_ctr);
         __syncthreads();
         // S, the acceptance test of position j, and the residual's entry at t_j
         if (wave == 0) {
@@ -373,7 +516,7 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
             if (lane == 0) {
                 const float S = q31_to_f32(Sq);
                 int next = 0;
-                uint64_t Z = Sq, adj = 0;
+                uint64_t before = 0, adj = 0;
                 int t = -1;
                 if (j < M) {
                     t = a.target_ids[t0 + j];
@@ -384,14 +527,12 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
                         next = 1;
                     } else {
                         const float rt = fminf(fmaxf(et - qj * S, 0.0f), 1.0f);  // NaN -> 0
-                        const uint64_t before = e31_at(expo(row[t], cb, b31));
+                        before = e31_at(expo(row[t], cb, b31));
                         adj = q31(rt);
-                        Z = Sq - before + adj;
-                        sh_part[t / kChunk] = sh_part[t / kChunk] - before + adj;
                     }
                 }
                 sh_next = next;
-                sh_Z = Z;
+                sh_before = before;
                 sh_t = next ? -1 : t;
                 sh_adj = adj;
             }
@@ -399,7 +540,7 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         __syncthreads();
         if (sh_next) continue;
         if (wave == 0) {
-            const int token = sample_row(row, v, nc, vec, cb, b31, sh_t, sh_adj, sh_Z, a.u_sample[b], sh_part);
+            const int token = sample_row(row, v, nc, vec, cb, b31, sh_tab, sh_t, sh_adj, sh_before, a.u_sample[b], sh_part);
             if (lane == 0) {
                 a.n_accepted[b] = j;
                 a.out_token[b] = token;
@@ -417,7 +558,12 @@ int launch_verify_logits(const LogitsArgs &a, hipStream_t stream) {
     p.a = a;
     p.nc = (a.v_t + kChunk - 1) / kChunk;
     p.vec = ((reinterpret_cast<uintptr_t>(a.logits) & 15u) == 0 && (a.ld % 8) == 0) ? 1 : 0;
-    hipLaunchKernelGGL(verify_logits_row, dim3(a.n_streams), dim3(kThreads), 8 * (size_t)p.nc, stream, p);
+    // the chunk sums (up to 64 KiB at the longest rows) sit beside the 64 KiB weight table in LDS
+    const size_t lds = 8 * (size_t)p.nc;
+    if (hipFuncSetAttribute(reinterpret_cast<const void *>(&verify_logits_row),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+        return TT_ELAUNCH;
+    hipLaunchKernelGGL(verify_logits_row, dim3(a.n_streams), dim3(kThreads), lds, stream, p);
     return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
 }
 

@@ -76,9 +76,9 @@ def test_logits_parity_with_lse(n, V, ld, shift):
 
 @pytest.mark.parametrize("shift", [-100.0, -3e9])
 def test_logits_lse_far_below_the_logits(shift):
-    """A caller's log-sum-exp far below the row's logits: x - L runs past 88 (up to about 3e9,
-    where converting k to an int would overflow without the clamp at 88); every P clamps to 1
-    and each e39 saturates, on both sides alike."""
+    """A caller's log-sum-exp far below the row's logits: the scaled exponent z runs past 31 (up
+    to about 4e9, where converting k to an int would overflow without the clamp at 31); every P
+    clamps to 1 and each Q31 weight saturates at 2^31, on both sides alike."""
     print(f"[case] logits+lse shift={shift}", flush=True)
     case = logits_case(37, 1000, None, seed=4)
     nacc, Ms = run_both(V=1000, case=case, max_m=8, lse=case_lse(1000, case, shift))
@@ -87,8 +87,8 @@ def test_logits_lse_far_below_the_logits(shift):
 
 @pytest.mark.parametrize("with_lse", [False, True])
 def test_logits_wide_range(with_lse):
-    """Logits spread over [-130, 5]: every x - m in the exponential's cut-off band [-100, -87),
-    below it, and near 0, so each e39 on both sides of the cut-off is compared."""
+    """Logits spread over [-130, 5]: scaled exponents far below the clamp at -1, at it, and up
+    to 31, so Q31 weights from 0 to 2^31 are compared."""
     print(f"[case] logits wide range lse={with_lse}", flush=True)
     V = 3000
     ids, off, q, bits, it, ua, us, Ms = logits_case(40, V, seed=11, max_m=4)
@@ -124,3 +124,73 @@ def test_logits_at_the_benchmark_width():
     case = logits_case(256, V, seed=9, max_m=3)
     run_both(V, case, 3)
     run_both(V, case, 3, lse=case_lse(V, case))
+
+
+@pytest.mark.parametrize("with_lse", [False, True])
+def test_logits_every_bf16_pattern(with_lse):
+    """Rows that are permutations of bf16 bit patterns, so every slot of the kernel's per-row
+    weight table and every pattern outside its domain (magnitudes below 2^-20 or from 256 up,
+    infinities, NaNs) meets the formula the oracle evaluates.  With a log-sum-exp: all 65,536
+    patterns, normalisers that put the clamp at 31 inside the finite range.  Without: every
+    pattern below 8 in magnitude, so the row's largest logit is finite and every value down to
+    the subnormals carries weight."""
+    print(f"[case] logits every bf16 pattern lse={with_lse}", flush=True)
+    rng = np.random.default_rng(77)
+    pats = np.arange(1 << 16, dtype=np.uint32)
+    if not with_lse:
+        mag = pats & 0x7FFF
+        pats = pats[mag < 0x4100]
+    V = len(pats)
+    n = 12
+    Ms = rng.integers(0, 3, n)
+    off = np.zeros(n + 1, np.int32)
+    off[1:] = np.cumsum(Ms)
+    nt = int(off[-1])
+    bits = np.stack([rng.permutation(pats) for _ in range(nt + n)]).astype(np.uint16)
+    ids = rng.integers(0, V, nt).astype(np.int32)
+    q = (rng.random(nt) * 0.5 + 0.05).astype(np.float32)
+    it = (1.0 / rng.uniform(0.5, 1.5, n)).astype(np.float32)
+    ua = (rng.integers(0, 1 << 24, nt) * 2.0 ** -24).astype(np.float32)
+    us = (rng.integers(0, 1 << 24, n) * 2.0 ** -24).astype(np.float32)
+    case = (ids, off, q, bits, it, ua, us, Ms)
+    lse = None
+    if with_lse:
+        lse = rng.uniform(-5.0, 60.0, nt + n).astype(np.float32)
+    run_both(V, case, 2, lse=lse)
+
+
+def test_logits_lse_residual_at_a_scaled_exponent_just_below_zero():
+    """A rejected proposal whose scaled exponent z lies in (-2^-25, 0): its probability E is 0
+    (z < 0) while its Q31 weight floor(2^z) is 1 (the polynomial rounds to 1.0).  The residual's
+    mass must drop the weight the row's sums counted (1), not the probability's 0: the row is
+    ten unit weights and that entry, so the sampled unit is the (floor(10 u) + 1)-th; counting
+    the entry's old weight would move the threshold past every entry."""
+    print("[case] logits+lse residual at z just below 0", flush=True)
+    V = 64
+    it = np.float32(1.0 / 0.7)
+    x_t = np.float32(1.265625)      # fma(x_t, c, 31 - L log2 e) = -2^-28 for this L
+    L = np.float32(23.295599)
+    y_unit = np.float32(x_t + 0.25)  # z about 0.5: weight 1
+    z_t = np.float32(float(x_t) * float(np.float32(it * np.float32(1.4426950408889634))) +
+                     float(np.float32(31.0) - np.float32(L * np.float32(1.4426950408889634))))
+    assert -2.0 ** -25 < z_t < 0 and oracle.exp2(z_t) == 1.0 and oracle.logit_prob(x_t, it, L) == 0.0
+    n = 4
+    Ms = np.ones(n, np.int64)
+    off = np.arange(n + 1, dtype=np.int32)
+    rows = np.full((2 * n, V), -100.0, np.float32)
+    ids = np.full(n, 5, np.int32)
+    for b in range(n):
+        r = b + b  # row of position 0 is off[b] + b
+        rows[r, 5] = x_t
+        rows[r, 20:30] = y_unit
+        rows[r + 1, :] = 0.0
+    bits = bf16_bits(rows)
+    q = np.full(n, 0.5, np.float32)
+    ua = np.full(n, 0.99, np.float32)
+    us = np.float32([0.95, 0.05, 0.5, 0.999])
+    lse = np.full(2 * n, L, np.float32)
+    case = (ids, off, q, bits, np.full(n, it, np.float32), ua, us, Ms)
+    o_nacc, _ = run_both(V, case, 1, lse=lse)
+    assert np.array_equal(o_nacc, np.zeros(n))
+    _, tok, z = oracle.verify_logits(V, ids, off, q, bits, np.full(n, it, np.float32), ua, us, max_m=1, lse=lse)
+    assert np.array_equal(z, np.full(n, 10)) and np.array_equal(tok, 20 + np.floor(us.astype(np.float64) * 10))
