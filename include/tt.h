@@ -253,21 +253,24 @@ int tt_verify_dense(int32_t n_streams, int32_t v,
  * target_logits: bf16 bit patterns, row target_off[b] + b + j (j in [0, M_b]) at a stride
  * of target_ld elements; inv_temperature[n_streams] fp32 (1 / T, > 0).  max_m as for
  * tt_verify.  Outputs (device): n_accepted, out_token as for tt_verify (no residual rows).
- * Arithmetic, all of it order-independent: x = logit * inv_temperature (NaN counts as
- * minus infinity), m = the row's largest x, e = exp(x - m) by a specified software
- * exponential (Cody-Waite reduction, degree-6 Taylor polynomial with fused multiply-adds,
- * 0 below -87), e39 = floor(e * 2^39) summed exactly, S = that sum * 2^-39 rounded once
- * to fp32, P_t(t_j) = e(t_j) / S in fp32; accept while q_j <= 0 or u_j < P_t(t_j) / q_j;
- * after a rejection at r the residual is the row's e39 with the entry at t_r replaced by
- * floor(clamp(e(t_r) - q_r * S, 0, 1) * 2^39), after full acceptance the bonus row's e39;
- * the token is the first index whose prefix exceeds floor(u_sample * Z) (the first
- * largest x when Z = 0).  A stream with M_b outside [0, max_m], an id outside [0, v_t)
- * or inv_temperature <= 0 gets n_accepted = out_token = -1.
- * lse (device, optional, one fp32 per logits row): the row's log-sum-exp of x, as an LM
- * head can emit it with its logits.  When given, m = lse and S = 1 (P = clamp(e, 0, 1),
- * the residual entry at t_r is floor(clamp(P(t_r) - q_r, 0, 1) * 2^39)): the acceptance
- * test reads one logit per position and only the residual (or bonus) row is read, once.
- * Without it each stream reads its rows 0 .. gamma twice (max, then sums), one after another.
+ * Arithmetic, all of it order-independent, in base 2: c = inv_temperature * log2(e) (fp32);
+ * y = logit * c (NaN counts as minus infinity); mu = the row's largest y; the scaled exponent
+ * z = fma(logit, c, fp32(31 - mu)) held in [-1, 31]; 2^z = p * 2^k with k = rint(z) and p the
+ * degree-5 Taylor polynomial of 2^(z - k) (coefficients (ln 2)^n / n! in fp32, Horner with
+ * fused multiply-adds); the weight e31 = floor(p * 2^k) (Q31), summed exactly;
+ * S = that sum * 2^-31 rounded once to fp32; E = p * 2^(k - 31) (0 for z < 0);
+ * P_t(t_j) = E(t_j) / S in fp32; accept while q_j <= 0 or u_j < P_t(t_j) / q_j; after a
+ * rejection at r the residual is the row's e31 with the entry at t_r replaced by
+ * floor(clamp(E(t_r) - q_r * S, 0, 1) * 2^31), after full acceptance the bonus row's e31;
+ * the token is the first index whose prefix exceeds floor(u_sample * Z) (the first largest
+ * y when Z = 0).  A stream with M_b outside [0, max_m], an id outside [0, v_t) or
+ * inv_temperature <= 0 gets n_accepted = out_token = -1.
+ * lse (device, optional, one fp32 per logits row): the row's log-sum-exp of logit *
+ * inv_temperature, as an LM head can emit it with its logits.  When given, mu = lse * log2(e)
+ * and S = 1 (P = clamp(E, 0, 1), the residual entry at t_r is floor(clamp(P(t_r) - q_r, 0, 1)
+ * * 2^31)): the acceptance test reads one logit per position and only the residual (or bonus)
+ * row is read, once.  Without it each stream reads its rows 0 .. gamma twice (max, then
+ * sums), one after another.
  * One kernel on `stream`, a workgroup per stream; no workspace.
  * TT_EINVAL on a bad size or a missing pointer, TT_EUNSUPPORTED for v_t > 2^23.
  */
@@ -399,6 +402,34 @@ int tt_vocab_intersection(const tt_vocab *vd, const void *vd_index, size_t vd_in
  */
 int tt_tli_proposal(int32_t n_rows, int32_t v_d, int32_t v_t, const int32_t *d2t, const int32_t *t2d,
                     const float *draft_probs, int64_t draft_ld, float *q_out, int64_t q_ld, void *stream);
+
+/*
+ * tt_verify_tli -- standard speculative sampling with the Token-Level Intersection
+ * proposal (App. D Alg. 3 feeding Alg. 4) in one call, the proposal rows formed where they
+ * are used instead of written: the result is that of tt_tli_proposal on the drafted
+ * positions' rows followed by tt_verify_dense on its output, bit for bit.
+ *
+ * Inputs (device): d2t[v_d], t2d[v_t] from tt_vocab_intersection; target_ids / target_off
+ * CSR proposals y_j (target ids, drawn from q'_j) as for tt_verify_dense; draft_probs: row
+ * target_off[b] + j (stride draft_ld >= v_d floats) is the draft distribution q_j over
+ * V_d; draft_mass (optional, may be NULL): one fp32 per draft row, S_j, the mass q_j puts
+ * on the intersection as the drafter formed it when it normalised q'_j -- when NULL, S_j
+ * is formed exactly as tt_tli_proposal forms it; target_probs: stream b owns the M_b + 1
+ * rows from row target_off[b] + b (stride target_ld >= v_t); u_accept, u_sample, max_m as
+ * for tt_verify_dense.
+ * Proposal: q'_j(y) = clamp(q_j(t2d[y]), 0, 1) / S_j when t2d[y] lies in [0, v_d) and S_j > 0,
+ * else 0.  Outputs (device): n_accepted, out_token as tt_verify_dense gives them for the
+ * rows q'_j (a stream with M_b outside [0, max_m] or an id outside [0, v_t) gets -1, -1).
+ * Reads: one gathered draft mass per tested position (with draft_mass; without it, draft
+ * row j in full for every tested position, one after another), then target row gamma and,
+ * after a rejection, the masses of draft row gamma gathered through t2d.  One kernel on
+ * `stream`, a workgroup per stream, no workspace.  TT_EINVAL on a bad size or a missing
+ * pointer, TT_EUNSUPPORTED for v_t > 2^21.
+ */
+int tt_verify_tli(int32_t n_streams, int32_t v_d, int32_t v_t, const int32_t *d2t, const int32_t *t2d,
+                  const int32_t *target_ids, const int32_t *target_off, const float *draft_probs, int64_t draft_ld,
+                  const float *draft_mass, const float *target_probs, int64_t target_ld, const float *u_accept,
+                  const float *u_sample, int32_t max_m, int32_t *n_accepted, int32_t *out_token, void *stream);
 
 /*
  * Workspace bytes tt_step needs: the larger of tt_align_workspace_size and

@@ -344,12 +344,14 @@ def round_to_f32(num: int, scale_bits: int) -> np.float32:
     return np.float32(np.ldexp(float(mant), shift - scale_bits))
 
 
-def tli_proposal(d2t, t2d, draft_probs):
+def tli_proposal(d2t, t2d, draft_probs, mass=None):
     """App. D Alg. 3 (TLI): q' over the target vocabulary from draft rows q over V_d,
     q'(y) = q(x) / S for y = d2t[x] in the intersection and 0 elsewhere, S the mass q puts on
     the intersection.  Readings: q is clamped to [0, 1] (NaN -> 0); S is the sum of the
     intersected masses, each truncated to a multiple of 2^-62 and summed exactly, then rounded
     once to the nearest fp32; q'(y) is the fp32 quotient; a row with S = 0 gives a zero row.
+    mass (optional, one fp32 per row): S as the drafter formed it when it normalised q', used
+    instead of the sum; a row whose S is not positive (or NaN) is a zero row.
 
     Rows of draft_probs are [n, V_d] float32; returns [n, V_t] float32."""
     q = np.asarray(draft_probs, np.float32)
@@ -362,9 +364,12 @@ def tli_proposal(d2t, t2d, draft_probs):
         qc = np.nan_to_num(q[r], nan=0.0)
         qc = np.minimum(np.maximum(qc, np.float32(0.0)), np.float32(1.0)).astype(np.float32)
         # floor(q * 2^62) is an exact integer below 2^63 (q has a 24-bit significand)
-        fixed = np.floor(qc[inter].astype(np.float64) * 2.0 ** 62)
-        S = round_to_f32(sum(int(v) for v in fixed), 62)
-        if S == 0:
+        if mass is None:
+            fixed = np.floor(qc[inter].astype(np.float64) * 2.0 ** 62)
+            S = round_to_f32(sum(int(v) for v in fixed), 62)
+        else:
+            S = np.float32(mass[r])
+        if not S > 0:
             continue
         out[r, d2t[inter]] = qc[inter] / S  # fp32 quotients
     return out

@@ -14,6 +14,10 @@ raised.
     delta_quantile / w_at_quantile  tt_delta_quantile  where that distribution reaches 0.9 (App. K)
     token_index / retokenize  tt_token_index_build / tt_retokenize  draft tokens -> proxy target
               tokens by greedy longest match (Sec. 4.2.1, Alg. 2, App. A.1)
+    vocab_intersection / tli_proposal / verify_tli  the Token-Level Intersection proposal
+              (App. D Alg. 3): the intersection maps, q' rows, and the verification with q'
+              formed on the fly
+    verify_logits  tt_verify_logits  verification from bf16 logits and a temperature (App. F)
 """
 from __future__ import annotations
 
@@ -22,6 +26,7 @@ import os
 
 __all__ = ["Vocab", "align", "align_workspace", "transfer", "verify", "verify_noalloc", "verify_dense", "verify_workspace", "lib",
            "delta_histogram", "delta_quantile", "w_at_quantile", "token_index", "retokenize", "LIB_PATH",
+           "vocab_intersection", "tli_proposal", "verify_tli", "verify_logits",
            "TTError", "path_capacity"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtt.so")
@@ -89,6 +94,8 @@ def lib():
         L.tt_vocab_intersection.restype = ctypes.c_int
         L.tt_tli_proposal.argtypes = [i32, i32, i32, P, P, P, i64, P, i64, P]
         L.tt_tli_proposal.restype = ctypes.c_int
+        L.tt_verify_tli.argtypes = [i32, i32, i32, P, P, P, P, P, i64, P, P, i64, P, P, i32, P, P, P]
+        L.tt_verify_tli.restype = ctypes.c_int
         L.tt_step_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, ctypes.POINTER(sz)]
         L.tt_step_workspace_size.restype = ctypes.c_int
         L.tt_step.argtypes = [VP, VP, i32, i32, i32, P, P, P, P, i32, i32, i32, P, i64, P, i64, P, P,
@@ -438,6 +445,36 @@ def tli_proposal(d2t, t2d, draft_probs, v_d: int | None = None, out=None, stream
                                ctypes.c_void_p(draft_probs.data_ptr()), int(draft_probs.stride(0)),
                                ctypes.c_void_p(out.data_ptr()), int(out.stride(0)), _stream_handle(stream))
     _check(st, "tt_tli_proposal")
+    return out
+
+
+def verify_tli(d2t, t2d, target_ids, target_off, draft_probs, target_probs, u_accept, u_sample, max_m: int,
+               draft_mass=None, v_d: int | None = None, out=None, stream=None):
+    """tt_verify_tli: standard speculative sampling with the TLI proposal formed on the fly from
+    draft rows [sum M, >= V_d] float32 (row target_off[b] + j for position j) against target rows
+    [rows, >= V_t]; draft_mass optional float32 [sum M], the drafter's S_j.  Returns
+    (n_accepted, out_token)."""
+    torch = _torch()
+    i32, f32 = torch.int32, torch.float32
+    v_d = int(d2t.numel()) if v_d is None else int(v_d)
+    v_t = int(t2d.numel())
+    n = int(target_off.numel()) - 1
+    dev = target_off.device
+    for name, t in (("draft_probs", draft_probs), ("target_probs", target_probs)):
+        if t.dim() != 2 or t.stride(1) != 1 or t.dtype != f32 or not t.is_cuda:
+            raise ValueError(f"{name} must be a 2-D row-major float32 device tensor")
+    if out is None:
+        out = (torch.empty(n, dtype=i32, device=dev), torch.empty(n, dtype=i32, device=dev))
+    nacc, tok = out
+    ids = target_ids if target_ids.numel() else torch.zeros(1, dtype=i32, device=dev)
+    ua = u_accept if u_accept.numel() else torch.zeros(1, dtype=f32, device=dev)
+    st = lib().tt_verify_tli(n, v_d, v_t, _ptr(d2t, i32, "d2t"), _ptr(t2d, i32, "t2d"), _ptr(ids, i32, "target_ids"),
+                             _ptr(target_off, i32, "target_off"), ctypes.c_void_p(draft_probs.data_ptr()),
+                             int(draft_probs.stride(0)), _ptr(draft_mass, f32, "draft_mass", allow_none=True),
+                             ctypes.c_void_p(target_probs.data_ptr()), int(target_probs.stride(0)),
+                             _ptr(ua, f32, "u_accept"), _ptr(u_sample, f32, "u_sample"), int(max_m),
+                             _ptr(nacc, i32, "n_accepted"), _ptr(tok, i32, "out_token"), _stream_handle(stream))
+    _check(st, "tt_verify_tli")
     return out
 
 

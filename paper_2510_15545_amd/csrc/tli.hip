@@ -63,15 +63,11 @@ __device__ inline float q62_to_f32(U128 n) {
     return ldexpf((float)m, sh - 62);
 }
 
-__global__ void __launch_bounds__(kThreads) tli_rows(TliArgs a, int vec_in, int vec_out) {
-    const int r = blockIdx.x;
+// S, the mass row q puts on the intersection: every intersected q(x) (clamped to [0, 1])
+// truncated to Q62 and the integers summed exactly, rounded once to fp32.  Called by every
+// thread of the workgroup (barriers inside); sh_part holds a partial sum per wave.
+__device__ float row_mass(const float *q, const int32_t *d2t, int v_d, bool vec_in, U128 *sh_part, float *sh_S) {
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
-    const float *q = a.draft_probs + (int64_t)r * a.draft_ld;
-    float *out = a.q_out + (int64_t)r * a.q_ld;
-    __shared__ U128 sh_part[kThreads / kWave];
-    __shared__ float sh_S;
-
-    // 1. exact Q62 sum of the intersected mass
     U128 acc{0, 0};
     auto add = [&](float x, int32_t m) {  // branch-free: the loads stay batched
         const uint64_t keep = 0ull - (uint64_t)(m >= 0);
@@ -80,8 +76,8 @@ __global__ void __launch_bounds__(kThreads) tli_rows(TliArgs a, int vec_in, int 
     int x0 = 0;
     if (vec_in) {
         const float4 *q4 = reinterpret_cast<const float4 *>(q);
-        const int4 *m4 = reinterpret_cast<const int4 *>(a.d2t);
-        const int n4 = a.v_d / 4;
+        const int4 *m4 = reinterpret_cast<const int4 *>(d2t);
+        const int n4 = v_d / 4;
         int k = tid;
         for (; k + (kUnroll - 1) * kThreads < n4; k += kUnroll * kThreads) {  // kUnroll loads of each in flight
             float4 v[kUnroll];
@@ -109,17 +105,33 @@ __global__ void __launch_bounds__(kThreads) tli_rows(TliArgs a, int vec_in, int 
         }
         x0 = 4 * n4;
     }
-    for (int x = x0 + tid; x < a.v_d; x += kThreads) add(q[x], a.d2t[x]);
+    for (int x = x0 + tid; x < v_d; x += kThreads) add(q[x], d2t[x]);
     for (int m = kWave / 2; m > 0; m >>= 1) acc = add128(acc, shfl_xor128(acc, m));
     if (lane == 0) sh_part[wave] = acc;
     __syncthreads();
     if (tid == 0) {
         U128 tot{0, 0};
         for (int w = 0; w < kThreads / kWave; ++w) tot = add128(tot, sh_part[w]);
-        sh_S = q62_to_f32(tot);
+        *sh_S = q62_to_f32(tot);
     }
     __syncthreads();
-    const float S = sh_S;
+    return *sh_S;
+}
+
+// q'(y) for the draft id x = t2d[y] whose mass g = q(x) was gathered (g = 0 when x lies
+// outside [0, v_d): the entry is 0 either way); 0 when S is not positive.
+__device__ __forceinline__ float qprime(float g, float S) { return S > 0.0f ? clamp01(g) / S : 0.0f; }
+
+__global__ void __launch_bounds__(kThreads) tli_rows(TliArgs a, int vec_in, int vec_out) {
+    const int r = blockIdx.x;
+    const int tid = threadIdx.x;
+    const float *q = a.draft_probs + (int64_t)r * a.draft_ld;
+    float *out = a.q_out + (int64_t)r * a.q_ld;
+    __shared__ U128 sh_part[kThreads / kWave];
+    __shared__ float sh_S;
+
+    // 1. exact Q62 sum of the intersected mass
+    const float S = row_mass(q, a.d2t, a.v_d, vec_in != 0, sh_part, &sh_S);
 
     // 2. q' over the target vocabulary
     // every lane loads (q[0] outside the intersection) so the gathers of a batch stay in flight together
@@ -159,6 +171,213 @@ __global__ void __launch_bounds__(kThreads) tli_rows(TliArgs a, int vec_in, int 
     }
 }
 
+// ------------------------------------------------------------------ fused verification
+// Standard speculative sampling (App. D Alg. 4) with the TLI proposal of each drafted
+// position formed where it is used, so q' rows are never written: one 1024-thread workgroup
+// per stream.
+//   acceptance: q'_j(t_j) = q_j(t2d[t_j]) / S_j, one gathered draft mass per position; S_j
+//     from draft_mass (wave 0 tests 64 positions per ballot) or, without it, by a pass over
+//     draft row j (the whole workgroup, row after row until the first rejection);
+//   residual: the chunk sums of max(0, p - q') over target row gamma, q' gathered through t2d
+//     from draft row gamma (the bonus row as is after full acceptance), then the exact
+//     inverse-CDF sample by wave 0 -- the arithmetic of tt_verify_dense element for element.
+constexpr int kWaves = kThreads / kWave;
+
+struct TliVerifyParams {
+    TliVerifyArgs a;
+    int32_t nc, vec_t, vec_d;
+};
+
+// 16 target probabilities of a lane (elements x0 .. x0+15 with x0 = c*1024 + lane*16) and the
+// q' values at them (0 past v_t); q' from draft row drow with mass S, or 0 when drow is null.
+__device__ __forceinline__ void lane_pq(const TliVerifyArgs &a, const float *prow, const float *drow, float S,
+                                        int x0, bool vec, float (&pv)[16], float (&dv)[16]) {
+    vcore::read16(prow, x0, a.v_t, vec, pv);
+    if (drow == nullptr) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) dv[k] = 0.0f;
+        return;
+    }
+    int32_t xs[16];
+    if (vec && x0 + 16 <= a.v_t) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int4 t = *reinterpret_cast<const int4 *>(a.t2d + x0 + 4 * q);
+            xs[4 * q] = t.x;
+            xs[4 * q + 1] = t.y;
+            xs[4 * q + 2] = t.z;
+            xs[4 * q + 3] = t.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) xs[k] = x0 + k < a.v_t ? a.t2d[x0 + k] : -1;
+    }
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const float g = (xs[k] >= 0 && xs[k] < a.v_d) ? drow[xs[k]] : 0.0f;
+        dv[k] = qprime(g, S);
+    }
+}
+
+__global__ void __launch_bounds__(kThreads) verify_tli_row(TliVerifyParams p) {
+    const TliVerifyArgs &a = p.a;
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    extern __shared__ uint64_t sh_part[];  // nc chunk sums (Q62)
+    __shared__ U128 sh_red[kWaves];
+    __shared__ float sh_S, sh_Sr;
+    __shared__ int sh_ok, sh_gamma, sh_ctr, sh_rej;
+
+    const int t0 = a.target_off[b];
+    const int M = a.target_off[b + 1] - t0;
+    if (!(M >= 0 && M <= a.max_m)) {
+        if (tid == 0) {
+            a.n_accepted[b] = -1;
+            a.out_token[b] = -1;
+        }
+        return;
+    }
+    if (wave == kWaves - 1) {  // every proposal's id inside the target vocabulary
+        bool ok = true;
+        for (int base = 0; ok && base < M; base += kWave) {
+            const int j = base + lane;
+            ok = !__any(j < M && (a.target_ids[t0 + j] < 0 || a.target_ids[t0 + j] >= a.v_t));
+        }
+        if (lane == 0) {
+            sh_ok = ok ? 1 : 0;
+            sh_ctr = kWaves;
+        }
+    }
+    int gamma = M;
+    float S_r = 0.0f;
+    if (a.draft_mass != nullptr) {
+        if (wave == 0) {
+            for (int base = 0; base < M && gamma == M; base += kWave) {
+                const int j = base + lane;
+                bool rej = false;
+                float Sj = 0.0f;
+                if (j < M) {
+                    const int tok = a.target_ids[t0 + j];
+                    const float uj = a.u_accept[t0 + j];
+                    Sj = a.draft_mass[t0 + j];
+                    if (tok >= 0 && tok < a.v_t) {
+                        const float pt = a.target_probs[(int64_t)(t0 + b + j) * a.target_ld + tok];
+                        const int32_t x = a.t2d[tok];
+                        const float g = (x >= 0 && x < a.v_d) ? a.draft_probs[(int64_t)(t0 + j) * a.draft_ld + x] : 0.0f;
+                        const float qj = qprime(g, Sj);
+                        rej = !((qj <= 0.0f) || (uj < pt / qj));
+                    }
+                }
+                const unsigned long long rm = __ballot(rej);
+                if (rm != 0ull) {
+                    const int l = __ffsll(rm) - 1;
+                    gamma = base + l;
+                    S_r = __shfl(Sj, l);
+                }
+            }
+            if (lane == 0) {
+                sh_gamma = gamma;
+                sh_Sr = S_r;
+            }
+        }
+        __syncthreads();
+        if (!sh_ok) {
+            if (tid == 0) {
+                a.n_accepted[b] = -1;
+                a.out_token[b] = -1;
+            }
+            return;
+        }
+        gamma = sh_gamma;
+        S_r = sh_Sr;
+    } else {
+        __syncthreads();
+        if (!sh_ok) {
+            if (tid == 0) {
+                a.n_accepted[b] = -1;
+                a.out_token[b] = -1;
+            }
+            return;
+        }
+        for (int j = 0; j < M; ++j) {  // S_j of each tested row, formed as tt_tli_proposal forms it
+            const float *drow = a.draft_probs + (int64_t)(t0 + j) * a.draft_ld;
+            const float Sj = row_mass(drow, a.d2t, a.v_d, p.vec_d != 0, sh_red, &sh_S);
+            if (tid == 0) {
+                const int tok = a.target_ids[t0 + j];
+                const float pt = a.target_probs[(int64_t)(t0 + b + j) * a.target_ld + tok];
+                const int32_t x = a.t2d[tok];
+                const float g = (x >= 0 && x < a.v_d) ? drow[x] : 0.0f;
+                const float qj = qprime(g, Sj);
+                sh_rej = !((qj <= 0.0f) || (a.u_accept[t0 + j] < pt / qj)) ? 1 : 0;
+            }
+            __syncthreads();
+            if (sh_rej) {
+                gamma = j;
+                S_r = Sj;
+                break;
+            }
+        }
+    }
+    // residual (or bonus) row: Q62 chunk sums of max(0, p - q') into LDS
+    const bool vec = p.vec_t != 0;
+    const float *prow = a.target_probs + (int64_t)(t0 + b + gamma) * a.target_ld;
+    const float *drow = gamma < M ? a.draft_probs + (int64_t)(t0 + gamma) * a.draft_ld : nullptr;
+    const int nc = p.nc;
+    for (int c = wave;;) {
+        if (c >= nc) break;
+        float pv[16], dv[16];
+        lane_pq(a, prow, drow, S_r, c * vcore::kChunk + lane * 16, vec, pv, dv);
+        uint64_t acc = 0;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) acc += q62(clamp01(pv[k] - dv[k]));  // 0 past v_t: pv = dv = 0
+        acc = vcore::wave_inclusive_scan(acc);
+        if (lane == kWave - 1) sh_part[c] = acc;
+        c = vcore::next_chunk(&sh_ctr, c, kWaves);
+    }
+    __syncthreads();
+    if (wave != 0) return;
+    uint64_t Z, T, base;
+    int cs;
+    const int st = vcore::find_crossing(nc, [&](int c) { return sh_part[c]; }, a.u_sample[b], Z, T, cs, base);
+    int token;
+    if (st == 1) {
+        token = vcore::wave_first_argmax(prow, a.v_t);
+    } else if (st == 2) {
+        token = a.v_t - 1;
+    } else {
+        const int x0 = cs * vcore::kChunk + lane * 16;
+        float pv[16], dv[16];
+        lane_pq(a, prow, drow, S_r, x0, vec, pv, dv);
+        uint64_t qv[16], sum = 0;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            qv[k] = x0 + k < a.v_t ? q62(clamp01(pv[k] - dv[k])) : 0ull;
+            sum += qv[k];
+        }
+        const uint64_t lincl = vcore::wave_inclusive_scan(sum) + base;
+        const uint64_t lexcl = lincl - sum;
+        const unsigned long long lhit = __ballot(lexcl <= T && T < lincl);
+        if (lhit == 0ull) {
+            token = a.v_t - 1;
+        } else {
+            const int tl = __ffsll(lhit) - 1;
+            uint64_t run = lexcl;
+            int k_at = 0;
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                run += qv[k];
+                k_at += run <= T ? 1 : 0;
+            }
+            token = __builtin_amdgcn_readlane(x0 + k_at, tl);
+        }
+    }
+    if (lane == 0) {
+        a.n_accepted[b] = gamma;
+        a.out_token[b] = token;
+    }
+}
+
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 }  // namespace
@@ -168,6 +387,17 @@ int launch_tli_proposal(const TliArgs &a, hipStream_t stream) {
     const int vec_in = aligned16(a.draft_probs) && aligned16(a.d2t) && a.draft_ld % 4 == 0;
     const int vec_out = aligned16(a.q_out) && aligned16(a.t2d) && a.q_ld % 4 == 0;
     hipLaunchKernelGGL(tli_rows, dim3(a.n_rows), dim3(kThreads), 0, stream, a, vec_in, vec_out);
+    return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+}
+
+int launch_verify_tli(const TliVerifyArgs &a, hipStream_t stream) {
+    if (a.n_streams == 0) return TT_OK;
+    TliVerifyParams p;
+    p.a = a;
+    p.nc = (a.v_t + vcore::kChunk - 1) / vcore::kChunk;
+    p.vec_t = aligned16(a.target_probs) && aligned16(a.t2d) && a.target_ld % 4 == 0;
+    p.vec_d = aligned16(a.draft_probs) && aligned16(a.d2t) && a.draft_ld % 4 == 0;
+    hipLaunchKernelGGL(verify_tli_row, dim3(a.n_streams), dim3(kThreads), 8 * (size_t)p.nc, stream, p);
     return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
 }
 

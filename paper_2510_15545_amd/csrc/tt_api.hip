@@ -16,6 +16,7 @@ constexpr int32_t kMaxQuantileDen = 65536;  // denominator of tt_delta_quantile'
 constexpr int32_t kMaxIndexTokens = 1 << 28;  // vocabulary size a token index accepts
 constexpr int32_t kMaxTokenBytes = 64;        // longest target token the index and lookups handle
 constexpr int32_t kMaxLogitsRow = 1 << 23;     // logits per row tt_verify_logits accepts (64-bit exact sums)
+constexpr int32_t kMaxTliRow = 1 << 21;        // target row tt_verify_tli accepts (chunk sums in 16 KB of LDS)
 constexpr int32_t kMaxRetokBytes = 4096;      // bytes of S (and tokens of T) per stream: 14 B of LDS each
 
 bool vocab_ok(const tt_vocab *v) {
@@ -162,6 +163,39 @@ int tt_verify_dense(int32_t n_streams, int32_t v, const int32_t *draft_ids, cons
     a.q_rows = draft_probs;
     a.q_ld = draft_ld;
     return tt::launch_verify(a, static_cast<hipStream_t>(stream));
+}
+
+int tt_verify_tli(int32_t n_streams, int32_t v_d, int32_t v_t, const int32_t *d2t, const int32_t *t2d,
+                  const int32_t *target_ids, const int32_t *target_off, const float *draft_probs, int64_t draft_ld,
+                  const float *draft_mass, const float *target_probs, int64_t target_ld, const float *u_accept,
+                  const float *u_sample, int32_t max_m, int32_t *n_accepted, int32_t *out_token, void *stream) {
+    if (n_streams < 0 || v_d < 1 || v_t < 1 || draft_ld < v_d || target_ld < v_t || max_m < 0 ||
+        max_m > kMaxVerifyLen)
+        return TT_EINVAL;
+    if (v_t > kMaxTliRow) return TT_EUNSUPPORTED;
+    if (n_streams == 0) return TT_OK;
+    if (!d2t || !t2d || !target_ids || !target_off || !draft_probs || !target_probs || !u_accept || !u_sample ||
+        !n_accepted || !out_token)
+        return TT_EINVAL;
+    tt::TliVerifyArgs a;
+    a.n_streams = n_streams;
+    a.v_d = v_d;
+    a.v_t = v_t;
+    a.d2t = d2t;
+    a.t2d = t2d;
+    a.target_ids = target_ids;
+    a.target_off = target_off;
+    a.draft_probs = draft_probs;
+    a.draft_ld = draft_ld;
+    a.draft_mass = draft_mass;
+    a.target_probs = target_probs;
+    a.target_ld = target_ld;
+    a.u_accept = u_accept;
+    a.u_sample = u_sample;
+    a.max_m = max_m;
+    a.n_accepted = n_accepted;
+    a.out_token = out_token;
+    return tt::launch_verify_tli(a, static_cast<hipStream_t>(stream));
 }
 
 int tt_verify_logits(int32_t n_streams, int32_t v_t, const int32_t *target_ids, const int32_t *target_off,

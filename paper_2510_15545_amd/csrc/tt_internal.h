@@ -124,6 +124,22 @@ struct TliArgs {
     int64_t q_ld;
 };
 int launch_tli_proposal(const TliArgs &a, hipStream_t stream);
+// Verification with the TLI proposal formed on the fly (tt_verify_tli): the proposal of
+// position j is q' of draft row target_off[b] + j, with S from draft_mass when given.
+struct TliVerifyArgs {
+    int32_t n_streams, v_d, v_t;
+    const int32_t *d2t, *t2d;
+    const int32_t *target_ids, *target_off;
+    const float *draft_probs;
+    int64_t draft_ld;
+    const float *draft_mass;  // per draft row, or null: formed as tt_tli_proposal forms it
+    const float *target_probs;
+    int64_t target_ld;
+    const float *u_accept, *u_sample;
+    int32_t max_m;
+    int32_t *n_accepted, *out_token;
+};
+int launch_verify_tli(const TliVerifyArgs &a, hipStream_t stream);
 size_t retok_lds_bytes(int32_t max_bytes);
 int launch_retokenize(const RetokArgs &a, hipStream_t stream);
 

@@ -62,6 +62,9 @@ int main(void) {
     EXPECT(tt_verify_logits(1, 10, D, D, F, (const uint16_t *)W, 9, F, NULL, F, F, 4, D, D, NULL) == TT_EINVAL);
     EXPECT(tt_verify_logits(0, 10, NULL, NULL, NULL, NULL, 10, NULL, NULL, NULL, NULL, 4, NULL, NULL, NULL) ==
            TT_OK);
+    EXPECT(tt_verify_tli(1, 10, 12, D, D, D, D, F, 9, NULL, F, 12, F, F, 4, D, D, NULL) == TT_EINVAL);
+    EXPECT(tt_verify_tli(0, 10, 12, NULL, NULL, NULL, NULL, NULL, 10, NULL, NULL, 12, NULL, NULL, 4, NULL, NULL,
+                         NULL) == TT_OK);
     printf("done\n");
     return 0;
 }

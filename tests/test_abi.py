@@ -180,6 +180,21 @@ def test_invalid_arguments_return_before_launch():
     assert tli(q=None) == tt.TT_EINVAL
     assert tli(n=0, q=None) == tt.TT_OK
 
+    def vtli(n=2, v_d=10, v_t=12, ld_d=10, ld_t=12, max_m=4, t2d=dummy, q=dummy, mass=None):
+        return L.tt_verify_tli(n, v_d, v_t, dummy, t2d, dummy, dummy, q, ld_d, mass, dummy, ld_t, dummy, dummy,
+                               max_m, dummy, dummy, None)
+    assert vtli(n=-1) == tt.TT_EINVAL
+    assert vtli(v_d=0) == tt.TT_EINVAL
+    assert vtli(v_t=0) == tt.TT_EINVAL
+    assert vtli(ld_d=9) == tt.TT_EINVAL
+    assert vtli(ld_t=11) == tt.TT_EINVAL
+    assert vtli(max_m=-1) == tt.TT_EINVAL
+    assert vtli(max_m=65537) == tt.TT_EINVAL
+    assert vtli(t2d=None) == tt.TT_EINVAL
+    assert vtli(q=None) == tt.TT_EINVAL
+    assert vtli(v_t=(1 << 21) + 1, ld_t=(1 << 21) + 1) == tt.TT_EUNSUPPORTED
+    assert vtli(n=0, q=None) == tt.TT_OK
+
 
 def test_binding_refuses_host_tensors():
     torch = pytest.importorskip("torch")

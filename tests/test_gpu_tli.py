@@ -161,3 +161,131 @@ def test_standard_sd_on_the_tli_proposal():
     torch.cuda.synchronize()
     wn, wt, _, _ = oracle.sd_verify(v_t, xs, off, qp, p, ua, us)
     assert np.array_equal(nacc.cpu().numpy(), wn) and np.array_equal(tok.cpu().numpy(), wt)
+
+
+def tli_case(rng, v_d, v_t, N, M, frac=0.6, ld_d=None, ld_t=None):
+    """N streams of M_b <= M drafted positions: draft rows q over V_d, proposals y_j drawn from
+    q' (target ids), target rows p over V_t (rows off[b] + b + j), uniforms."""
+    d2t, t2d = random_maps(rng, v_d, v_t, frac)
+    Ms = rng.integers(0, M + 1, N)
+    off = np.zeros(N + 1, np.int32)
+    off[1:] = np.cumsum(Ms)
+    nt = int(off[-1])
+    q = (rng.random((nt, v_d)) ** 6).astype(np.float32)
+    q /= q.sum(axis=1, keepdims=True)
+    qp = oracle.tli_proposal(d2t, t2d, q)
+    ys = np.zeros(nt, np.int32)
+    for r in range(nt):
+        c = np.cumsum(qp[r].astype(np.float64))
+        ys[r] = min(int(np.searchsorted(c, rng.random() * c[-1], side="right")), v_t - 1) if c[-1] > 0 else 0
+    p = rng.random((nt + N, v_t)).astype(np.float32) ** 3
+    p /= p.sum(axis=1, keepdims=True)
+    # the target puts the proposal's mass or more on it now and then: acceptances, several rows
+    hit = rng.random(nt) < 0.5
+    rows_of = (off[:-1] + np.arange(N))[np.repeat(np.arange(N), Ms)] + (np.arange(nt) - np.repeat(off[:-1], Ms))
+    p[rows_of[hit], ys[hit]] += qp[hit, ys[hit]] * 2
+    ua = rng.random(nt).astype(np.float32)
+    us = rng.random(N).astype(np.float32)
+    qd = np.zeros((nt, ld_d or v_d), np.float32)
+    qd[:, :v_d] = q
+    pt = np.zeros((nt + N, ld_t or v_t), np.float32)
+    pt[:, :v_t] = p
+    return dict(d2t=d2t, t2d=t2d, off=off, Ms=Ms, q=q, qd=qd, ys=ys, p=p, pt=pt, ua=ua, us=us, v_d=v_d, v_t=v_t)
+
+
+def fused(c, max_m, mass=None):
+    import torch
+
+    import paper_2510_15545_amd as tt
+
+    nacc, tok = tt.verify_tli(to_dev(c["d2t"]), to_dev(c["t2d"]), to_dev(c["ys"]), to_dev(c["off"]), to_dev(c["qd"]),
+                              to_dev(c["pt"]), to_dev(c["ua"]), to_dev(c["us"]), max_m,
+                              draft_mass=None if mass is None else to_dev(np.asarray(mass, np.float32)), v_d=c["v_d"])
+    torch.cuda.synchronize()
+    return nacc.cpu().numpy(), tok.cpu().numpy()
+
+
+def two_calls(c, max_m):
+    import torch
+
+    import paper_2510_15545_amd as tt
+
+    qp = tt.tli_proposal(to_dev(c["d2t"]), to_dev(c["t2d"]), to_dev(c["qd"]), v_d=c["v_d"])
+    nacc, tok, _ = tt.verify_dense(c["v_t"], to_dev(c["ys"]), to_dev(c["off"]), qp, to_dev(c["pt"]), to_dev(c["ua"]),
+                                   to_dev(c["us"]), max_m)
+    torch.cuda.synchronize()
+    return nacc.cpu().numpy(), tok.cpu().numpy()
+
+
+def oracle_tli(c, max_m, mass=None):
+    qp = oracle.tli_proposal(c["d2t"], c["t2d"], c["q"], mass=mass)
+    n, t, _, _ = oracle.sd_verify(c["v_t"], c["ys"], c["off"], qp, c["p"], c["ua"], c["us"], max_m=max_m)
+    return n, t
+
+
+def intersected_mass(c):
+    return np.array([oracle.round_to_f32(sum(int(v) for v in np.floor(
+        np.clip(np.nan_to_num(r, nan=0.0), 0, 1)[c["d2t"] >= 0].astype(np.float64) * 2.0 ** 62)), 62)
+        for r in c["q"]], np.float32)
+
+
+@pytest.mark.parametrize("v_d,v_t,N,M,ld_d,ld_t", [(3000, 2500, 40, 4, None, None), (4099, 5123, 24, 6, 4101, 5127),
+                                                   (777, 1024, 70, 3, None, None), (64, 3, 9, 2, None, None)])
+def test_fused_tli_verification_matches_the_two_calls_and_the_oracle(v_d, v_t, N, M, ld_d, ld_t):
+    """tt_verify_tli against tt_tli_proposal + tt_verify_dense and the oracle's Alg. 3 then
+    Alg. 4, bit for bit, with S formed in the kernel and passed in as the drafter's: ragged
+    rows, odd strides, streams that draft nothing, rows whose intersection holds no mass
+    (q' = 0 keeps the proposal), NaN and above-one draft masses, proposals outside the
+    intersection, and sentinel streams (an id outside V_t, M above max_m)."""
+    print(f"[case] fused tli v_d={v_d} v_t={v_t} N={N} M={M} ld={ld_d},{ld_t}", flush=True)
+    rng = np.random.default_rng(v_d + v_t + N)
+    c = tli_case(rng, v_d, v_t, N, M, ld_d=ld_d, ld_t=ld_t)
+    nt = int(c["off"][-1])
+    if nt >= 3:
+        c["q"][0] = np.where(c["d2t"] >= 0, 0.0, c["q"][0])  # no intersected mass
+        c["q"][1, 0] = np.nan
+        c["q"][2, -1] = 1.5
+        c["ys"][min(3, nt - 1)] = int(np.nonzero(c["t2d"] < 0)[0][0]) if (c["t2d"] < 0).any() else 0
+        c["qd"][:, :v_d] = c["q"]
+    want = oracle_tli(c, M)
+    for got in (fused(c, M), fused(c, M, intersected_mass(c)), two_calls(c, M)):
+        assert np.array_equal(got[0], want[0]), np.nonzero(got[0] != want[0])[0][:5]
+        assert np.array_equal(got[1], want[1]), np.nonzero(got[1] != want[1])[0][:5]
+    assert (want[0] > 0).any() and (want[0] < c["Ms"]).any()
+    # sentinels: an id outside V_t in stream 1, max_m below stream 2's M
+    b1 = int(np.argmax(c["Ms"] > 0))
+    bad = dict(c, ys=c["ys"].copy())
+    bad["ys"][c["off"][b1]] = v_t
+    n1, t1 = fused(bad, M)
+    assert n1[b1] == -1 and t1[b1] == -1
+    keep = np.arange(N) != b1
+    assert np.array_equal(n1[keep], want[0][keep]) and np.array_equal(t1[keep], want[1][keep])
+    if c["Ms"].max() > 0:
+        small = int(c["Ms"].max()) - 1
+        n2, t2 = fused(c, small)
+        over = c["Ms"] > small
+        assert np.all(n2[over] == -1) and np.all(t2[over] == -1)
+
+
+def test_fused_tli_with_the_drafters_mass():
+    """S_j taken as given (App. D Alg. 3 normalises q' on the draft side): masses off the
+    intersected sum by up to a factor of two either way, and zero or NaN masses (q' = 0)."""
+    print("[case] fused tli with draft masses", flush=True)
+    rng = np.random.default_rng(48)
+    c = tli_case(rng, 2000, 3000, 48, 5)
+    mass = intersected_mass(c) * rng.uniform(0.5, 2.0, len(c["q"])).astype(np.float32)
+    mass[::7] = 0.0
+    mass[3::11] = np.nan
+    want = oracle_tli(c, 5, mass=mass)
+    got = fused(c, 5, mass)
+    assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
+
+
+def test_fused_tli_at_the_benchmark_vocabulary_sizes():
+    print("[case] fused tli workload 3 vocabulary sizes", flush=True)
+    wl = synth.make(3, n_streams=4, probs=False)
+    rng = np.random.default_rng(49)
+    c = tli_case(rng, len(wl.vocab_d.offsets) - 1, len(wl.vocab_t.offsets) - 1, 32, 4, frac=0.8)
+    want = oracle_tli(c, 4)
+    for got in (fused(c, 4), fused(c, 4, intersected_mass(c)), two_calls(c, 4)):
+        assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])

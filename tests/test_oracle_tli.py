@@ -179,3 +179,35 @@ def test_standard_sd_on_the_tli_proposal_follows_the_target(orc, seed):
                                     u24(rng, N), u24(rng, N))
     first = np.where(nacc > 0, xs, tok)
     assert chi2_pvalue(np.bincount(first, minlength=V_t), p[0]) > ALPHA
+
+
+def test_given_mass_replaces_the_normaliser(orc):
+    """A drafter's S (App. D Alg. 3 normalises q' on the draft side): the computed S passed back
+    gives the same rows bit for bit; twice S halves every entry exactly (a power-of-two scale of
+    the divisor); zero, negative or NaN S gives a zero row; S is taken as given even where it
+    differs from the intersected mass."""
+    rng = np.random.default_rng(5)
+    v_d, v_t = 50, 40
+    d2t = np.full(v_d, -1, np.int32)
+    t2d = np.full(v_t, -1, np.int32)
+    xs, ys = rng.choice(v_d, 30, replace=False), rng.choice(v_t, 30, replace=False)
+    d2t[xs], t2d[ys] = ys, xs
+    q = rng.random((6, v_d)).astype(np.float32)
+    q /= q.sum(axis=1, keepdims=True)
+    base = orc.tli_proposal(d2t, t2d, q)
+    S = np.array([np.float32(q[r][d2t >= 0].sum()) for r in range(6)], np.float32)
+    S_exact = np.array([np.float32(np.clip(q[r], 0, 1)[d2t >= 0][0]) / base[r][d2t[d2t >= 0][0]]
+                        for r in range(6)], np.float32)
+    same = orc.tli_proposal(d2t, t2d, q, mass=np.array([orc.round_to_f32(
+        sum(int(v) for v in np.floor(q[r][d2t >= 0].astype(np.float64) * 2.0 ** 62)), 62) for r in range(6)],
+        np.float32))
+    assert np.array_equal(same.view(np.uint32), base.view(np.uint32))
+    doubled = orc.tli_proposal(d2t, t2d, q, mass=2 * S)
+    assert np.array_equal(doubled, orc.tli_proposal(d2t, t2d, q, mass=S) / np.float32(2))
+    dead = orc.tli_proposal(d2t, t2d, q, mass=np.float32([0.0, -1.0, np.nan, 0.5, 0.5, 0.5]))
+    assert not dead[:3].any()
+    inter_y = d2t[d2t >= 0]
+    inter_x = np.nonzero(d2t >= 0)[0]
+    assert np.array_equal(dead[3][inter_y], q[3][inter_x] / np.float32(0.5))
+    assert not np.delete(dead[3], inter_y).any()
+    assert np.allclose(S_exact, S, rtol=1e-6)
