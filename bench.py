@@ -121,6 +121,11 @@ def parse():
     ap.add_argument("--logits", action="store_true",
                     help="verification from bf16 target logits and a temperature (tt_verify_logits) on the "
                          "benchmark's 256 streams at V_t=151,936 instead of fp32 probability rows")
+    ap.add_argument("--tli", action="store_true",
+                    help="standard speculative sampling with the Token-Level Intersection proposal (App. D "
+                         "Alg. 3) on 256 streams x M=8 at the benchmark's vocabularies: tt_verify_tli (q' formed "
+                         "on the fly, with and without the drafter's masses) against tt_tli_proposal + "
+                         "tt_verify_dense")
     ap.add_argument("--traffic", type=str, default=None,
                     help="counter summary with the measured HBM bytes per launch of the dominant kernel "
                          "(default: profiles/<kernel>_counters.txt)")
@@ -137,6 +142,8 @@ def main():
 
     if args.dense:
         return main_dense(args)
+    if args.tli:
+        return main_tli(args)
     if args.logits:
         return main_logits(args)
 
@@ -550,6 +557,120 @@ def main_dense(args):
             "sample": f"{k} whole steps of the benchmark batch ({n} streams), {dt * 1e3:.1f} ms each",
             "cpu_model": cpu_model(),
             "matches_gpu": bool(np.array_equal(o_n, acc) and np.array_equal(o_t, tok.cpu().numpy()))}
+    print(json.dumps(result), flush=True)
+
+
+def tli_workload(dev, n, M):
+    """The TLI benchmark's inputs, generated on the GPU (seeded): the intersection of the
+    benchmark's vocabularies, n streams x M draft rows softmax(3 N(0,1)) over V_d, proposals
+    drawn from q', target rows softmax(3 N(0,1)) over V_t with the proposal raised to the row's
+    maximum + 1 at half of the positions, the drafter's masses S_j (fp32 sums), uniforms on
+    the 2^-24 grid."""
+    import torch
+
+    import paper_2510_15545_amd as tt
+    from paper_2510_15545_amd import synth
+
+    S = synth.make(3, n_streams=4, probs=False)
+    vd = tt.Vocab.from_host(S.vocab_d.data, S.vocab_d.offsets, S.vocab_d.max_len, dev)
+    vt = tt.Vocab.from_host(S.vocab_t.data, S.vocab_t.offsets, S.vocab_t.max_len, dev)
+    d2t, t2d = tt.vocab_intersection(vd, tt.token_index(vd), vt, tt.token_index(vt))
+    v_d, v_t = int(d2t.numel()), int(t2d.numel())
+    nt = n * M
+    g = torch.Generator(device=dev)
+    g.manual_seed(4004)
+    q = torch.softmax(torch.randn((nt, v_d), generator=g, device=dev).mul_(3.0), dim=1)
+    qp = tt.tli_proposal(d2t, t2d, q)
+    ys = torch.multinomial(qp, 1, generator=g).view(-1).to(torch.int32)
+    del qp
+    off = torch.arange(0, nt + 1, M, dtype=torch.int32, device=dev)
+    x = torch.randn((nt + n, v_t), generator=g, device=dev).mul_(3.0)
+    rows = (torch.arange(nt, device=dev) // M) * (M + 1) + torch.arange(nt, device=dev) % M
+    force = torch.rand(nt, generator=g, device=dev) < 0.5
+    x[rows[force], ys.long()[force]] = x[rows[force]].max(dim=1).values + 1.0
+    p = torch.softmax(x, dim=1)
+    del x
+    mass = (q * (d2t >= 0).to(torch.float32)).sum(dim=1).contiguous()
+    ua = torch.randint(0, 1 << 24, (nt,), generator=g, device=dev).float().mul_(2.0 ** -24)
+    us = torch.randint(0, 1 << 24, (n,), generator=g, device=dev).float().mul_(2.0 ** -24)
+    return {"d2t": d2t, "t2d": t2d, "ys": ys, "off": off, "q": q, "p": p, "mass": mass, "ua": ua, "us": us,
+            "n": n, "M": M, "nt": nt, "v_d": v_d, "v_t": v_t, "inter": int((d2t >= 0).sum().item())}
+
+
+def main_tli(args):
+    """TLI verification (App. D Alg. 3 feeding Alg. 4): 256 streams x M=8 drafted positions over
+    the benchmark's vocabularies (V_d 128,256, V_t 151,936, their byte-string intersection);
+    draft rows softmax(3 N(0,1)), proposals drawn from q', target rows softmax(3 N(0,1)) with
+    the proposal raised to the row's maximum + 1 at half of the positions.  Inputs are generated
+    on the GPU (seeded).  Timed: tt_verify_tli with the drafter's masses (the step), without
+    them, and tt_tli_proposal over every draft row followed by tt_verify_dense."""
+    import torch
+
+    import paper_2510_15545_amd as tt
+
+    tt.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_gen = time.time()
+    W = tli_workload(dev, args.streams or 256, 8)
+    d2t, t2d, ys, off, q, p, mass, ua, us = (W[k] for k in ("d2t", "t2d", "ys", "off", "q", "p", "mass", "ua", "us"))
+    n, M, nt, v_t, inter = W["n"], W["M"], W["nt"], W["v_t"], W["inter"]
+    v_d = W["v_d"]
+    torch.cuda.synchronize()
+    t_gen = time.time() - t_gen
+    nacc = torch.empty(n, dtype=torch.int32, device=dev)
+    tok = torch.empty(n, dtype=torch.int32, device=dev)
+    outs = {}
+
+    def fused(with_mass):
+        return lambda i: tt.verify_tli(d2t, t2d, ys, off, q, p, ua, us, M, draft_mass=mass if with_mass else None,
+                                       out=(nacc, tok))
+    qbuf = torch.empty((nt, v_t), dtype=torch.float32, device=dev)
+    ws = tt.verify_workspace(n, v_t, dev)
+
+    def two_calls(i):
+        tt.tli_proposal(d2t, t2d, q, out=qbuf)
+        tt.verify_dense(v_t, ys, off, qbuf, p, ua, us, M, workspace=ws, out=(nacc, tok, None))
+
+    times = {}
+    for name, fn in (("fused_with_mass", fused(True)), ("fused", fused(False)), ("two_calls", two_calls)):
+        fn(0)
+        torch.cuda.synchronize()
+        outs[name] = (nacc.cpu().numpy().copy(), tok.cpu().numpy().copy())
+        times[name] = graph_ms(fn, k=max(1, min(args.graph_steps, 8)), reps=max(2, args.steps // 8))
+    # the drafter's S here is an fp32 sum, not the exact intersected mass the kernel forms without
+    # it, so that run is compared with the others only through its acceptance counts
+    acc = outs["fused"][0]
+    tested = int(np.minimum(acc + 1, M).sum())
+    rejected = int((acc < M).sum())
+    ms = times["fused_with_mass"]
+    # algorithmic bytes with the drafter's masses: per tested position the id, u, S, t2d entry,
+    # gathered draft mass and target probability; per stream the target row gamma, u_sample and
+    # the outputs; per rejected stream the draft masses on the intersection; the map t2d once
+    kbytes = int(24 * tested + n * (4 * v_t + 12) + rejected * 4 * inter + 4 * v_t)
+    gbs = kbytes / (ms * 1e-3) / 1e9
+    acc_m = outs["fused_with_mass"][0]
+    result = {
+        "metric": "verified draft tokens/s, TLI proposals (App. D Alg. 3 + 4) at V_d=128,256 / V_t=151,936; "
+                  "HBM GB/s vs peak",
+        "value": round(nt / (ms * 1e-3), 1), "unit": "draft tokens/s", "n_gpus": 1,
+        "steps": max(2, args.steps // 8) * max(1, min(args.graph_steps, 8)), "warmup": 1,
+        "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32+i64", "data": "synthetic",
+        "config": {"workload": f"{n} streams x M={M}, V_d={v_d}, V_t={v_t}, intersection {inter}", "streams": n,
+                   "draft_tokens_per_step": nt, "path": "tt_verify_tli with the drafter's masses",
+                   "launch": "hip-graph of %d steps" % max(1, min(args.graph_steps, 8))},
+        "accept": {"mean_gamma": round(float(acc_m.mean()), 3), "rejected_streams": int((acc_m < M).sum())},
+        "us_per_step": {k: round(v * 1e3, 2) for k, v in times.items()},
+        "same_outputs_fused_and_two_calls": bool(np.array_equal(outs["fused"][0], outs["two_calls"][0]) and
+                                                 np.array_equal(outs["fused"][1], outs["two_calls"][1])),
+        "with_mass_acceptance_agreement": round(float((acc_m == acc).mean()), 4),
+        "roofline": {"kernel": "verify_tli_row", "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "traffic_note": "no counters for this kernel", "algorithmic_bytes_per_launch": kbytes,
+                     "launch_us": round(ms * 1e3, 2)},
+        "gen_seconds": round(t_gen, 1),
+    }
     print(json.dumps(result), flush=True)
 
 

@@ -18,6 +18,8 @@
 // The row is read from HBM once; the maps are shared by every row and stay in cache.
 #include "verify_core.h"
 
+TT_STAMPS_TABLE(tli)
+
 namespace tt {
 namespace {
 
@@ -188,17 +190,8 @@ struct TliVerifyParams {
     int32_t nc, vec_t, vec_d;
 };
 
-// 16 target probabilities of a lane (elements x0 .. x0+15 with x0 = c*1024 + lane*16) and the
-// q' values at them (0 past v_t); q' from draft row drow with mass S, or 0 when drow is null.
-__device__ __forceinline__ void lane_pq(const TliVerifyArgs &a, const float *prow, const float *drow, float S,
-                                        int x0, bool vec, float (&pv)[16], float (&dv)[16]) {
-    vcore::read16(prow, x0, a.v_t, vec, pv);
-    if (drow == nullptr) {
-#pragma unroll
-        for (int k = 0; k < 16; ++k) dv[k] = 0.0f;
-        return;
-    }
-    int32_t xs[16];
+// The 16 draft ids t2d of a lane's elements x0 .. x0+15 (x0 = c*1024 + lane*16; -1 past v_t).
+__device__ __forceinline__ void load_x(const TliVerifyArgs &a, int x0, bool vec, int32_t (&xs)[16]) {
     if (vec && x0 + 16 <= a.v_t) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -212,11 +205,43 @@ __device__ __forceinline__ void lane_pq(const TliVerifyArgs &a, const float *pro
 #pragma unroll
         for (int k = 0; k < 16; ++k) xs[k] = x0 + k < a.v_t ? a.t2d[x0 + k] : -1;
     }
+}
+
+// Their target probabilities (0 past v_t) and ids.
+__device__ __forceinline__ void load_px(const TliVerifyArgs &a, const float *prow, int x0, bool vec, float (&pv)[16],
+                                        int32_t (&xs)[16]) {
+    vcore::read16(prow, x0, a.v_t, vec, pv);
+    load_x(a, x0, vec, xs);
+}
+
+// The draft masses q(x) at the 16 ids (0 for an id outside [0, v_d), or without a draft row).
+// Only the lanes that keep an id load (the intersection is often a small part of V_t).
+__device__ __forceinline__ void gather16(const TliVerifyArgs &a, const float *drow, const int32_t (&xs)[16],
+                                         float (&gv)[16]) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) gv[k] = (drow != nullptr && xs[k] >= 0 && xs[k] < a.v_d) ? drow[xs[k]] : 0.0f;
+}
+
+// The Q62 sum of the 16 residual entries q62(clamp01(p - q')) (q' = qprime(g, S); 0 past v_t).
+__device__ __forceinline__ uint64_t residual_sum16(const float (&pv)[16], const float (&gv)[16], float S, int x0,
+                                                   int vt) {
+    uint64_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) sum += x0 + k < vt ? q62(clamp01(pv[k] - qprime(gv[k], S))) : 0ull;
+    return sum;
+}
+
+// Q62 residual entries q62(clamp01(p - q')) of the 16 elements (q' = qprime(g, S); 0 past v_t,
+// where p = g = 0).
+__device__ __forceinline__ uint64_t residual16(const float (&pv)[16], const float (&gv)[16], float S, int x0, int vt,
+                                               uint64_t (&qv)[16]) {
+    uint64_t sum = 0;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
-        const float g = (xs[k] >= 0 && xs[k] < a.v_d) ? drow[xs[k]] : 0.0f;
-        dv[k] = qprime(g, S);
+        qv[k] = x0 + k < vt ? q62(clamp01(pv[k] - qprime(gv[k], S))) : 0ull;
+        sum += qv[k];
     }
+    return sum;
 }
 
 __global__ void __launch_bounds__(kThreads) verify_tli_row(TliVerifyParams p) {
@@ -229,6 +254,7 @@ __global__ void __launch_bounds__(kThreads) verify_tli_row(TliVerifyParams p) {
     __shared__ float sh_S, sh_Sr;
     __shared__ int sh_ok, sh_gamma, sh_ctr, sh_rej;
 
+    TT_STAMP(0);
     const int t0 = a.target_off[b];
     const int M = a.target_off[b + 1] - t0;
     if (!(M >= 0 && M <= a.max_m)) {
@@ -319,23 +345,41 @@ __global__ void __launch_bounds__(kThreads) verify_tli_row(TliVerifyParams p) {
             }
         }
     }
+    TT_STAMP(1);
     // residual (or bonus) row: Q62 chunk sums of max(0, p - q') into LDS
     const bool vec = p.vec_t != 0;
     const float *prow = a.target_probs + (int64_t)(t0 + b + gamma) * a.target_ld;
     const float *drow = gamma < M ? a.draft_probs + (int64_t)(t0 + gamma) * a.draft_ld : nullptr;
     const int nc = p.nc;
-    for (int c = wave;;) {
-        if (c >= nc) break;
-        float pv[16], dv[16];
-        lane_pq(a, prow, drow, S_r, c * vcore::kChunk + lane * 16, vec, pv, dv);
-        uint64_t acc = 0;
+    {
+        // each wave: chunk c's probabilities and draft masses, chunk cn's probabilities and ids
+        // in flight behind them (a chunk's gathers wait for its ids only)
+        float pv[16], gv[16], pn[16];
+        int32_t xs[16];
+        int c = wave, cn = nc;
+        if (c < nc) {
+            load_px(a, prow, c * vcore::kChunk + lane * 16, vec, pv, xs);
+            gather16(a, drow, xs, gv);
+            cn = vcore::next_chunk(&sh_ctr, c, kWaves);
+            if (cn < nc) load_px(a, prow, cn * vcore::kChunk + lane * 16, vec, pn, xs);
+        }
+        while (c < nc) {
+            uint64_t acc = residual_sum16(pv, gv, S_r, c * vcore::kChunk + lane * 16, a.v_t);
+            acc = vcore::wave_inclusive_scan(acc);
+            if (lane == kWave - 1) sh_part[c] = acc;
+            c = cn;
+            if (c < nc) {
 #pragma unroll
-        for (int k = 0; k < 16; ++k) acc += q62(clamp01(pv[k] - dv[k]));  // 0 past v_t: pv = dv = 0
-        acc = vcore::wave_inclusive_scan(acc);
-        if (lane == kWave - 1) sh_part[c] = acc;
-        c = vcore::next_chunk(&sh_ctr, c, kWaves);
+                for (int k = 0; k < 16; ++k) pv[k] = pn[k];
+                gather16(a, drow, xs, gv);
+                cn = vcore::next_chunk(&sh_ctr, c, kWaves);
+                if (cn < nc) load_px(a, prow, cn * vcore::kChunk + lane * 16, vec, pn, xs);
+            }
+        }
     }
+    if (wave < 12) TT_STAMP_WAVE(4 + wave);
     __syncthreads();
+    TT_STAMP(2);
     if (wave != 0) return;
     uint64_t Z, T, base;
     int cs;
@@ -347,14 +391,12 @@ __global__ void __launch_bounds__(kThreads) verify_tli_row(TliVerifyParams p) {
         token = a.v_t - 1;
     } else {
         const int x0 = cs * vcore::kChunk + lane * 16;
-        float pv[16], dv[16];
-        lane_pq(a, prow, drow, S_r, x0, vec, pv, dv);
-        uint64_t qv[16], sum = 0;
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-            qv[k] = x0 + k < a.v_t ? q62(clamp01(pv[k] - dv[k])) : 0ull;
-            sum += qv[k];
-        }
+        float pv[16], gv[16];
+        int32_t xs[16];
+        load_px(a, prow, x0, vec, pv, xs);
+        gather16(a, drow, xs, gv);
+        uint64_t qv[16];
+        const uint64_t sum = residual16(pv, gv, S_r, x0, a.v_t, qv);
         const uint64_t lincl = vcore::wave_inclusive_scan(sum) + base;
         const uint64_t lexcl = lincl - sum;
         const unsigned long long lhit = __ballot(lexcl <= T && T < lincl);
@@ -376,6 +418,7 @@ __global__ void __launch_bounds__(kThreads) verify_tli_row(TliVerifyParams p) {
         a.n_accepted[b] = gamma;
         a.out_token[b] = token;
     }
+    TT_STAMP(3);
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
