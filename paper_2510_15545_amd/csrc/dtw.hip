@@ -38,7 +38,9 @@
 //     the rows' runs.
 //
 // LDS layout (bytes, each region 16-byte aligned):
-//   tslot [max_m][TB] / tlen [max_m]   target token bytes and lengths
+//   tslot [max_m + 8][TB + 4] / tlen [max_m + 8]  target token bytes and lengths: 4 empty
+//                                      slots on each side, a pad dword per slot when the plan fits
+//                                      that way
 //   dslot [max_k][TB] / dlen [max_k]   draft token bytes and lengths
 //   row0, row1 [64 + max_m + 136] int32 C of the row above the strip / of the strip's last
 //                                      row, by column with a 64-entry front pad
@@ -81,11 +83,13 @@ constexpr int kRowFront = 64;                    // row buffers hold columns -64
 constexpr int kRowBack = 136;
 constexpr size_t kLdsLimit = 160 * 1024 - 1024;  // gfx950 LDS per workgroup, less static use
 constexpr uint32_t kOutOfBand = 0x80808080u;     // four cost bytes with the out-of-band bit
+constexpr int kTPad = 4;                         // empty target slots before column 1 and after column M
 
 __host__ __device__ inline size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
 
 struct LdsPlan {
     size_t tslot, tlen, dslot, dlen, row0, row1, cost, path, total;
+    int tstride;  // dwords per target token slot
 };
 
 __host__ __device__ inline int band_half_width_bound(int32_t max_k, int32_t max_m, int32_t w) {
@@ -104,13 +108,17 @@ __host__ __device__ inline int row_words_bound(int32_t max_k, int32_t max_m, int
     return (int)((W + 15) / 16) + 1;
 }
 
-__host__ __device__ inline LdsPlan plan_lds(int32_t max_k, int32_t max_m, int32_t w, int tb) {
+// Target token slots take TB / 4 + 1 dwords when the plan fits the LDS that way: the helper
+// lanes of a row read slots four apart, which an odd stride spreads over distinct banks (a
+// stride of TB / 4 dwords puts two lanes on every bank they use); else TB / 4.
+__host__ __device__ inline LdsPlan plan_lds_with(int32_t max_k, int32_t max_m, int32_t w, int tb, int tstride) {
     LdsPlan p;
     size_t off = 0;
+    p.tstride = tstride;
     p.tslot = off;
-    off = align16(off + (size_t)max_m * tb);
+    off = align16(off + 4 * ((size_t)max_m + 2 * kTPad) * tstride);
     p.tlen = off;
-    off = align16(off + (size_t)max_m);
+    off = align16(off + (size_t)max_m + 2 * kTPad);
     p.dslot = off;
     off = align16(off + (size_t)max_k * tb);
     p.dlen = off;
@@ -130,6 +138,11 @@ __host__ __device__ inline LdsPlan plan_lds(int32_t max_k, int32_t max_m, int32_
     off = align16(off + 8 * (size_t)max_k);
     p.total = off;
     return p;
+}
+
+__host__ __device__ inline LdsPlan plan_lds(int32_t max_k, int32_t max_m, int32_t w, int tb) {
+    const LdsPlan wide = plan_lds_with(max_k, max_m, w, tb, tb / 4 + 1);
+    return wide.total <= kLdsLimit ? wide : plan_lds_with(max_k, max_m, w, tb, tb / 4);
 }
 
 struct Band {
@@ -216,7 +229,7 @@ __device__ __forceinline__ uint32_t myers_distance(const uint32_t (&pw)[TB / 4],
 // token of more than two bytes.
 template <int TB>
 __device__ __forceinline__ void chunk_costs(const Band &g, const Strip &st, int T0, uint32_t *buf,
-                                            const uint32_t *tslot, const uint8_t *tlen, const uint32_t *dslot,
+                                            const uint32_t *tslot, int ts, const uint8_t *tlen, const uint32_t *dslot,
                                             const uint8_t *dlen, int h, int nh) {
     for (int item = h; item < st.R * kGroups; item += nh) {
         const int r = item / kGroups, gq = item % kGroups;
@@ -239,11 +252,10 @@ __device__ __forceinline__ void chunk_costs(const Band &g, const Strip &st, int 
                     uint32_t yw[kBatch][TB / 4];
                     int yn[kBatch];
 #pragma unroll
-                    for (int v = 0; v < kBatch; ++v) {
-                        int j = jb + u0 + v;
-                        j = j < 1 ? 1 : (j > g.M ? g.M : j);
-                        read_slot<TB>(tslot + (j - 1) * (TB / 4), yw[v]);
-                        yn[v] = tlen[j - 1];
+                    for (int v = 0; v < kBatch; ++v) {  // jb - 1 + kTPad >= 0: the item meets the band
+                        const int sl = jb + u0 + v - 1 + kTPad;
+                        read_slot<TB>(tslot + sl * ts, yw[v]);
+                        yn[v] = tlen[sl];
                     }
 #pragma unroll
                     for (int v = 0; v < kBatch; ++v) {
@@ -273,8 +285,8 @@ __device__ __forceinline__ void chunk_costs(const Band &g, const Strip &st, int 
                     const int j = jb + u;
                     if (j >= jl && j <= jh) {
                         uint32_t yw[TB / 4];
-                        read_slot<TB>(tslot + (j - 1) * (TB / 4), yw);
-                        const uint32_t d = (uint32_t)token_distance<TB>(xw, xm, yw, tlen[j - 1]);
+                        read_slot<TB>(tslot + (j - 1 + kTPad) * ts, yw);
+                        const uint32_t d = (uint32_t)token_distance<TB>(xw, xm, yw, tlen[j - 1 + kTPad]);
                         packed = (packed & ~(0xFFu << (8 * u))) | (d << (8 * u));
                     }
                 }
@@ -345,7 +357,7 @@ __device__ __forceinline__ void sweep_chunk(Sweep &sw, const uint32_t *buf, cons
     }
 }
 
-template <int TB>
+template <int TB, int TS>
 __global__ void __launch_bounds__(band_threads<TB>()) __attribute__((amdgpu_waves_per_eu(band_threads<TB>() / 64)))
 dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
                                                      int rw, const int32_t *order) {
@@ -359,6 +371,7 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
     const int t0 = a.target_off[b], M = a.target_off[b + 1] - t0;
 
     uint32_t *tslot = reinterpret_cast<uint32_t *>(lds + lp.tslot);
+    constexpr int ts = TS;  // dwords per target token slot (lp.tstride)
     uint8_t *tlen = lds + lp.tlen;
     uint32_t *dslot = reinterpret_cast<uint32_t *>(lds + lp.dslot);
     uint8_t *dlen = lds + lp.dlen;
@@ -376,9 +389,16 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
     if (shape_ok) {
         for (int e = tid; e < K + M; e += kThreads) {
             const bool ok = e < K ? stage_token<TB>(a.vd, a.draft_ids[d0 + e], dslot + e * (TB / 4), dlen + e)
-                                  : stage_token<TB>(a.vt, a.target_ids[t0 + e - K], tslot + (e - K) * (TB / 4),
-                                                    tlen + (e - K));
+                                  : stage_token<TB>(a.vt, a.target_ids[t0 + e - K], tslot + (e - K + kTPad) * ts,
+                                                    tlen + (e - K + kTPad));
             bad |= ok ? 0 : 1;
+        }
+        // the empty slots around the target tokens (read by items that straddle the band's ends)
+        if (tid < 2 * kTPad * ts) {
+            const int sl = tid / ts, q = tid % ts;
+            const int slot = sl < kTPad ? sl : M + sl;  // 0 .. kTPad-1 and M + kTPad .. M + 2 kTPad - 1
+            tslot[slot * ts + q] = 0u;
+            if (q == 0) tlen[slot] = 0;
         }
     }
     if (dtw::block_or(bad, votes, kThreads / kWave)) {
@@ -409,7 +429,7 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
         }
     }
     Strip st = strip_at(g, 0);
-    chunk_costs<TB>(g, st, 0, costbuf, tslot, tlen, dslot, dlen, tid, kThreads);
+    chunk_costs<TB>(g, st, 0, costbuf, tslot, ts, tlen, dslot, dlen, tid, kThreads);
     __syncthreads();
     // the sweep is the critical path: its wave wins issue arbitration on its SIMD
     if (wave == 0) __builtin_amdgcn_s_setprio(3);
@@ -434,9 +454,9 @@ dtw_band(AlignArgs a, LdsPlan lp, uint32_t *gcodes, size_t gcode_stride,
             if (wave == 0) {
                 sweep_chunk(sw, cur_buf, rowIn, rowOut, c * kChunk, st.jfirst, rw);
             } else if (c + 1 < st.nchunks) {
-                chunk_costs<TB>(g, st, (c + 1) * kChunk, next_buf, tslot, tlen, dslot, dlen, tid - kWave, kHelpers);
+                chunk_costs<TB>(g, st, (c + 1) * kChunk, next_buf, tslot, ts, tlen, dslot, dlen, tid - kWave, kHelpers);
             } else if (s + 1 < nstrips) {
-                chunk_costs<TB>(g, nxt, 0, next_buf, tslot, tlen, dslot, dlen, tid - kWave, kHelpers);
+                chunk_costs<TB>(g, nxt, 0, next_buf, tslot, ts, tlen, dslot, dlen, tid - kWave, kHelpers);
             }
             __syncthreads();
             ++gidx;
@@ -792,14 +812,16 @@ int launch_tb(const AlignArgs &a, void *workspace, size_t workspace_bytes, hipSt
                            dim3(kOrderThreads), 0, stream, a, order);
         if (hipGetLastError() != hipSuccess) return TT_ELAUNCH;
     }
-    if (lp.total > 64 * 1024) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void *>(&dtw_band<TB>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lp.total) != hipSuccess)
+    auto launch = [&](auto kernel) -> int {
+        if (lp.total > 64 * 1024 &&
+            hipFuncSetAttribute(reinterpret_cast<const void *>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lp.total) != hipSuccess)
             return TT_ELAUNCH;
-    }
-    hipLaunchKernelGGL(dtw_band<TB>, dim3(a.n_pairs), dim3(band_threads<TB>()), lp.total, stream, a, lp,
-                       static_cast<uint32_t *>(workspace), stride, rw, order);
-    return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+        hipLaunchKernelGGL(kernel, dim3(a.n_pairs), dim3(band_threads<TB>()), lp.total, stream, a, lp,
+                           static_cast<uint32_t *>(workspace), stride, rw, order);
+        return hipGetLastError() == hipSuccess ? TT_OK : TT_ELAUNCH;
+    };
+    return lp.tstride == TB / 4 + 1 ? launch(&dtw_band<TB, TB / 4 + 1>) : launch(&dtw_band<TB, TB / 4>);
 }
 
 }  // namespace
