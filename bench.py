@@ -15,6 +15,7 @@ a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -126,6 +127,13 @@ def parse():
                          "Alg. 3) on 256 streams x M=8 at the benchmark's vocabularies: tt_verify_tli (q' formed "
                          "on the fly, with and without the drafter's masses) against tt_tli_proposal + "
                          "tt_verify_dense")
+    ap.add_argument("--read-ceiling", action="store_true",
+                    help="time plain device reads of the benchmark's bytes (256 rows x 151,936 fp32, rotating "
+                         "replicas) with a library reduction and a device-to-device copy: the practical HBM "
+                         "read rate the verification's rows are compared against")
+    ap.add_argument("--phase-stamps", action="store_true",
+                    help="with a library built with -DTT_PHASE_STAMPS: where verify_row's and step_fused's time "
+                         "goes on the benchmark batch (per-workgroup real-time stamps at the phase boundaries)")
     ap.add_argument("--traffic", type=str, default=None,
                     help="counter summary with the measured HBM bytes per launch of the dominant kernel "
                          "(default: profiles/<kernel>_counters.txt)")
@@ -146,6 +154,10 @@ def main():
         return main_tli(args)
     if args.logits:
         return main_logits(args)
+    if args.read_ceiling:
+        return main_read_ceiling(args)
+    if args.phase_stamps:
+        return main_phase_stamps(args)
 
     import torch
 
@@ -558,6 +570,129 @@ def main_dense(args):
             "cpu_model": cpu_model(),
             "matches_gpu": bool(np.array_equal(o_n, acc) and np.array_equal(o_t, tok.cpu().numpy()))}
     print(json.dumps(result), flush=True)
+
+
+def main_phase_stamps(args):
+    """Phase times of verify_row and step_fused on the benchmark batch from the stamps a
+    -DTT_PHASE_STAMPS build records (the 100 MHz real-time counter at each phase boundary, per
+    workgroup, of the last launch): 20 launches back to back in a HIP graph, then the table is
+    read; five samples."""
+    import torch
+
+    import paper_2510_15545_amd as tt
+    from paper_2510_15545_amd import synth
+
+    L = tt.lib()
+    if not hasattr(L, "tt_phase_stamps_verify") or not hasattr(L, "tt_phase_stamps_step"):
+        print("the library was built without phase stamps: python3 -m paper_2510_15545_amd.build "
+              "-DTT_PHASE_STAMPS", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    S = synth.make(3, n_streams=args.streams)
+    n = S.n
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    mtb = max(S.vocab_d.max_len, S.vocab_t.max_len)
+    vd = tt.Vocab.from_host(S.vocab_d.data, S.vocab_d.offsets, S.vocab_d.max_len, dev)
+    vt = tt.Vocab.from_host(S.vocab_t.data, S.vocab_t.offsets, S.vocab_t.max_len, dev)
+    di, do, ti, to, vi = t(S.draft_ids), t(S.draft_off), t(S.target_ids), t(S.target_off), t(S.verify_ids)
+    mk, mm = max(1, S.max_k), max(1, S.max_m)
+    R = max(1, args.replicas)
+    dp = t(S.draft_probs)
+    tp = [t(S.target_probs)]
+    for _ in range(R - 1):
+        tp.append(tp[0].clone())
+    ua, us = t(S.u_accept), t(S.u_sample)
+    a_out = tt.align(vd, vt, di, do, ti, to, args.w, mk, mm)
+    q = tt.transfer(S.v_d, di, do, to, a_out[3], dp)
+    nacc = torch.empty(n, dtype=torch.int32, device=dev)
+    tok = torch.empty(n, dtype=torch.int32, device=dev)
+    ws = tt.verify_workspace(n, S.v_t, dev)
+    st_ws = tt.step_workspace(n, S.v_t, mk, mm, args.w, mtb, dev)
+    st_out = (torch.empty(n, dtype=torch.int32, device=dev), torch.empty(n, dtype=torch.int32, device=dev),
+              torch.empty(max(1, tt.path_capacity(S.draft_off[-1], S.target_off[-1])), dtype=torch.int32,
+                          device=dev),
+              torch.empty(max(1, int(S.target_off[-1])), dtype=torch.int32, device=dev), torch.empty_like(q),
+              torch.empty_like(nacc), torch.empty_like(tok), None)
+    hip = ctypes.CDLL("libamdhip64.so")
+    slots = 16
+
+    def table(unit):
+        f = getattr(L, "tt_phase_stamps_" + unit)
+        f.restype = ctypes.c_void_p
+        buf = np.zeros(n * slots, np.uint64)
+        torch.cuda.synchronize()
+        if hip.hipMemcpy(buf.ctypes.data_as(ctypes.c_void_p), ctypes.c_void_p(f()), ctypes.c_size_t(buf.nbytes),
+                         2) != 0:
+            raise RuntimeError("hipMemcpy of the stamp table failed")
+        return buf.reshape(n, slots).astype(np.int64)
+
+    def stats(x):
+        x = np.asarray(x, np.float64)
+        return {"p0": round(float(x.min()), 2), "p50": round(float(np.median(x)), 2),
+                "p90": round(float(np.percentile(x, 90)), 2), "p100": round(float(x.max()), 2)}
+
+    kernels = {
+        "verify_row": (lambda i: tt.verify(S.v_t, vi, to, q, tp[i % R], ua, us, mm, workspace=ws,
+                                           out=(nacc, tok, None)), "verify",
+                       [("acceptance scan (wave 0)", 0, 1), ("stream the row (all waves, to the barrier)", 2, 4),
+                        ("sample (wave 0)", 4, 5)], 5),
+        "step_fused": (lambda i: tt.step(vd, vt, S.v_d, S.v_t, di, do, ti, to, args.w, mk, mm, dp, tp[i % R], ua, us,
+                                         workspace=st_ws, out=st_out), "step",
+                       [("staging and prefetch", 0, 1), ("distances, recurrence, move tables", 1, 2),
+                        ("backtrack, transfer, acceptance", 2, 3), ("stream the row (to the barrier)", 3, 5),
+                        ("sample (wave 0)", 5, 6)], 6),
+    }
+    out = {"metric": "phase times per workgroup (us) on the benchmark batch", "streams": n}
+    for name, (fn, unit, phases, last) in kernels.items():
+        us_launch = graph_ms(fn, k=20, reps=5) * 1e3
+        samples = {ph: [] for ph, _, _ in phases}
+        ends, spans, starts = [], [], []
+        for _ in range(5):
+            graph_ms(fn, k=20, reps=1)
+            st = table(unit)
+            rel = (st - st[:, 0].min()) / 100.0  # 100 MHz counter -> us
+            for ph, a, b in phases:
+                samples[ph].extend(rel[:, b] - rel[:, a])
+            ends.extend(rel[:, last])
+            starts.extend(rel[:, 0])
+            spans.append(rel[:, last].max())
+        out[name] = {"launch_us_by_events": round(us_launch, 2),
+                     "phases": {ph: stats(v) for ph, v in samples.items()},
+                     "workgroup_start": stats(starts), "workgroup_end": stats(ends),
+                     "span_first_start_to_last_end": stats(spans)}
+    print(json.dumps(out), flush=True)
+
+
+def main_read_ceiling(args):
+    """Reads of the verification's row bytes without the verification: torch.sum over 256 rows
+    x 151,936 fp32 (one replica of four per step, as the benchmark rotates them), and a copy
+    of the same bytes (read + write), each eight to a HIP graph, HIP events."""
+    import torch
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    rows, v = 256, 151_936
+    R = max(1, args.replicas)
+    g = torch.Generator(device=dev)
+    g.manual_seed(5005)
+    xs = [torch.rand((rows, v), generator=g, device=dev) for _ in range(R)]
+    dst = torch.empty_like(xs[0])
+    acc = torch.empty((), device=dev)
+    nbytes = 4 * rows * v
+    reps = max(2, args.steps // 8)
+    sum_ms = graph_ms(lambda i: torch.sum(xs[i % R], out=acc), k=8, reps=reps)
+    copy_ms = graph_ms(lambda i: dst.copy_(xs[i % R]), k=8, reps=reps)
+    out = {"metric": "plain HBM reads of the benchmark's row bytes", "bytes_per_launch": nbytes,
+           "sum_us": round(sum_ms * 1e3, 2), "sum_GBps": round(nbytes / (sum_ms * 1e-3) / 1e9, 1),
+           "copy_us": round(copy_ms * 1e3, 2),
+           "copy_read_GBps": round(nbytes / (copy_ms * 1e-3) / 1e9, 1),
+           "copy_read_write_GBps": round(2 * nbytes / (copy_ms * 1e-3) / 1e9, 1),
+           "peak_GBps": HBM_PEAK_GBS}
+    print(json.dumps(out), flush=True)
 
 
 def tli_workload(dev, n, M):
