@@ -667,31 +667,149 @@ def main_phase_stamps(args):
     print(json.dumps(out), flush=True)
 
 
+READ_PROBE_SRC = r"""
+#include <hip/hip_runtime.h>
+// Plain reads of rows x v floats with non-temporal 16-byte loads; one float per workgroup is
+// written so that the loads are kept.
+//   rows_read:   one 1024-thread workgroup per row, one load per lane and step
+//   rows_chunks: one 1024-thread workgroup per row in the verification's order (wave w takes
+//                1024-float chunks w, w + 16, ..., four loads per lane and chunk)
+//   rows_split:  S workgroups of T threads per row, each a contiguous share, four loads per lane
+//   grid_read:   a grid-stride loop over the whole array, 2,048 workgroups of 256 threads
+typedef float f4v __attribute__((ext_vector_type(4)));
+__global__ void __launch_bounds__(1024) rows_read(const float *x, long v, float *out) {
+    const f4v *r = reinterpret_cast<const f4v *>(x + (long)blockIdx.x * v);
+    const long n4 = v / 4;
+    f4v acc = {0, 0, 0, 0};
+    for (long k = threadIdx.x; k < n4; k += 1024) acc += __builtin_nontemporal_load(r + k);
+    const float s = acc.x + acc.y + acc.z + acc.w;
+    if (s == 12345.0f) out[blockIdx.x] = s;
+}
+__global__ void __launch_bounds__(1024) rows_chunks(const float *x, long v, float *out) {
+    const f4v *r = reinterpret_cast<const f4v *>(x + (long)blockIdx.x * v);
+    const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+    const long n4 = v / 4;
+    f4v acc = {0, 0, 0, 0};
+    for (long c = wave; c * 256 < n4; c += 16) {
+        f4v t[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const long k = c * 256 + u * 64 + lane;
+            t[u] = k < n4 ? __builtin_nontemporal_load(r + k) : f4v{0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc += t[u];
+    }
+    const float s = acc.x + acc.y + acc.z + acc.w;
+    if (s == 12345.0f) out[blockIdx.x] = s;
+}
+template <int T>
+__global__ void __launch_bounds__(T) rows_split(const float *x, long v, int S, float *out) {
+    const int b = blockIdx.x / S, s = blockIdx.x % S;
+    const long n4 = v / 4, lo = n4 * s / S, hi = n4 * (s + 1) / S;
+    const f4v *r = reinterpret_cast<const f4v *>(x + (long)b * v);
+    f4v acc = {0, 0, 0, 0};
+    long k = lo + threadIdx.x;
+    for (; k + 3 * T < hi; k += 4 * T) {
+        f4v t[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) t[u] = __builtin_nontemporal_load(r + k + u * T);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc += t[u];
+    }
+    for (; k < hi; k += T) acc += __builtin_nontemporal_load(r + k);
+    const float sm = acc.x + acc.y + acc.z + acc.w;
+    if (sm == 12345.0f) out[blockIdx.x % 4096] = sm;
+}
+__global__ void __launch_bounds__(256) grid_read(const float *x, long n4, float *out) {
+    const f4v *r = reinterpret_cast<const f4v *>(x);
+    f4v acc = {0, 0, 0, 0};
+    for (long k = blockIdx.x * 256L + threadIdx.x; k < n4; k += (long)gridDim.x * 256) acc += __builtin_nontemporal_load(r + k);
+    const float s = acc.x + acc.y + acc.z + acc.w;
+    if (s == 12345.0f) out[blockIdx.x] = s;
+}
+// kind 0: rows_read, 1: rows_chunks, 2: rows_split 2 x 512, 3: rows_split 4 x 256, 4: grid_read
+extern "C" int probe(int kind, const float *x, int rows, long v, float *out, void *stream) {
+    hipStream_t st = (hipStream_t)stream;
+    switch (kind) {
+    case 0: hipLaunchKernelGGL(rows_read, dim3(rows), dim3(1024), 0, st, x, v, out); break;
+    case 1: hipLaunchKernelGGL(rows_chunks, dim3(rows), dim3(1024), 0, st, x, v, out); break;
+    case 2: hipLaunchKernelGGL(rows_split<512>, dim3(rows * 2), dim3(512), 0, st, x, v, 2, out); break;
+    case 3: hipLaunchKernelGGL(rows_split<256>, dim3(rows * 4), dim3(256), 0, st, x, v, 4, out); break;
+    case 4: hipLaunchKernelGGL(grid_read, dim3(2048), dim3(256), 0, st, x, (long)rows * v / 4, out); break;
+    default: return 2;
+    }
+    return hipGetLastError() == hipSuccess ? 0 : 1;
+}
+"""
+
+
 def main_read_ceiling(args):
-    """Reads of the verification's row bytes without the verification: torch.sum over 256 rows
-    x 151,936 fp32 (one replica of four per step, as the benchmark rotates them), and a copy
-    of the same bytes (read + write), each eight to a HIP graph, HIP events."""
+    """Plain reads of the verification's row bytes (256 rows x 151,936 fp32, one replica of four
+    per launch, as the benchmark rotates them), by read-only kernels built here from the source
+    above: the verification's launch shape (a 1024-thread workgroup per row, also in its chunk
+    order), several workgroups per row, and a grid-stride loop; for reference torch.sum of the
+    same bytes and a device-to-device copy.  The kernels run eight to a HIP graph; torch.sum and the
+    copy are launched back to back (no graph: the library reduction may clear its scratch with
+    memsets); HIP events."""
+    import subprocess
+    import tempfile
+
     import torch
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     rows, v = 256, 151_936
+    tmp = tempfile.mkdtemp(prefix="tt_read_probe_")
+    src, lib = os.path.join(tmp, "probe.hip"), os.path.join(tmp, "probe.so")
+    with open(src, "w") as f:
+        f.write(READ_PROBE_SRC)
+    subprocess.run(["/opt/rocm/bin/hipcc", "--offload-arch=gfx950", "-O3", "-fPIC", "-shared", "-Xclang",
+                    "-target-feature", "-Xclang", "-packed-fp32-ops", src, "-o", lib], check=True,
+                   stdout=subprocess.DEVNULL, stderr=subprocess.DEVNULL)
+    P = ctypes.CDLL(lib)
+    P.probe.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_long, ctypes.c_void_p, ctypes.c_void_p]
     R = max(1, args.replicas)
     g = torch.Generator(device=dev)
     g.manual_seed(5005)
     xs = [torch.rand((rows, v), generator=g, device=dev) for _ in range(R)]
     dst = torch.empty_like(xs[0])
-    acc = torch.empty((), device=dev)
+    sink = torch.zeros(4096, device=dev)
     nbytes = 4 * rows * v
-    reps = max(2, args.steps // 8)
-    sum_ms = graph_ms(lambda i: torch.sum(xs[i % R], out=acc), k=8, reps=reps)
-    copy_ms = graph_ms(lambda i: dst.copy_(xs[i % R]), k=8, reps=reps)
-    out = {"metric": "plain HBM reads of the benchmark's row bytes", "bytes_per_launch": nbytes,
-           "sum_us": round(sum_ms * 1e3, 2), "sum_GBps": round(nbytes / (sum_ms * 1e-3) / 1e9, 1),
-           "copy_us": round(copy_ms * 1e3, 2),
-           "copy_read_GBps": round(nbytes / (copy_ms * 1e-3) / 1e9, 1),
-           "copy_read_write_GBps": round(2 * nbytes / (copy_ms * 1e-3) / 1e9, 1),
-           "peak_GBps": HBM_PEAK_GBS}
+    reps = max(8, args.steps)
+
+    def stream():
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+    kinds = {"rows_read": 0, "rows_chunks": 1, "rows_split_2x512": 2, "rows_split_4x256": 3, "grid_read": 4}
+    probe_ms = {name: graph_ms(lambda i, kd=kd: P.probe(kd, xs[i % R].data_ptr(), rows, v, sink.data_ptr(), stream()),
+                               k=8, reps=max(2, reps // 8)) for name, kd in kinds.items()}
+
+    def eager_ms(fn):
+        for i in range(4):
+            fn(i)
+        torch.cuda.synchronize()
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for i in range(reps):
+            fn(i)
+        s1.record()
+        torch.cuda.synchronize()
+        return s0.elapsed_time(s1) / reps
+
+    sum_ms = eager_ms(lambda i: torch.sum(xs[i % R]))
+    copy_ms = eager_ms(lambda i: dst.copy_(xs[i % R]))
+
+    def gbs(ms, k=1):
+        return round(k * nbytes / (ms * 1e-3) / 1e9, 1)
+
+    out = {"metric": "plain HBM reads of the benchmark's row bytes", "bytes_per_launch": nbytes}
+    for name, ms in probe_ms.items():
+        out[name + "_us"] = round(ms * 1e3, 2)
+        out[name + "_GBps"] = gbs(ms)
+    out.update({"torch_sum_us": round(sum_ms * 1e3, 2), "torch_sum_GBps": gbs(sum_ms),
+                "copy_us": round(copy_ms * 1e3, 2), "copy_read_write_GBps": gbs(copy_ms, 2),
+                "peak_GBps": HBM_PEAK_GBS})
     print(json.dumps(out), flush=True)
 
 

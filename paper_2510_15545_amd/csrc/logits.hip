@@ -185,27 +185,11 @@ __device__ __forceinline__ void lane_weights(const uint64_t *tab, const uint32_t
     }
 }
 
-// v plus v shifted across lanes by a DPP control (32 bits; lanes without a source add 0)
-template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ uint32_t dpp_add32(uint32_t v) {
-    return v + __builtin_amdgcn_update_dpp(0u, v, CTRL, ROW_MASK, 0xF, true);
-}
-
-__device__ __forceinline__ uint32_t wave_total32(uint32_t v) {  // valid in lane 63
-    v = dpp_add32<0x111, 0xF>(v);  // row_shr:1
-    v = dpp_add32<0x112, 0xF>(v);  // row_shr:2
-    v = dpp_add32<0x114, 0xF>(v);  // row_shr:4
-    v = dpp_add32<0x118, 0xF>(v);  // row_shr:8
-    v = dpp_add32<0x142, 0xA>(v);  // row_bcast:15
-    v = dpp_add32<0x143, 0xC>(v);  // row_bcast:31
-    return v;
-}
-
 // The wave's total of per-lane sums of 16 weights (each at most 2^35), in lane 63: the low 20
 // and the high 15 bits are summed as 32-bit values (64 of them stay below 2^26 and 2^21).
 __device__ __forceinline__ uint64_t chunk_total(uint64_t a) {
-    const uint32_t lo = wave_total32((uint32_t)a & 0xFFFFFu);
-    const uint32_t hi = wave_total32((uint32_t)(a >> 20));
+    const uint32_t lo = vcore::wave_scan32((uint32_t)a & 0xFFFFFu);
+    const uint32_t hi = vcore::wave_scan32((uint32_t)(a >> 20));
     return ((uint64_t)hi << 20) + lo;
 }
 

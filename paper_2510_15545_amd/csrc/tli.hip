@@ -365,7 +365,7 @@ __global__ void __launch_bounds__(kThreads) verify_tli_row(TliVerifyParams p) {
         }
         while (c < nc) {
             uint64_t acc = residual_sum16(pv, gv, S_r, c * vcore::kChunk + lane * 16, a.v_t);
-            acc = vcore::wave_inclusive_scan(acc);
+            acc = vcore::wave_total(acc);
             if (lane == kWave - 1) sh_part[c] = acc;
             c = cn;
             if (c < nc) {
