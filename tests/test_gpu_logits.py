@@ -194,3 +194,25 @@ def test_logits_lse_residual_at_a_scaled_exponent_just_below_zero():
     assert np.array_equal(o_nacc, np.zeros(n))
     _, tok, z = oracle.verify_logits(V, ids, off, q, bits, np.full(n, it, np.float32), ua, us, max_m=1, lse=lse)
     assert np.array_equal(z, np.full(n, 10)) and np.array_equal(tok, 20 + np.floor(us.astype(np.float64) * 10))
+
+
+@pytest.mark.parametrize("with_lse", [False, True])
+def test_logits_at_the_row_limit(with_lse):
+    """Rows of 2^23 bf16 logits (8,192 chunks: 64 KiB of chunk sums beside the 64 KiB weight
+    table in LDS), with and without normalisers, against the oracle."""
+    print(f"[case] logits V=2^23 lse={with_lse}", flush=True)
+    V = 1 << 23
+    rng = np.random.default_rng(52)
+    n = 2
+    Ms = np.array([1, 0])
+    off = np.array([0, 1, 1], np.int32)
+    x = rng.standard_normal((3, V), dtype=np.float32) * np.float32(3)
+    ids = np.array([int(rng.integers(0, V))], np.int32)
+    x[0, ids[0]] = x[0].max() + 1.0  # accepted often: the bonus row is reached as well
+    bits = bf16_bits(x)
+    q = np.float32([0.3])
+    it = np.float32([1.0 / 0.7, 1.0])
+    ua = np.float32([0.5])
+    us = np.float32([0.25, 0.75])
+    case = (ids, off, q, bits, it, ua, us, Ms)
+    run_both(V, case, 1, lse=case_lse(V, case) if with_lse else None)

@@ -289,3 +289,25 @@ def test_fused_tli_at_the_benchmark_vocabulary_sizes():
     want = oracle_tli(c, 4)
     for got in (fused(c, 4), fused(c, 4, intersected_mass(c)), two_calls(c, 4)):
         assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
+
+
+@pytest.mark.parametrize("v_t", [1 << 21, (1 << 21) + 1])
+def test_fused_tli_at_the_row_limit(v_t):
+    """Target rows of 2^21 floats (2,048 chunks: the chunk sums fill the kernel's LDS) match the
+    oracle; one float more is refused with TT_EUNSUPPORTED before anything runs."""
+    import paper_2510_15545_amd as tt
+
+    print(f"[case] fused tli v_t={v_t}", flush=True)
+    rng = np.random.default_rng(51)
+    if v_t > 1 << 21:
+        c = tli_case(rng, 300, 50, 2, 1)
+        d2t, t2d = random_maps(rng, 300, v_t, 0.001)
+        c.update(d2t=d2t, t2d=t2d, v_t=v_t, pt=np.zeros((int(c["off"][-1]) + 2, v_t), np.float32))
+        with pytest.raises(tt.TTError) as e:
+            fused(c, 1)
+        assert e.value.status == tt.TT_EUNSUPPORTED
+        return
+    c = tli_case(rng, 4000, v_t, 3, 2, frac=0.5)
+    want = oracle_tli(c, 2)
+    for got in (fused(c, 2), fused(c, 2, intersected_mass(c))):
+        assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
