@@ -867,6 +867,13 @@ def main_tli(args):
     t_gen = time.time()
     W = tli_workload(dev, args.streams or 256, 8)
     d2t, t2d, ys, off, q, p, mass, ua, us = (W[k] for k in ("d2t", "t2d", "ys", "off", "q", "p", "mass", "ua", "us"))
+    # consecutive steps read different copies of the draft and target rows (as in the default
+    # benchmark), so the Infinity Cache cannot serve a step from the one before
+    R = max(1, args.replicas)
+    qs, ps = [q], [p]
+    for _ in range(R - 1):
+        qs.append(q.clone())
+        ps.append(p.clone())
     n, M, nt, v_t, inter = W["n"], W["M"], W["nt"], W["v_t"], W["inter"]
     v_d = W["v_d"]
     torch.cuda.synchronize()
@@ -876,14 +883,14 @@ def main_tli(args):
     outs = {}
 
     def fused(with_mass):
-        return lambda i: tt.verify_tli(d2t, t2d, ys, off, q, p, ua, us, M, draft_mass=mass if with_mass else None,
-                                       out=(nacc, tok))
+        return lambda i: tt.verify_tli(d2t, t2d, ys, off, qs[i % R], ps[i % R], ua, us, M,
+                                       draft_mass=mass if with_mass else None, out=(nacc, tok))
     qbuf = torch.empty((nt, v_t), dtype=torch.float32, device=dev)
     ws = tt.verify_workspace(n, v_t, dev)
 
     def two_calls(i):
-        tt.tli_proposal(d2t, t2d, q, out=qbuf)
-        tt.verify_dense(v_t, ys, off, qbuf, p, ua, us, M, workspace=ws, out=(nacc, tok, None))
+        tt.tli_proposal(d2t, t2d, qs[i % R], out=qbuf)
+        tt.verify_dense(v_t, ys, off, qbuf, ps[i % R], ua, us, M, workspace=ws, out=(nacc, tok, None))
 
     times = {}
     for name, fn in (("fused_with_mass", fused(True)), ("fused", fused(False)), ("two_calls", two_calls)):
@@ -911,7 +918,7 @@ def main_tli(args):
         "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32+i64", "data": "synthetic",
         "config": {"workload": f"{n} streams x M={M}, V_d={v_d}, V_t={v_t}, intersection {inter}", "streams": n,
-                   "draft_tokens_per_step": nt, "path": "tt_verify_tli with the drafter's masses",
+                   "draft_tokens_per_step": nt, "path": "tt_verify_tli with the drafter's masses", "replicas": R,
                    "launch": "hip-graph of %d steps" % max(1, min(args.graph_steps, 8))},
         "accept": {"mean_gamma": round(float(acc_m.mean()), 3), "rejected_streams": int((acc_m < M).sum())},
         "us_per_step": {k: round(v * 1e3, 2) for k, v in times.items()},
