@@ -57,6 +57,8 @@ KERNEL_SOURCES = {
     "step_fused": ("step.hip", "dtw_rows.h", "dtw_common.h", "verify_core.h"),
     "verify_row": ("verify.hip", "verify_core.h"),
     "dtw_band": ("dtw.hip", "dtw_common.h"),
+    "verify_logits_row": ("logits.hip", "verify_core.h"),
+    "verify_tli_row": ("tli.hip", "verify_core.h"),
 }
 # int32 VALU issue peak of MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (a wave64 instruction
 # occupies its SIMD four cycles), in lane-operations per second
@@ -81,6 +83,20 @@ def read_counters(path, workload, kernel):
     if kv.get("source_sha256") != source_digest(KERNEL_SOURCES[kernel]):
         return None, "kernel changed since the counters were taken"
     return kv, ""
+
+
+def copy_calibration(args, dev):
+    """With --copy-calib-mb: one plain device-to-device copy of that many MiB after the timed
+    calls, whose counter readings scale a kernel's FETCH_SIZE and WRITE_SIZE to bytes."""
+    import torch
+
+    if not args.copy_calib_mb:
+        return
+    src = torch.empty(args.copy_calib_mb * (1 << 20) // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
 
 
 def read_traffic(path, workload, kernel):
@@ -361,12 +377,7 @@ def main():
               "align": lambda i: do_align(), "transfer": lambda i: do_transfer()}[args.only]
         kernel_ms(fn, 200)
 
-    if args.copy_calib_mb:
-        src = torch.empty(args.copy_calib_mb * (1 << 20) // 4, dtype=torch.float32, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
+    copy_calibration(args, dev)
 
     # ---- derived metrics
     Ka = np.diff(A.draft_off)
@@ -524,12 +535,7 @@ def main_dense(args):
     ms = s0.elapsed_time(s1) / (reps * gs)
     step(0)
     torch.cuda.synchronize()
-    if args.copy_calib_mb:
-        src = torch.empty(args.copy_calib_mb * (1 << 20) // 4, dtype=torch.float32, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
+    copy_calibration(args, dev)
     acc = nacc.cpu().numpy()
     m = np.diff(D.off)
     # algorithmic bytes: the target row of every stream, the draft row of every rejected
@@ -893,11 +899,27 @@ def main_tli(args):
         tt.verify_dense(v_t, ys, off, qbuf, ps[i % R], ua, us, M, workspace=ws, out=(nacc, tok, None))
 
     times = {}
-    for name, fn in (("fused_with_mass", fused(True)), ("fused", fused(False)), ("two_calls", two_calls)):
+    # --eager (profiler passes): only the fused call with the drafter's masses, launched one by one
+    runs = (("fused_with_mass", fused(True)),) if args.eager else \
+        (("fused_with_mass", fused(True)), ("fused", fused(False)), ("two_calls", two_calls))
+    for name, fn in runs:
         fn(0)
         torch.cuda.synchronize()
         outs[name] = (nacc.cpu().numpy().copy(), tok.cpu().numpy().copy())
-        times[name] = graph_ms(fn, k=max(1, min(args.graph_steps, 8)), reps=max(2, args.steps // 8))
+        if args.eager:
+            reps = max(2, args.steps)
+            s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s0.record()
+            for i in range(reps):
+                fn(i)
+            s1.record()
+            torch.cuda.synchronize()
+            times[name] = s0.elapsed_time(s1) / reps
+        else:
+            times[name] = graph_ms(fn, k=max(1, min(args.graph_steps, 8)), reps=max(2, args.steps // 8))
+    copy_calibration(args, dev)
+    if "fused" not in outs:
+        outs["fused"] = outs["fused_with_mass"]
     # the drafter's S here is an fp32 sum, not the exact intersected mass the kernel forms without
     # it, so that run is compared with the others only through its acceptance counts
     acc = outs["fused"][0]
@@ -910,6 +932,9 @@ def main_tli(args):
     kbytes = int(24 * tested + n * (4 * v_t + 12) + rejected * 4 * inter + 4 * v_t)
     gbs = kbytes / (ms * 1e-3) / 1e9
     acc_m = outs["fused_with_mass"][0]
+    wl_name = f"{n} streams x M={M}, V_d={v_d}, V_t={v_t}, intersection {inter}"
+    traffic, note = read_traffic(args.traffic or os.path.join(ROOT, "profiles", "verify_tli_row_counters.txt"),
+                                 wl_name, "verify_tli_row")
     result = {
         "metric": "verified draft tokens/s, TLI proposals (App. D Alg. 3 + 4) at V_d=128,256 / V_t=151,936; "
                   "HBM GB/s vs peak",
@@ -917,17 +942,18 @@ def main_tli(args):
         "steps": max(2, args.steps // 8) * max(1, min(args.graph_steps, 8)), "warmup": 1,
         "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32+i64", "data": "synthetic",
-        "config": {"workload": f"{n} streams x M={M}, V_d={v_d}, V_t={v_t}, intersection {inter}", "streams": n,
+        "config": {"workload": wl_name, "streams": n,
                    "draft_tokens_per_step": nt, "path": "tt_verify_tli with the drafter's masses", "replicas": R,
-                   "launch": "hip-graph of %d steps" % max(1, min(args.graph_steps, 8))},
+                   "launch": "eager" if args.eager else "hip-graph of %d steps" % max(1, min(args.graph_steps, 8))},
         "accept": {"mean_gamma": round(float(acc_m.mean()), 3), "rejected_streams": int((acc_m < M).sum())},
         "us_per_step": {k: round(v * 1e3, 2) for k, v in times.items()},
-        "same_outputs_fused_and_two_calls": bool(np.array_equal(outs["fused"][0], outs["two_calls"][0]) and
-                                                 np.array_equal(outs["fused"][1], outs["two_calls"][1])),
+        "same_outputs_fused_and_two_calls": None if "two_calls" not in outs else bool(
+            np.array_equal(outs["fused"][0], outs["two_calls"][0]) and
+            np.array_equal(outs["fused"][1], outs["two_calls"][1])),
         "with_mass_acceptance_agreement": round(float((acc_m == acc).mean()), 4),
         "roofline": {"kernel": "verify_tli_row", "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                     "traffic_note": "no counters for this kernel", "algorithmic_bytes_per_launch": kbytes,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "traffic_note": note, "algorithmic_bytes_per_launch": kbytes,
                      "launch_us": round(ms * 1e3, 2)},
         "gen_seconds": round(t_gen, 1),
     }
@@ -1020,6 +1046,7 @@ def main_logits(args):
     ms = s0.elapsed_time(s1) / (reps * gs)
     step(0)
     torch.cuda.synchronize()
+    copy_calibration(args, dev)
     acc = nacc.cpu().numpy()
     if lse is None:
         # algorithmic bytes: each row a stream reads (rows 0 .. gamma, once), t_j, q_j, u_j per
@@ -1035,19 +1062,22 @@ def main_logits(args):
     gbs = kbytes / (ms * 1e-3) / 1e9
     elems_per_s = V * rows_read / (ms * 1e-3)
     draft_tokens = int(S.draft_off[-1])
+    wl_name = f"{n} streams V_t={V} bf16 logits T=0.7 30% forced" + (" with row log-sum-exp" if lse is not None else "")
+    traffic, note = read_traffic(args.traffic or os.path.join(
+        ROOT, "profiles", "verify_logits_row" + ("_lse" if lse is not None else "") + "_counters.txt"),
+        wl_name, "verify_logits_row")
     result = {
         "metric": "verified draft tokens/s from bf16 logits (T=0.7) at V_t=151,936; HBM GB/s vs peak",
         "value": round(draft_tokens / (ms * 1e-3), 1), "unit": "draft tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16+f32+i64", "data": "synthetic",
-        "config": {"workload": f"{n} streams V_t={V} bf16 logits T=0.7 30% forced" +
-                   (" with row log-sum-exp" if lse is not None else ""), "streams": n,
+        "config": {"workload": wl_name, "streams": n,
                    "target_positions": int(m.sum()), "v_t": V, "replicas": R, "path": "tt_verify_logits" + ("+lse" if lse is not None else ""),
                    "launch": "eager" if args.eager else "hip-graph of %d steps" % gs},
         "accept": {"mean_gamma": round(float(acc.mean()), 3), "rows_read": rows_read},
         "roofline": {"kernel": "verify_logits_row", "bound": "hbm", "achieved": round(gbs, 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                     "traffic_note": "no counters for this kernel", "algorithmic_bytes_per_launch": kbytes,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "traffic_note": note, "algorithmic_bytes_per_launch": kbytes,
                      "launch_us": round(ms * 1e3, 2), "logits_per_s": round(elems_per_s, 1)},
         "gen_seconds": round(t_gen, 1),
     }

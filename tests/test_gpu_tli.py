@@ -267,6 +267,21 @@ def test_fused_tli_verification_matches_the_two_calls_and_the_oracle(v_d, v_t, N
         assert np.all(n2[over] == -1) and np.all(t2[over] == -1)
 
 
+@pytest.mark.parametrize("v_d,v_t,frac", [(128256, 60000, 0.9), (1200000, 5000, 0.5)])
+def test_fused_tli_dense_and_wide_draft_vocabularies(v_d, v_t, frac):
+    """A dense intersection (54,000 of V_d = 128,256 ids: most lanes gather) and a draft
+    vocabulary of 1.2 M ids, bit for bit against the oracle, with S formed in the kernel and
+    passed in."""
+    print(f"[case] fused tli dense/wide v_d={v_d} v_t={v_t} frac={frac}", flush=True)
+    rng = np.random.default_rng(v_d + v_t)
+    c = tli_case(rng, v_d, v_t, 3, 2, frac=frac)
+    want = oracle_tli(c, 2)
+    for got in (fused(c, 2), fused(c, 2, intersected_mass(c))):
+        assert np.array_equal(got[0], want[0]), np.nonzero(got[0] != want[0])[0][:5]
+        assert np.array_equal(got[1], want[1]), np.nonzero(got[1] != want[1])[0][:5]
+    assert (want[0] < c["Ms"]).any()  # a residual row is sampled
+
+
 def test_fused_tli_with_the_drafters_mass():
     """S_j taken as given (App. D Alg. 3 normalises q' on the draft side): masses off the
     intersected sum by up to a factor of two either way, and zero or NaN masses (q' = 0)."""
