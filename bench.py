@@ -1154,6 +1154,16 @@ def dtw_stress(dev, w):
                   k=10, reps=5)
     K, M = np.diff(wl.draft_off), np.diff(wl.target_off)
     cells = band_cells(K, M, w)
+    # the step before the alignment on the same pairs: draft ids -> proxy target ids (greedy
+    # longest match); the token index is built once, outside the timing
+    idx = tt.token_index(vt)
+    maxb = int(max(np.add.reduceat(np.diff(wl.vocab_d.offsets)[wl.draft_ids], wl.draft_off[:-1])))
+    rt = (torch.empty(wl.n * wl.max_m, dtype=torch.int32, device=dev), torch.empty(wl.n + 1, dtype=torch.int32, device=dev))
+    tt.retokenize(vd, vt, idx, di, do, maxb, wl.max_m, out=rt)
+    torch.cuda.synchronize()
+    rt_ok = bool(np.array_equal(rt[1].cpu().numpy(), wl.target_off) and
+                 np.array_equal(rt[0].cpu().numpy()[:int(wl.target_off[-1])], wl.target_ids))
+    ms_rt = graph_ms(lambda i: tt.retokenize(vd, vt, idx, di, do, maxb, wl.max_m, out=rt), k=10, reps=5)
     kv, why = read_counters(os.path.join(ROOT, "profiles", "dtw_band_counters.txt"), wl.spec.name, "dtw_band")
     issue = None
     if kv is not None:  # wave instructions over the 1,024 SIMDs' issue slots (one per 4 cycles)
@@ -1164,6 +1174,9 @@ def dtw_stress(dev, w):
             "valu_issue_frac": None if issue is None else round(issue, 4),
             "lds_bank_conflict_rate": None if kv is None else float(kv["lds_bank_conflict_rate"]),
             "counter_note": why or "dtw_band SQ_INSTS_VALU per launch over the tt_align call's time",
+            "tt_retokenize_us": round(ms_rt * 1e3, 2),
+            "retokenize_bytes": int((np.diff(wl.vocab_d.offsets)[wl.draft_ids]).sum()),
+            "retokenize_matches_workload": rt_ok,
             "gen_seconds": round(gen, 1)}
 
 

@@ -320,8 +320,9 @@ int tt_delta_quantile(const int32_t *hist, int32_t n_bins, int32_t num, int32_t 
 /*
  * Token index for longest-match lookups in a vocabulary (used by tt_retokenize for
  * the target vocabulary).  tt_token_index_size gives its bytes for n_tokens
- * (16 bytes per hash slot, a power of two >= 4 * n_tokens slots); n_tokens in
- * [1, 2^28].  tt_token_index_build fills `index` (device, 16-byte aligned, at
+ * (16 bytes per hash slot, a power of two >= 4 * n_tokens slots, then a filter of
+ * 2 bits per slot that lets a lookup skip most byte strings that are no token);
+ * n_tokens in [1, 2^28].  tt_token_index_build fills `index` (device, 16-byte aligned, at
  * least that many bytes, owned by the caller) from the table `v` in three kernels
  * on `stream`; tokens of length 0 or above v->max_token_bytes are left out, and of
  * several tokens with the same bytes only the lowest id can be found.  The index

@@ -31,7 +31,7 @@ int main(void) {
     EXPECT(tt_align_workspace_size(1024, 512, 512, 8, 8, &n) == TT_OK && n > 0);
     EXPECT(tt_align_workspace_size(8, 4096, 4096, -1, 16, &n) == TT_EUNSUPPORTED);
     EXPECT(tt_step_workspace_size(256, 151936, 8, 30, 8, 8, &n) == TT_OK);
-    EXPECT(tt_token_index_size(151936, &n) == TT_OK && n == 16u * (1u << 20));
+    EXPECT(tt_token_index_size(151936, &n) == TT_OK && n == 16u * (1u << 20) + (1u << 20) / 4u);
     EXPECT(tt_retokenize_workspace_size(4, 0, &n) == TT_EINVAL);
 
     tt_vocab v = {(const uint8_t *)0x1000, D, 10, 8};

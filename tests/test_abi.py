@@ -112,8 +112,9 @@ def test_invalid_arguments_return_before_launch():
 
     n = ctypes.c_size_t(0)
     assert L.tt_token_index_size(0, ctypes.byref(n)) == tt.TT_EINVAL
-    assert L.tt_token_index_size(1000, ctypes.byref(n)) == 0 and n.value == 16 * 4096
-    assert L.tt_token_index_size(151936, ctypes.byref(n)) == 0 and n.value == 16 * (1 << 20)
+    # 16-byte slots (a power of two >= 4 x the tokens) and a filter of 2 bits per slot
+    assert L.tt_token_index_size(1000, ctypes.byref(n)) == 0 and n.value == 16 * 4096 + 4096 // 4
+    assert L.tt_token_index_size(151936, ctypes.byref(n)) == 0 and n.value == 16 * (1 << 20) + (1 << 20) // 4
     assert L.tt_token_index_build(ctypes.byref(big), dummy, 1 << 30, None) == tt.TT_EUNSUPPORTED
     assert L.tt_token_index_build(ctypes.byref(v), P(0x1004), 1 << 30, None) == tt.TT_EINVAL  # not 16-byte aligned
     assert L.tt_token_index_build(ctypes.byref(v), dummy, 16, None) == tt.TT_EWORKSPACE
