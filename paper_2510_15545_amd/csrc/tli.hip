@@ -181,8 +181,11 @@ __global__ void __launch_bounds__(kThreads) tli_rows(TliArgs a, int vec_in, int 
 //     from draft_mass (wave 0 tests 64 positions per ballot) or, without it, by a pass over
 //     draft row j (the whole workgroup, row after row until the first rejection);
 //   residual: the chunk sums of max(0, p - q') over target row gamma, q' gathered through t2d
-//     from draft row gamma (the bonus row as is after full acceptance), then the exact
-//     inverse-CDF sample by wave 0 -- the arithmetic of tt_verify_dense element for element.
+//     from draft row gamma (the bonus row as is after full acceptance), the row read in
+//     vcore::load_chunk's element order (a 16-byte load instruction covers 1 KB; a chunk's sum
+//     does not depend on the order), then the exact inverse-CDF sample by wave 0, which reads
+//     the crossing chunk again in position order -- the arithmetic of tt_verify_dense element
+//     for element.
 constexpr int kWaves = kThreads / kWave;
 
 struct TliVerifyParams {
@@ -207,7 +210,7 @@ __device__ __forceinline__ void load_x(const TliVerifyArgs &a, int x0, bool vec,
     }
 }
 
-// Their target probabilities (0 past v_t) and ids.
+// Their target probabilities (0 past v_t) and ids (the sampler's crossing chunk, in position order).
 __device__ __forceinline__ void load_px(const TliVerifyArgs &a, const float *prow, int x0, bool vec, float (&pv)[16],
                                         int32_t (&xs)[16]) {
     vcore::read16(prow, x0, a.v_t, vec, pv);
@@ -222,15 +225,6 @@ __device__ __forceinline__ void gather16(const TliVerifyArgs &a, const float *dr
     for (int k = 0; k < 16; ++k) gv[k] = (drow != nullptr && xs[k] >= 0 && xs[k] < a.v_d) ? drow[xs[k]] : 0.0f;
 }
 
-// The Q62 sum of the 16 residual entries q62(clamp01(p - q')) (q' = qprime(g, S); 0 past v_t).
-__device__ __forceinline__ uint64_t residual_sum16(const float (&pv)[16], const float (&gv)[16], float S, int x0,
-                                                   int vt) {
-    uint64_t sum = 0;
-#pragma unroll
-    for (int k = 0; k < 16; ++k) sum += x0 + k < vt ? q62(clamp01(pv[k] - qprime(gv[k], S))) : 0ull;
-    return sum;
-}
-
 // Q62 residual entries q62(clamp01(p - q')) of the 16 elements (q' = qprime(g, S); 0 past v_t,
 // where p = g = 0).
 __device__ __forceinline__ uint64_t residual16(const float (&pv)[16], const float (&gv)[16], float S, int x0, int vt,
@@ -240,6 +234,43 @@ __device__ __forceinline__ uint64_t residual16(const float (&pv)[16], const floa
     for (int k = 0; k < 16; ++k) {
         qv[k] = x0 + k < vt ? q62(clamp01(pv[k] - qprime(gv[k], S))) : 0ull;
         sum += qv[k];
+    }
+    return sum;
+}
+
+// The row pass in vcore::load_chunk's element order (lane l holds elements 256 u + 4 l + j of a
+// chunk, so each 16-byte load instruction covers 1 KB of the row): the target probabilities
+// with the non-temporal hint, the 16 ids t2d in the same order (-1 past v_t).
+__device__ __forceinline__ void load_px_strided(const TliVerifyArgs &a, const float *prow, int c, bool vec,
+                                                float4 (&pv)[4], int32_t (&xs)[16]) {
+    const int lane = threadIdx.x % kWave;
+    const int xb = c * vcore::kChunk;
+    vcore::load_chunk(prow, xb, lane, a.v_t, vec, pv);
+    if (vec && xb + vcore::kChunk <= a.v_t) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int4 t = *reinterpret_cast<const int4 *>(a.t2d + xb + u * 256 + lane * 4);
+            xs[4 * u] = t.x;
+            xs[4 * u + 1] = t.y;
+            xs[4 * u + 2] = t.z;
+            xs[4 * u + 3] = t.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            const int y = xb + (k >> 2) * 256 + lane * 4 + (k & 3);
+            xs[k] = y < a.v_t ? a.t2d[y] : -1;
+        }
+    }
+}
+
+// Q62 sum of the 16 residual entries in that order (p = g = 0 past v_t gives 0).
+__device__ __forceinline__ uint64_t residual_sum_strided(const float4 (&pv)[4], const float (&gv)[16], float S) {
+    uint64_t sum = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        sum += q62(clamp01(pv[u].x - qprime(gv[4 * u], S))) + q62(clamp01(pv[u].y - qprime(gv[4 * u + 1], S))) +
+               q62(clamp01(pv[u].z - qprime(gv[4 * u + 2], S))) + q62(clamp01(pv[u].w - qprime(gv[4 * u + 3], S)));
     }
     return sum;
 }
@@ -354,26 +385,27 @@ __global__ void __launch_bounds__(kThreads) verify_tli_row(TliVerifyParams p) {
     {
         // each wave: chunk c's probabilities and draft masses, chunk cn's probabilities and ids
         // in flight behind them (a chunk's gathers wait for its ids only)
-        float pv[16], gv[16], pn[16];
+        float4 pv[4], pn[4];
+        float gv[16];
         int32_t xs[16];
         int c = wave, cn = nc;
         if (c < nc) {
-            load_px(a, prow, c * vcore::kChunk + lane * 16, vec, pv, xs);
+            load_px_strided(a, prow, c, vec, pv, xs);
             gather16(a, drow, xs, gv);
             cn = vcore::next_chunk(&sh_ctr, c, kWaves);
-            if (cn < nc) load_px(a, prow, cn * vcore::kChunk + lane * 16, vec, pn, xs);
+            if (cn < nc) load_px_strided(a, prow, cn, vec, pn, xs);
         }
         while (c < nc) {
-            uint64_t acc = residual_sum16(pv, gv, S_r, c * vcore::kChunk + lane * 16, a.v_t);
+            uint64_t acc = residual_sum_strided(pv, gv, S_r);
             acc = vcore::wave_total(acc);
             if (lane == kWave - 1) sh_part[c] = acc;
             c = cn;
             if (c < nc) {
 #pragma unroll
-                for (int k = 0; k < 16; ++k) pv[k] = pn[k];
+                for (int u = 0; u < 4; ++u) pv[u] = pn[u];
                 gather16(a, drow, xs, gv);
                 cn = vcore::next_chunk(&sh_ctr, c, kWaves);
-                if (cn < nc) load_px(a, prow, cn * vcore::kChunk + lane * 16, vec, pn, xs);
+                if (cn < nc) load_px_strided(a, prow, cn, vec, pn, xs);
             }
         }
     }
