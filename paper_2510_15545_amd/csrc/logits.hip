@@ -114,6 +114,46 @@ __device__ __forceinline__ void load16(const uint16_t *row, int x0, int v, bool 
     }
 }
 
+// The 16 bf16 a lane takes of chunk c in the row passes: elements 512 u + 8 lane + j (u < 2,
+// j < 8), so that each of the two 16-byte load instructions covers 1 KB of the row (16
+// consecutive logits a lane would make each span 2 KB); 0 past v.  NT: the non-temporal hint
+// (the row's last read).  A chunk's sums and maximum do not depend on the order.
+template <bool NT>
+__device__ __forceinline__ void load16s(const uint16_t *row, int c, int lane, int v, bool vec, uint32_t (&w)[8]) {
+    const int xb = c * kChunk;
+    if (vec && xb + kChunk <= v) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const uint4 *src = reinterpret_cast<const uint4 *>(row + xb + u * 512 + lane * 8);
+            uint4 t;
+            if constexpr (NT) {
+                typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+                const u4v q = __builtin_nontemporal_load(reinterpret_cast<const u4v *>(src));
+                t = make_uint4(q.x, q.y, q.z, q.w);
+            } else {
+                t = *src;
+            }
+            w[4 * u] = t.x;
+            w[4 * u + 1] = t.y;
+            w[4 * u + 2] = t.z;
+            w[4 * u + 3] = t.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int x = xb + (k >> 2) * 512 + lane * 8 + 2 * (k & 3);
+            const uint32_t lo = x < v ? row[x] : 0u;
+            const uint32_t hi = x + 1 < v ? row[x + 1] : 0u;
+            w[k] = lo | (hi << 16);
+        }
+    }
+}
+
+// Index of element k (0..15) of a lane's 16 in chunk c, in load16s's order.
+__device__ __forceinline__ int elem_index_s(int c, int lane, int k) {
+    return c * kChunk + (k >> 3) * 512 + lane * 8 + (k & 7);
+}
+
 // bf16 element k (0..15) of a lane's 16
 __device__ __forceinline__ uint32_t elem(const uint32_t (&w)[8], int k) {
     return (k & 1) ? (w[k >> 1] >> 16) : (w[k >> 1] & 0xFFFFu);
@@ -185,6 +225,24 @@ __device__ __forceinline__ void lane_weights(const uint64_t *tab, const uint32_t
     }
 }
 
+// As lane_weights for a lane's 16 logits of chunk c in load16s's order.
+__device__ __forceinline__ void lane_weights_s(const uint64_t *tab, const uint32_t (&w)[8], int c, int v, float sc,
+                                               float b31, uint64_t (&e)[16]) {
+    const int lane = threadIdx.x % kWave;
+    uint64_t any = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const uint32_t o = tab_offsets(w[k]);
+        e[2 * k] = elem_index_s(c, lane, 2 * k) < v ? tab_at(tab, o & 0xFFFFu) : 0u;
+        e[2 * k + 1] = elem_index_s(c, lane, 2 * k + 1) < v ? tab_at(tab, o >> 16) : 0u;
+        any |= e[2 * k] | e[2 * k + 1];
+    }
+    if (any >= kSentinel) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) e[k] = elem_index_s(c, lane, k) < v ? e31_at(expo(elem(w, k), sc, b31)) : 0u;
+    }
+}
+
 // The wave's total of per-lane sums of 16 weights (each at most 2^35), in lane 63: the low 20
 // and the high 15 bits are summed as 32-bit values (64 of them stay below 2^26 and 2^21).
 __device__ __forceinline__ uint64_t chunk_total(uint64_t a) {
@@ -203,19 +261,18 @@ __device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, b
     uint32_t w[8] = {}, nx[8] = {};
     int c = wave, cn = nc, cnn = nc;  // chunk summed, chunk in flight, the one after it
     if (c < nc) {
-        load16(row, c * kChunk + lane * 16, v, vec, w);
+        load16s<true>(row, c, lane, v, vec, w);
         cn = vcore::next_chunk(next, c, kWaves);
         if (cn < nc) {
-            load16(row, cn * kChunk + lane * 16, v, vec, nx);
+            load16s<true>(row, cn, lane, v, vec, nx);
             cnn = vcore::next_chunk(next, cn, kWaves);
         }
     }
     build_table(tab, sc, b31);
     __syncthreads();
     while (c < nc) {
-        const int x0 = c * kChunk + lane * 16;
         uint64_t acc = 0;
-        if (x0 + 16 <= v) {
+        if ((c + 1) * kChunk <= v) {
 #pragma unroll
             for (int k = 0; k < 8; ++k) {
                 const uint32_t o = tab_offsets(w[k]);
@@ -228,7 +285,7 @@ __device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, b
             }
         } else {  // the row's ragged end
             uint64_t e[16];
-            lane_weights(tab, w, x0, v, sc, b31, e);
+            lane_weights_s(tab, w, c, v, sc, b31, e);
 #pragma unroll
             for (int k = 0; k < 16; ++k) acc += e[k];
         }
@@ -240,7 +297,7 @@ __device__ __forceinline__ void chunk_sums(const uint16_t *row, int v, int nc, b
             for (int k = 0; k < 8; ++k) w[k] = nx[k];
             cn = cnn;
             if (cn < nc) {
-                load16(row, cn * kChunk + lane * 16, v, vec, nx);
+                load16s<true>(row, cn, lane, v, vec, nx);
                 cnn = vcore::next_chunk(next, cn, kWaves);
             }
         }
@@ -462,17 +519,16 @@ __global__ void __launch_bounds__(kThreads) verify_logits_row(LogitsParams p) {
         // pass 1: the row's largest x
         float m = -INFINITY;
         uint32_t w[8] = {}, nx[8] = {};
-        if (wave < nc) load16(row, wave * kChunk + lane * 16, v, vec, w);
+        if (wave < nc) load16s<false>(row, wave, lane, v, vec, w);
         for (int c = wave; c < nc; c += kWaves) {
-            const int x0 = c * kChunk + lane * 16;
-            if (c + kWaves < nc) load16(row, x0 + kWaves * kChunk, v, vec, nx);
-            if (x0 + 16 <= v) {
+            if (c + kWaves < nc) load16s<false>(row, c + kWaves, lane, v, vec, nx);
+            if ((c + 1) * kChunk <= v) {
 #pragma unroll
                 for (int k = 0; k < 16; ++k) m = fmaxf(m, scaled(elem(w, k), cb));
             } else {
 #pragma unroll
                 for (int k = 0; k < 16; ++k)
-                    if (x0 + k < v) m = fmaxf(m, scaled(elem(w, k), cb));
+                    if (elem_index_s(c, lane, k) < v) m = fmaxf(m, scaled(elem(w, k), cb));
             }
 #pragma unroll
             for (int k = 0; k < 8; ++k) w[k] = nx[k];
