@@ -23,7 +23,8 @@
 // (an LM head can emit them with its logits) it uses m = L and S = 1: the acceptance test
 // needs one gathered logit per position and only the residual (or bonus) row is read, once.
 // Wave 0 samples: the chunk sums lane-blocked, the crossing chunk's e31 recomputed from its
-// 1024 logits.  A lane reads 16 consecutive bf16 (two 16-byte loads).
+// 1024 logits.  In the row passes a lane reads 16 bf16 with two 16-byte loads, each load
+// instruction covering 1 KB of the row; the sampler reads 16 consecutive bf16 a lane.
 #include "verify_core.h"
 
 TT_STAMPS_TABLE(logits)
@@ -97,7 +98,7 @@ __device__ __forceinline__ float scaled(uint32_t bits16, float c) { return bf16_
 // the scaled exponent z of a logit: fma(logit, c, b31) with b31 = 31 - mu
 __device__ __forceinline__ float expo(uint32_t bits16, float c, float b31) { return fmaf(bf16_value(bits16), c, b31); }
 
-// The 16 logits of a lane in chunk c (elements c*1024 + lane*16 + k, zero bits past v).
+// 16 consecutive logits x0 .. x0 + 15 of a lane (the sampler's crossing chunk; zero bits past v).
 __device__ __forceinline__ void load16(const uint16_t *row, int x0, int v, bool vec, uint32_t (&w)[8]) {
     if (vec && x0 + 16 <= v) {
         const uint4 a = *reinterpret_cast<const uint4 *>(row + x0);
